@@ -1,0 +1,219 @@
+/*
+ * fp64 CPU oracle for the tiled Newton–Schulz map of Hierarchical Muon.
+ *
+ * TEST INFRASTRUCTURE ONLY. Only tests/, __graft_entry__.smoke() and the
+ * cpu_baseline leg of bench.py load this library. The HIP product path never
+ * links, imports or calls it, and it shares no code, header, table or helper
+ * with that path.
+ *
+ * Everything here is written straight from the paper's definitions, in
+ * double precision, with plain loops and no blocking, fusion or reordering:
+ *
+ *   Sec. 2.2, eqs. (ns_iteration), (ns_quintic), (phi_k_def):
+ *     for a nonzero H x W matrix A with H <= W,
+ *       X_0     = A / ||A||_F
+ *       X_{k+1} = (a I + b X_k X_k^T + c (X_k X_k^T)^2) X_k
+ *       Phi_K(A) = X_K
+ *     with I of size H x H. If H > W the recurrence runs on A^T and the
+ *     result is transposed back. Phi_K(0) = 0.
+ *
+ *   Sec. 2.1 (Notation) and eq. (tiling_operator): the tiling operator B_T
+ *     sets R = ceil(H/T), C = ceil(W/T), zero-pads A to (RT) x (CT) and cuts
+ *     it into an R x C grid of T x T tiles; B_T^{-1} reassembles the tiles
+ *     and drops the padding.
+ *
+ *   Sec. 4.1, eq. (tiled_ns):  Phi_{K,T}(A) = B_T^{-1}({Phi_K(A_rc)}).
+ *
+ * Every tile is therefore a full T x T (square) matrix, padding included,
+ * exactly as the definition states; no orientation choice arises for tiles.
+ * Tiles are numbered row-major over the grid: id = r*C + c.
+ *
+ * Status codes: 0 ok, -1 bad argument, -2 out of memory.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_OK 0
+#define ORACLE_BAD_ARG (-1)
+#define ORACLE_NO_MEM (-2)
+
+/* C (n x m) = P (n x q) * Q (q x m); all row-major and contiguous. */
+static void matmul(const double* P, const double* Q, double* C, int64_t n, int64_t q, int64_t m)
+{
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t j = 0; j < m; ++j) {
+            double s = 0.0;
+            for (int64_t k = 0; k < q; ++k) s += P[i * q + k] * Q[k * m + j];
+            C[i * m + j] = s;
+        }
+}
+
+/* G (n x n) = X X^T for X (n x m). */
+static void gram(const double* X, double* G, int64_t n, int64_t m)
+{
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t j = 0; j < n; ++j) {
+            double s = 0.0;
+            for (int64_t k = 0; k < m; ++k) s += X[i * m + k] * X[j * m + k];
+            G[i * n + j] = s;
+        }
+}
+
+/* Row-oriented Phi_K for n <= m: X is n x m, overwritten with Phi_K(X). */
+static int phi_k_rows(double* X, int64_t n, int64_t m, int K, double a, double b, double c)
+{
+    double nrm2 = 0.0;
+    for (int64_t i = 0; i < n * m; ++i) nrm2 += X[i] * X[i];
+    double nrm = sqrt(nrm2);
+    if (nrm == 0.0) { /* Phi_K(0) = 0 */
+        for (int64_t i = 0; i < n * m; ++i) X[i] = 0.0;
+        return ORACLE_OK;
+    }
+    for (int64_t i = 0; i < n * m; ++i) X[i] = X[i] / nrm;
+
+    double* A = (double*)malloc(sizeof(double) * n * n);  /* X X^T            */
+    double* A2 = (double*)malloc(sizeof(double) * n * n); /* (X X^T)^2        */
+    double* M = (double*)malloc(sizeof(double) * n * n);  /* aI + bA + cA^2   */
+    double* Xn = (double*)malloc(sizeof(double) * n * m); /* M X              */
+    if (!A || !A2 || !M || !Xn) {
+        free(A); free(A2); free(M); free(Xn);
+        return ORACLE_NO_MEM;
+    }
+    for (int k = 0; k < K; ++k) {
+        gram(X, A, n, m);
+        matmul(A, A, A2, n, n, n);
+        for (int64_t i = 0; i < n; ++i)
+            for (int64_t j = 0; j < n; ++j)
+                M[i * n + j] = (i == j ? a : 0.0) + b * A[i * n + j] + c * A2[i * n + j];
+        matmul(M, X, Xn, n, n, m);
+        memcpy(X, Xn, sizeof(double) * n * m);
+    }
+    free(A); free(A2); free(M); free(Xn);
+    return ORACLE_OK;
+}
+
+/*
+ * Phi_K(A) for a dense H x W matrix (row-major, leading dimension ld_in),
+ * written to Y (leading dimension ld_out). Applies the orientation rule of
+ * Sec. 2.2: when H > W the recurrence runs on A^T and is transposed back.
+ */
+int oracle_phi_k(const double* A, int64_t H, int64_t W, int64_t ld_in, int K,
+                 double a, double b, double c, double* Y, int64_t ld_out)
+{
+    if (!A || !Y || H < 1 || W < 1 || ld_in < W || ld_out < W || K < 0) return ORACLE_BAD_ARG;
+    int transpose = H > W;
+    int64_t n = transpose ? W : H, m = transpose ? H : W;
+    double* X = (double*)malloc(sizeof(double) * n * m);
+    if (!X) return ORACLE_NO_MEM;
+    for (int64_t i = 0; i < H; ++i)
+        for (int64_t j = 0; j < W; ++j) {
+            if (transpose) X[j * m + i] = A[i * ld_in + j];
+            else X[i * m + j] = A[i * ld_in + j];
+        }
+    int st = phi_k_rows(X, n, m, K, a, b, c);
+    if (st == ORACLE_OK)
+        for (int64_t i = 0; i < H; ++i)
+            for (int64_t j = 0; j < W; ++j)
+                Y[i * ld_out + j] = transpose ? X[j * m + i] : X[i * m + j];
+    free(X);
+    return st;
+}
+
+/* Number of tiles of B_T(A): R*C with R = ceil(H/T), C = ceil(W/T). */
+int64_t oracle_tile_count(int64_t H, int64_t W, int64_t T)
+{
+    if (H < 1 || W < 1 || T < 1) return -1;
+    int64_t R = (H + T - 1) / T, C = (W + T - 1) / T;
+    return R * C;
+}
+
+/*
+ * Phi_K of tile `tile_id` of B_T(A), returned as the full T x T tile Y
+ * (padding included, contiguous). The tile is cut from the zero-padded
+ * (RT) x (CT) matrix: entry (i, j) of tile (r, c) is A[rT+i][cT+j] when that
+ * lies inside A and 0 otherwise.
+ */
+int oracle_ns_tile(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t T,
+                   int64_t tile_id, int K, double a, double b, double c, double* Y)
+{
+    if (!A || !Y || H < 1 || W < 1 || ld_in < W || T < 1 || K < 0) return ORACLE_BAD_ARG;
+    int64_t R = (H + T - 1) / T, C = (W + T - 1) / T;
+    if (tile_id < 0 || tile_id >= R * C) return ORACLE_BAD_ARG;
+    int64_t r = tile_id / C, cc = tile_id % C;
+    double* S = (double*)malloc(sizeof(double) * T * T);
+    if (!S) return ORACLE_NO_MEM;
+    for (int64_t i = 0; i < T; ++i)
+        for (int64_t j = 0; j < T; ++j) {
+            int64_t gi = r * T + i, gj = cc * T + j;
+            S[i * T + j] = (gi < H && gj < W) ? A[gi * ld_in + gj] : 0.0;
+        }
+    int st = oracle_phi_k(S, T, T, T, K, a, b, c, Y, T);
+    free(S);
+    return st;
+}
+
+/*
+ * Phi_{K,T}(A), eq. (tiled_ns): every tile of B_T(A) through Phi_K, then
+ * B_T^{-1} (reassemble, drop the padding) into Y (H x W, leading dim ld_out).
+ * Tiles are independent; they are spread over OpenMP threads.
+ */
+int oracle_ns_tiled(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t T, int K,
+                    double a, double b, double c, double* Y, int64_t ld_out)
+{
+    if (!A || !Y || H < 1 || W < 1 || ld_in < W || ld_out < W || T < 1 || K < 0) return ORACLE_BAD_ARG;
+    int64_t R = (H + T - 1) / T, C = (W + T - 1) / T;
+    int status = ORACLE_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < R * C; ++t) {
+        double* Yt = (double*)malloc(sizeof(double) * T * T);
+        int st = Yt ? oracle_ns_tile(A, H, W, ld_in, T, t, K, a, b, c, Yt) : ORACLE_NO_MEM;
+        if (st == ORACLE_OK) {
+            int64_t r = t / C, cc = t % C;
+            for (int64_t i = 0; i < T; ++i)
+                for (int64_t j = 0; j < T; ++j) {
+                    int64_t gi = r * T + i, gj = cc * T + j;
+                    if (gi < H && gj < W) Y[gi * ld_out + gj] = Yt[i * T + j];
+                }
+        } else {
+#pragma omp critical
+            status = st;
+        }
+        free(Yt);
+    }
+    return status;
+}
+
+/*
+ * A sample of tiles: Phi_K of tiles tile_ids[0..n_sel) of B_T(A), each
+ * written as a full T x T tile at Y + s*T*T. Used where the whole matrix is
+ * too large for the oracle to finish in seconds.
+ */
+int oracle_ns_tiles(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t T, int K,
+                    double a, double b, double c, int64_t n_sel, const int64_t* tile_ids, double* Y)
+{
+    if (!tile_ids || n_sel < 0) return ORACLE_BAD_ARG;
+    int status = ORACLE_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t s = 0; s < n_sel; ++s) {
+        int st = oracle_ns_tile(A, H, W, ld_in, T, tile_ids[s], K, a, b, c, Y + s * T * T);
+        if (st != ORACLE_OK) {
+#pragma omp critical
+            status = st;
+        }
+    }
+    return status;
+}
+
+/* Threads an OpenMP parallel region of this library uses (0 without OpenMP). */
+int oracle_num_threads(void)
+{
+    int n = 0;
+#pragma omp parallel
+    {
+#pragma omp atomic
+        n += 1;
+    }
+    return n;
+}

@@ -1,0 +1,162 @@
+/*
+ * himuon.h — C ABI of the MI355X (gfx950) tiled Newton–Schulz library.
+ *
+ * The library evaluates the tiled Newton–Schulz map of Hierarchical Muon,
+ *
+ *     Phi_{K,T}(G) = B_T^{-1}( { Phi_K(G_rc) }_{r,c} )        eq. (tiled_ns), Sec. 4.1
+ *
+ * on a batch of matrices in one call:
+ *   - B_T (Sec. 2.1, eq. tiling_operator) pads an H x W matrix with zeros to
+ *     (RT) x (CT), R = ceil(H/T), C = ceil(W/T), and cuts it into T x T tiles;
+ *     B_T^{-1} reassembles them and drops the padding;
+ *   - Phi_K (Sec. 2.2, eqs. ns_iteration, ns_quintic, phi_k_def) normalises
+ *     a tile, X_0 = S/||S||_F (Phi_K(0) = 0), and applies K steps of
+ *     X <- (aI + bA + cA^2) X with A = X X^T;
+ *   - tiles of every matrix in the call are batched into shared launches
+ *     ("cross-layer batching", Sec. 4.3) and split into the fewest balanced
+ *     chunks that fit a memory budget ("memory-bounded chunking", Sec. 4.3).
+ *
+ * All entry points are plain C: host pointers for the small per-matrix
+ * arrays, device pointers for matrix data and workspace, and a HIP stream
+ * passed as void* (a hipStream_t; NULL is the null stream). No entry point
+ * allocates device memory or synchronises the device on the compute path.
+ *
+ * Matrices are row-major: element (i, j) of matrix l sits at
+ * ptr_l + i*ld_l + j (in elements). One call uses one storage dtype for all
+ * inputs and outputs.
+ */
+#ifndef HIMUON_H
+#define HIMUON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage type of every input and output matrix in a call. */
+typedef enum himuon_dtype {
+    HIMUON_F32 = 0,  /* IEEE binary32                                        */
+    HIMUON_BF16 = 1  /* bfloat16; results rounded to nearest even on store   */
+} himuon_dtype_t;
+
+/* Operand type of the matrix-core (MFMA) products; accumulation, the
+ * normalisation and the polynomial epilogues are fp32 in every mode. */
+typedef enum himuon_compute {
+    HIMUON_COMPUTE_DEFAULT = 0, /* F32 for f32 storage; for bf16 storage F16 when the
+                                   coefficients keep every operand inside the fp16
+                                   range (himuon_select_compute), else BF16          */
+    HIMUON_COMPUTE_F32 = 1,     /* fp32 operands (v_mfma_f32_32x32x2_f32)            */
+    HIMUON_COMPUTE_F16 = 2,     /* fp16 operands, round-to-nearest-even              */
+    HIMUON_COMPUTE_BF16 = 3     /* bf16 operands, round-to-nearest-even              */
+} himuon_compute_t;
+
+/* Status codes. Every error is detected before anything is enqueued: a call
+ * that returns an error has left the stream and all buffers untouched. */
+typedef enum himuon_status {
+    HIMUON_OK = 0,
+    HIMUON_ERR_INVALID_ARG = -1, /* null pointer, rows/cols < 1, ld < cols, K < 0,
+                                    n_mats < 1, non-finite a/b/c, unknown enum     */
+    HIMUON_ERR_UNSUPPORTED = -2, /* T not in {32, 64, 128, 256}, or a dtype/compute
+                                    pair that has no kernel                        */
+    HIMUON_ERR_WORKSPACE = -3,   /* workspace smaller than
+                                    himuon_ns_tiled_workspace_size(n_mats), or a
+                                    chunk budget smaller than one tile             */
+    HIMUON_ERR_HIP = -4,         /* a HIP runtime call failed (see
+                                    himuon_last_hip_error)                         */
+    HIMUON_ERR_RANGE = -5        /* HIMUON_COMPUTE_F16 requested but the iterates can
+                                    leave the fp16 range for these a, b, c, K      */
+} himuon_status_t;
+
+/* Device workspace bytes a call over n_mats matrices needs: the per-matrix
+ * descriptor table the kernels read (64 bytes per matrix, rounded up to
+ * 256). Host-only; returns 0 for n_mats < 1. */
+size_t himuon_ns_tiled_workspace_size(int64_t n_mats);
+
+/*
+ * Y_l = Phi_{K,T}(X_l) for l = 0 .. n_mats-1, enqueued on `stream`.
+ *
+ * in_ptrs[l], out_ptrs[l]  device pointers to matrix l (storage `dtype`).
+ *                          out_ptrs[l] == in_ptrs[l] (in place, same ld) is
+ *                          allowed: each tile is read completely before any
+ *                          of it is written, and one tile has one owner.
+ *                          Any other overlap between matrices is undefined.
+ * rows[l], cols[l]         H and W of matrix l (>= 1).
+ * ld_in, ld_out            leading dimensions in elements (>= cols[l]); either
+ *                          may be NULL, meaning contiguous rows (ld = cols).
+ * T                        tile size, one of 32, 64, 128, 256. A matrix with
+ *                          T >= max(H, W) is one zero-padded tile, which gives
+ *                          Phi_K of the whole matrix (Sec. 4.3).
+ * K                        Newton-Schulz steps (>= 0). K = 0 returns S/||S||_F
+ *                          per tile.
+ * a, b, c                  the polynomial coefficients (finite), e.g. Muon's
+ *                          quintic (3.4445, -4.7750, 2.0315), eq. (ns_quintic).
+ * dtype, compute           himuon_dtype_t and himuon_compute_t values.
+ * workspace                device memory of at least
+ *                          himuon_ns_tiled_workspace_size(n_mats) bytes, owned by
+ *                          the caller; it must stay untouched until the work
+ *                          enqueued by this call has completed on `stream`.
+ * chunk_budget_bytes       bound on the bytes a chunk of tiles stands for
+ *                          (input tile + output tile, 2*T*T*sizeof(dtype) per
+ *                          tile); 0 means one chunk. Chunking never changes a
+ *                          result bit.
+ * stream                   hipStream_t to enqueue on.
+ *
+ * Returns HIMUON_OK once everything is enqueued (asynchronous: kernel faults
+ * surface at the caller's next synchronisation). Non-finite input values stay
+ * within their own tile. The host arrays are read only during the call; the
+ * device buffers must outlive the enqueued work.
+ */
+int himuon_ns_tiled(int64_t n_mats,
+                    const void* const* in_ptrs, void* const* out_ptrs,
+                    const int64_t* rows, const int64_t* cols,
+                    const int64_t* ld_in, const int64_t* ld_out,
+                    int T, int K, float a, float b, float c,
+                    int dtype, int compute,
+                    void* workspace, size_t workspace_bytes,
+                    size_t chunk_budget_bytes,
+                    void* stream);
+
+/*
+ * Host-only planner (no HIP call): the tiles and chunks himuon_ns_tiled
+ * would use. Tiles are numbered matrix by matrix, row-major over each
+ * matrix's R x C grid. The chunk count is the fewest whose per-chunk bytes
+ * (2*T*T*sizeof(dtype) per tile) fit chunk_budget_bytes (0: one chunk), and
+ * the chunks are balanced: chunk i covers [bounds[i], bounds[i+1]) with
+ * sizes that differ by at most one tile.
+ *
+ * T may be any value >= 1 here (planning only). *total_tiles and *n_chunks
+ * are always written on success; chunk_bounds (may be NULL) receives
+ * n_chunks + 1 entries when max_bounds >= n_chunks + 1.
+ * Errors: HIMUON_ERR_INVALID_ARG, HIMUON_ERR_WORKSPACE (budget below one tile).
+ */
+int himuon_plan_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols,
+                       int T, int dtype, size_t chunk_budget_bytes,
+                       int64_t* total_tiles, int64_t* n_chunks,
+                       int64_t* chunk_bounds, int64_t max_bounds);
+
+/*
+ * Host-only: the compute mode a call with these arguments resolves to
+ * (a himuon_compute_t value >= 1), or a negative status. For bf16 storage
+ * and HIMUON_COMPUTE_DEFAULT it returns F16 when the scalar iterates
+ * p^k(s), s in [0, 1], k <= K (p(s) = as + bs^3 + cs^5, which is what every
+ * singular value of the normalised tile follows, Sec. 2.2) bound |X|, |A|,
+ * |A^2| and |bA + cA^2| well inside fp16's range, else BF16.
+ */
+int himuon_select_compute(int dtype, int compute, int K, float a, float b, float c);
+
+/* Static English text for a status code. */
+const char* himuon_status_string(int status);
+
+/* The hipError_t value behind the calling thread's last HIMUON_ERR_HIP. */
+int himuon_last_hip_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int himuon_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HIMUON_H */

@@ -1,0 +1,185 @@
+"""Python binding of libhimuon.so, the MI355X tiled Newton–Schulz library.
+
+Argument marshalling only: every step of the map (tiling, normalisation, the
+K Newton–Schulz steps, reassembly, batching and chunking) runs in the native
+library declared in ``include/himuon.h``. PyTorch is used for device memory
+and streams. If the library is missing the import of any entry point raises;
+there is no fallback implementation.
+
+Low-level names mirror the C ABI (``himuon_ns_tiled``, ``himuon_plan_chunks``,
+``himuon_ns_tiled_workspace_size``, ``himuon_select_compute``,
+``himuon_status_string``, ``himuon_last_hip_error``, ``himuon_version``);
+``ns_tiled`` is the tensor-level convenience wrapper.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(PKG, "libhimuon.so")
+
+# himuon_dtype_t / himuon_compute_t / himuon_status_t
+F32, BF16 = 0, 1
+COMPUTE_DEFAULT, COMPUTE_F32, COMPUTE_F16, COMPUTE_BF16 = 0, 1, 2, 3
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_RANGE = 0, -1, -2, -3, -4, -5
+TILE_SIZES = (32, 64, 128, 256)
+QUINTIC = (3.4445, -4.7750, 2.0315)  # eq. (ns_quintic)
+
+_lib = None
+
+
+class HimuonError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        msg = f"{what}: {himuon_status_string(status)} (status {status})"
+        if status == ERR_HIP:
+            msg += f", hipError {himuon_last_hip_error()}"
+        super().__init__(msg)
+
+
+def lib():
+    """The loaded native library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIBRARY):
+            raise ImportError(f"{LIBRARY} is missing; build it with "
+                              "`python -m paper_2606_27216_amd.build_lib`")
+        L = ctypes.CDLL(LIBRARY)
+        i64, vp, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+        L.himuon_ns_tiled_workspace_size.argtypes = [i64]
+        L.himuon_ns_tiled_workspace_size.restype = sz
+        L.himuon_ns_tiled.argtypes = [i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                      ctypes.c_int, ctypes.c_int, vp, sz, sz, vp]
+        L.himuon_ns_tiled.restype = ctypes.c_int
+        L.himuon_plan_chunks.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, sz, vp, vp, vp, i64]
+        L.himuon_plan_chunks.restype = ctypes.c_int
+        L.himuon_select_compute.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                            ctypes.c_float, ctypes.c_float, ctypes.c_float]
+        L.himuon_select_compute.restype = ctypes.c_int
+        L.himuon_status_string.argtypes = [ctypes.c_int]
+        L.himuon_status_string.restype = ctypes.c_char_p
+        L.himuon_last_hip_error.argtypes = []
+        L.himuon_last_hip_error.restype = ctypes.c_int
+        L.himuon_version.argtypes = []
+        L.himuon_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _i64_array(vals):
+    vals = [int(v) for v in vals]
+    return (ctypes.c_int64 * len(vals))(*vals)
+
+
+def _ptr_array(vals):
+    vals = [int(v) for v in vals]
+    return (ctypes.c_void_p * len(vals))(*vals)
+
+
+# ---------------------------------------------------------------- raw C ABI
+
+def himuon_ns_tiled_workspace_size(n_mats: int) -> int:
+    return int(lib().himuon_ns_tiled_workspace_size(int(n_mats)))
+
+
+def himuon_ns_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c,
+                    dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream) -> int:
+    """Same arguments as the C function; Python sequences for the per-matrix
+    arrays (``ld_in``/``ld_out`` may be None), integers for device pointers
+    and the stream handle. Returns the status code."""
+    return int(lib().himuon_ns_tiled(
+        int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
+        None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
+        int(T), int(K), float(a), float(b), float(c), int(dtype), int(compute),
+        int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes),
+        int(stream) if stream else None))
+
+
+def himuon_plan_chunks(rows, cols, T, dtype=BF16, chunk_budget_bytes=0):
+    """Returns (total_tiles, [chunk bounds]) or raises HimuonError."""
+    n = len(rows)
+    total = ctypes.c_int64()
+    nch = ctypes.c_int64()
+    st = lib().himuon_plan_chunks(n, _i64_array(rows), _i64_array(cols), int(T), int(dtype),
+                                  int(chunk_budget_bytes), ctypes.byref(total), ctypes.byref(nch), None, 0)
+    if st != OK:
+        raise HimuonError(st, "himuon_plan_chunks")
+    bounds = (ctypes.c_int64 * (nch.value + 1))()
+    st = lib().himuon_plan_chunks(n, _i64_array(rows), _i64_array(cols), int(T), int(dtype),
+                                  int(chunk_budget_bytes), ctypes.byref(total), ctypes.byref(nch),
+                                  bounds, nch.value + 1)
+    if st != OK:
+        raise HimuonError(st, "himuon_plan_chunks")
+    return total.value, list(bounds)
+
+
+def himuon_select_compute(dtype, compute, K, a, b, c) -> int:
+    return int(lib().himuon_select_compute(int(dtype), int(compute), int(K), float(a), float(b), float(c)))
+
+
+def himuon_status_string(status: int) -> str:
+    return lib().himuon_status_string(int(status)).decode()
+
+
+def himuon_last_hip_error() -> int:
+    return int(lib().himuon_last_hip_error())
+
+
+def himuon_version() -> int:
+    return int(lib().himuon_version())
+
+
+# ------------------------------------------------------------ tensor wrapper
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; expected float32 or bfloat16")
+
+
+def ns_tiled(inputs, outputs=None, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT,
+             chunk_budget_bytes=0, workspace=None, stream=None):
+    """Φ_{K,T} of every 2-D CUDA tensor in ``inputs`` in one library call.
+
+    ``outputs`` defaults to fresh tensors; passing ``outputs=inputs`` runs in
+    place. Rows may be strided (``stride(1) == 1`` is required). The call is
+    asynchronous on ``stream`` (default: torch's current stream). Returns the
+    outputs."""
+    import torch
+    inputs = list(inputs)
+    if not inputs:
+        raise ValueError("no matrices")
+    code = _dtype_code(inputs[0])
+    dev = inputs[0].device
+    for x in inputs:
+        if x.dim() != 2 or not x.is_cuda or x.device != dev or _dtype_code(x) != code or x.stride(1) != 1:
+            raise ValueError("inputs must be 2-D row-major CUDA tensors of one dtype on one device")
+    if outputs is None:
+        outputs = [torch.empty_like(x, memory_format=torch.contiguous_format) for x in inputs]
+    outputs = list(outputs)
+    if len(outputs) != len(inputs):
+        raise ValueError("inputs and outputs differ in length")
+    for x, y in zip(inputs, outputs):
+        if y.shape != x.shape or y.dtype != x.dtype or y.device != dev or y.stride(1) != 1:
+            raise ValueError("each output must match its input's shape, dtype and device")
+    n = len(inputs)
+    need = himuon_ns_tiled_workspace_size(n)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    a, b, c = coeffs
+    st = himuon_ns_tiled(
+        n, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs],
+        [x.shape[0] for x in inputs], [x.shape[1] for x in inputs],
+        [x.stride(0) for x in inputs], [y.stride(0) for y in outputs],
+        T, K, a, b, c, code, compute, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+        chunk_budget_bytes, stream.cuda_stream)
+    if st != OK:
+        raise HimuonError(st, "himuon_ns_tiled")
+    return outputs

@@ -1,0 +1,311 @@
+// C ABI of the tiled Newton–Schulz library: argument validation, the tile
+// and chunk plan, descriptor upload, and one kernel launch per chunk.
+//
+// Plan (Sec. 4.3 "cross-layer batching" and "memory-bounded chunking";
+// Sec. 4.4 "runtime tile-size reconfiguration"): every matrix of a call
+// contributes its R x C tiles to one global, densely numbered tile set; the
+// set is split into the fewest chunks whose staged bytes fit the budget,
+// balanced to within one tile. The plan is O(#matrices) integer work and is
+// rebuilt on every call, so changing T between calls costs nothing extra.
+#include "himuon_internal.h"
+#include "../../include/himuon.h"
+
+#include <math.h>
+#include <mutex>
+#include <string.h>
+#include <vector>
+
+namespace {
+
+using himuon::MatDesc;
+
+constexpr int kVersion = 100;  // 0.1.0
+
+thread_local int g_last_hip_error = 0;
+
+int hip_fail(hipError_t e)
+{
+    g_last_hip_error = (int)e;
+    return HIMUON_ERR_HIP;
+}
+
+size_t elem_size(int dtype) { return dtype == HIMUON_BF16 ? 2 : 4; }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Tiles per matrix prefix and total; validates shapes. T >= 1.
+int plan_tiles(int64_t n_mats, const int64_t* rows, const int64_t* cols, int64_t T,
+               std::vector<int64_t>* begin, int64_t* total)
+{
+    if (n_mats < 1 || !rows || !cols || T < 1) return HIMUON_ERR_INVALID_ARG;
+    int64_t acc = 0;
+    if (begin) begin->resize((size_t)n_mats);
+    for (int64_t m = 0; m < n_mats; ++m) {
+        if (rows[m] < 1 || cols[m] < 1) return HIMUON_ERR_INVALID_ARG;
+        const int64_t t = ceil_div(rows[m], T) * ceil_div(cols[m], T);
+        if (begin) (*begin)[(size_t)m] = acc;
+        if (acc > INT64_MAX - t) return HIMUON_ERR_INVALID_ARG;
+        acc += t;
+    }
+    *total = acc;
+    return HIMUON_OK;
+}
+
+// Fewest chunks whose per-chunk bytes (2*T*T*elem per tile) fit `budget`.
+int plan_chunk_count(int64_t total, int64_t T, size_t elem, size_t budget, int64_t* n_chunks)
+{
+    if (budget == 0) {
+        *n_chunks = 1;
+        return HIMUON_OK;
+    }
+    const unsigned __int128 per_tile = (unsigned __int128)2 * (unsigned __int128)T * (unsigned __int128)T * elem;
+    const unsigned __int128 fit = (unsigned __int128)budget / per_tile;
+    if (fit == 0) return HIMUON_ERR_WORKSPACE;
+    const int64_t per_chunk = fit > (unsigned __int128)total ? total : (int64_t)fit;
+    *n_chunks = ceil_div(total, per_chunk);
+    return HIMUON_OK;
+}
+
+int64_t chunk_bound(int64_t i, int64_t total, int64_t n_chunks)
+{
+    return (int64_t)(((__int128)i * total) / n_chunks);
+}
+
+bool finite3(float a, float b, float c) { return isfinite(a) && isfinite(b) && isfinite(c); }
+
+// Largest |p^k(s)| over s in [0, 1] and k < K, for p(s) = a s + b s^3 + c s^5:
+// each singular value of the normalised tile starts in [0, 1] and follows p
+// exactly, so this bounds every entry of the operand X at every step. The
+// interval is sampled densely; a factor of 4 covers what falls between points.
+double iterate_bound(int K, double a, double b, double c)
+{
+    constexpr int kPts = 8193;
+    double m = 1.0;
+    std::vector<double> s(kPts);
+    for (int i = 0; i < kPts; ++i) s[i] = (double)i / (kPts - 1);
+    for (int k = 1; k < K; ++k) {
+        for (int i = 0; i < kPts; ++i) {
+            const double x = s[i];
+            const double y = a * x + b * x * x * x + c * x * x * x * x * x;
+            s[i] = y;
+            const double ay = fabs(y);
+            if (!(ay < 1e30)) return INFINITY;
+            if (ay > m) m = ay;
+        }
+    }
+    return m;
+}
+
+int resolve_compute(int dtype, int compute, int K, float a, float b, float c)
+{
+    if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
+    if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
+    if (!finite3(a, b, c) || K < 0) return HIMUON_ERR_INVALID_ARG;
+    if (dtype == HIMUON_F32) {
+        if (compute == HIMUON_COMPUTE_DEFAULT || compute == HIMUON_COMPUTE_F32) return HIMUON_COMPUTE_F32;
+        return HIMUON_ERR_UNSUPPORTED;
+    }
+    if (compute == HIMUON_COMPUTE_F32) return HIMUON_ERR_UNSUPPORTED;
+    if (compute == HIMUON_COMPUTE_BF16) return HIMUON_COMPUTE_BF16;
+    // fp16 operands: X (<= M), A and the A-operand of A^2 (<= M^2) and
+    // B = bA + cA^2 (<= |b| M^2 + |c| M^4) must stay far below 65504.
+    const double M = 4.0 * iterate_bound(K, a, b, c);
+    const double M2 = M * M;
+    const double bound = fmax(fmax(M, M2), fabs((double)b) * M2 + fabs((double)c) * M2 * M2);
+    const bool safe = bound < 16384.0;
+    if (compute == HIMUON_COMPUTE_F16) return safe ? HIMUON_COMPUTE_F16 : HIMUON_ERR_RANGE;
+    return safe ? HIMUON_COMPUTE_F16 : HIMUON_COMPUTE_BF16;
+}
+
+// Pinned host staging for the descriptor table. A ring of slots lets the
+// host run several calls ahead of the GPU; a slot is reused only after the
+// copy that read it has completed (its event).
+struct StagingSlot {
+    void* host = nullptr;
+    size_t cap = 0;
+    hipEvent_t ev = nullptr;
+    int dev = -1;
+    bool pending = false;
+};
+
+constexpr int kSlots = 8;
+std::mutex g_staging_mu;
+StagingSlot g_slots[kSlots];
+unsigned g_next_slot = 0;
+
+int upload_descs(const std::vector<MatDesc>& descs, void* workspace, hipStream_t stream, int dev)
+{
+    const size_t bytes = descs.size() * sizeof(MatDesc);
+    std::lock_guard<std::mutex> lock(g_staging_mu);
+    StagingSlot& sl = g_slots[g_next_slot++ % kSlots];
+    hipError_t e;
+    if (sl.pending) {
+        e = hipEventSynchronize(sl.ev);
+        if (e != hipSuccess) return hip_fail(e);
+        sl.pending = false;
+    }
+    if (sl.cap < bytes) {
+        if (sl.host) {
+            e = hipHostFree(sl.host);
+            if (e != hipSuccess) return hip_fail(e);
+            sl.host = nullptr;
+            sl.cap = 0;
+        }
+        size_t cap = 4096;
+        while (cap < bytes) cap *= 2;
+        e = hipHostMalloc(&sl.host, cap, hipHostMallocDefault);
+        if (e != hipSuccess) return hip_fail(e);
+        sl.cap = cap;
+    }
+    if (sl.dev != dev) {
+        if (sl.ev) (void)hipEventDestroy(sl.ev);
+        sl.ev = nullptr;
+        e = hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(e);
+        sl.dev = dev;
+    }
+    memcpy(sl.host, descs.data(), bytes);
+    e = hipMemcpyAsync(workspace, sl.host, bytes, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail(e);
+    e = hipEventRecord(sl.ev, stream);
+    if (e != hipSuccess) return hip_fail(e);
+    sl.pending = true;
+    return HIMUON_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t himuon_ns_tiled_workspace_size(int64_t n_mats)
+{
+    if (n_mats < 1) return 0;
+    const size_t b = (size_t)n_mats * sizeof(MatDesc);
+    return (b + 255) / 256 * 256;
+}
+
+int himuon_plan_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
+                       size_t chunk_budget_bytes, int64_t* total_tiles, int64_t* n_chunks,
+                       int64_t* chunk_bounds, int64_t max_bounds)
+{
+    if (!total_tiles || !n_chunks) return HIMUON_ERR_INVALID_ARG;
+    if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
+    int64_t total = 0, nc = 0;
+    int st = plan_tiles(n_mats, rows, cols, T, nullptr, &total);
+    if (st != HIMUON_OK) return st;
+    st = plan_chunk_count(total, T, elem_size(dtype), chunk_budget_bytes, &nc);
+    if (st != HIMUON_OK) return st;
+    *total_tiles = total;
+    *n_chunks = nc;
+    if (chunk_bounds && max_bounds >= nc + 1)
+        for (int64_t i = 0; i <= nc; ++i) chunk_bounds[i] = chunk_bound(i, total, nc);
+    return HIMUON_OK;
+}
+
+int himuon_select_compute(int dtype, int compute, int K, float a, float b, float c)
+{
+    return resolve_compute(dtype, compute, K, a, b, c);
+}
+
+int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+                    const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a,
+                    float b, float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
+                    size_t chunk_budget_bytes, void* stream)
+{
+    // ---- validation: nothing is enqueued unless every check passes
+    if (n_mats < 1 || n_mats > INT32_MAX || !in_ptrs || !out_ptrs || !rows || !cols) return HIMUON_ERR_INVALID_ARG;
+    if (K < 0 || !finite3(a, b, c)) return HIMUON_ERR_INVALID_ARG;
+    if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
+    if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
+    if (T != 32 && T != 64 && T != 128 && T != 256) return HIMUON_ERR_UNSUPPORTED;
+    for (int64_t m = 0; m < n_mats; ++m) {
+        if (!in_ptrs[m] || !out_ptrs[m] || rows[m] < 1 || cols[m] < 1) return HIMUON_ERR_INVALID_ARG;
+        const int64_t li = ld_in ? ld_in[m] : cols[m];
+        const int64_t lo = ld_out ? ld_out[m] : cols[m];
+        if (li < cols[m] || lo < cols[m]) return HIMUON_ERR_INVALID_ARG;
+        if (rows[m] > INT64_MAX / li || rows[m] > INT64_MAX / lo) return HIMUON_ERR_INVALID_ARG;
+    }
+    const int op = resolve_compute(dtype, compute, K, a, b, c);
+    if (op < 0) return op;
+    const himuon::Storage st = dtype == HIMUON_BF16 ? himuon::Storage::BF16 : himuon::Storage::F32;
+    const himuon::Operand opnd = (himuon::Operand)op;
+    if (!himuon::has_kernel(T, st, opnd)) return HIMUON_ERR_UNSUPPORTED;
+    if (!workspace || workspace_bytes < himuon_ns_tiled_workspace_size(n_mats)) return HIMUON_ERR_WORKSPACE;
+
+    std::vector<int64_t> begin;
+    int64_t total = 0, n_chunks = 0;
+    int s = plan_tiles(n_mats, rows, cols, T, &begin, &total);
+    if (s != HIMUON_OK) return s;
+    s = plan_chunk_count(total, T, elem_size(dtype), chunk_budget_bytes, &n_chunks);
+    if (s != HIMUON_OK) return s;
+
+    // ---- descriptor table
+    const size_t align = dtype == HIMUON_BF16 ? 8 : 16;
+    std::vector<MatDesc> descs((size_t)n_mats);
+    for (int64_t m = 0; m < n_mats; ++m) {
+        MatDesc& d = descs[(size_t)m];
+        d.in = in_ptrs[m];
+        d.out = out_ptrs[m];
+        d.rows = rows[m];
+        d.cols = cols[m];
+        d.ld_in = ld_in ? ld_in[m] : cols[m];
+        d.ld_out = ld_out ? ld_out[m] : cols[m];
+        d.tile_begin = begin[(size_t)m];
+        d.tiles_c = (int32_t)ceil_div(cols[m], T);
+        d.flags = 0;
+        if ((uintptr_t)d.in % align == 0 && d.ld_in % 4 == 0) d.flags |= himuon::MAT_VEC_IN;
+        if ((uintptr_t)d.out % align == 0 && d.ld_out % 4 == 0) d.flags |= himuon::MAT_VEC_OUT;
+        if (ceil_div(cols[m], T) > INT32_MAX) return HIMUON_ERR_INVALID_ARG;
+    }
+
+    // ---- run on the stream's device
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    int cur = 0, dev = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return hip_fail(e);
+    dev = cur;
+    if (hs) {
+        e = hipStreamGetDevice(hs, &dev);
+        if (e != hipSuccess) return hip_fail(e);
+    }
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e);
+
+    int status = upload_descs(descs, workspace, hs, dev);
+    if (status == HIMUON_OK) {
+        himuon::KernelArgs ka;
+        ka.descs = static_cast<const MatDesc*>(workspace);
+        ka.n_mats = (int32_t)n_mats;
+        ka.K = K;
+        ka.a = a;
+        ka.b = b;
+        ka.c = c;
+        ka.b_over_c = c != 0.f ? b / c : 0.f;
+        for (int64_t i = 0; i < n_chunks && status == HIMUON_OK; ++i) {
+            ka.tile_begin = chunk_bound(i, total, n_chunks);
+            ka.tile_end = chunk_bound(i + 1, total, n_chunks);
+            e = himuon::launch_ns_tiled(T, st, opnd, ka, hs);
+            if (e != hipSuccess) status = hip_fail(e);
+        }
+    }
+    if (dev != cur) (void)hipSetDevice(cur);
+    return status;
+}
+
+const char* himuon_status_string(int status)
+{
+    switch (status) {
+    case HIMUON_OK: return "success";
+    case HIMUON_ERR_INVALID_ARG: return "invalid argument";
+    case HIMUON_ERR_UNSUPPORTED: return "unsupported tile size or dtype/compute combination";
+    case HIMUON_ERR_WORKSPACE: return "workspace or chunk budget too small";
+    case HIMUON_ERR_HIP: return "HIP runtime error";
+    case HIMUON_ERR_RANGE: return "fp16 operands would leave the fp16 range for these coefficients";
+    default: return "unknown status";
+    }
+}
+
+int himuon_last_hip_error(void) { return g_last_hip_error; }
+
+int himuon_version(void) { return kVersion; }
+
+}  // extern "C"

@@ -1,0 +1,270 @@
+"""HIP path against the fp64 oracle, element by element, through the C ABI.
+
+Bars (written here, from the target): per-tile relative Frobenius error
+<= 1e-5 for fp32 storage and <= 2e-2 for bf16 storage; bit-exact equality
+for properties that hold exactly in any fixed-order arithmetic (batching,
+chunking, tile permutation, repetition, power-of-two scaling, sign).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_27216_amd as hm
+import workloads
+from parity import COEF32, TOL, sampled_tile_errors, tile_errors, to_f64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def announce(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def run(mats, T, K=5, coeffs=COEF32, compute=hm.COMPUTE_DEFAULT, budget=0, outputs=None):
+    out = hm.ns_tiled(mats, outputs=outputs, T=T, K=K, coeffs=coeffs, compute=compute, chunk_budget_bytes=budget)
+    torch.cuda.synchronize()
+    return out
+
+
+def check_full(x, y, T, K=5, coeffs=COEF32, tol=None):
+    S = to_f64(x)
+    R = oracle.ns_tiled(S, T, K, *coeffs)
+    e = tile_errors(to_f64(y), R, T)
+    tol = TOL[x.dtype] if tol is None else tol
+    assert np.all(np.isfinite(e)), "non-finite tile"
+    assert e.max() <= tol, f"max per-tile error {e.max():.3e} > {tol:.1e} (p50 {np.median(e):.3e})"
+    return e
+
+
+# ------------------------------------------------------------------ configs
+
+def test_config1_fp32_T32():
+    announce("256x256 fp32 N(0,1) seed 0, T=32, K=5")
+    x = workloads.gaussian(256, 256, 0, "f32", DEV)
+    (y,) = run([x], 32)
+    e = check_full(x, y, 32)
+    assert len(e) == 64
+
+
+@pytest.mark.parametrize("T", [32, 64, 128])
+def test_config2_bf16(T):
+    announce(f"4096x4096 bf16 low-rank+noise seed 2, T={T}, K=5")
+    x = workloads.lowrank_plus_noise(4096, 4096, 2, "bf16", DEV)
+    (y,) = run([x], T)
+    check_full(x, y, T)
+
+
+def test_config2_bf16_operands_T128():
+    """bf16 MFMA operands (instead of the default fp16) at T=128, K=5."""
+    announce("4096x4096 bf16, compute=BF16, T=128")
+    x = workloads.lowrank_plus_noise(4096, 4096, 2, "bf16", DEV)
+    (y,) = run([x], 128, compute=hm.COMPUTE_BF16)
+    check_full(x, y, 128)
+
+
+def test_config3_one_layer_sampled():
+    announce("7B layer (7 matrices) bf16 T=128 K=5, 24 sampled tiles per matrix")
+    mats = workloads.layer_7b(3000, "bf16", DEV)
+    outs = run(mats, 128)
+    rng = np.random.default_rng(3)
+    for x, y in zip(mats, outs):
+        S = to_f64(x)
+        n = oracle.tile_count(*S.shape, 128)
+        ids = np.sort(rng.choice(n, 24, replace=False))
+        ref = oracle.ns_tiles(S, 128, 5, *COEF32, ids)
+        e = sampled_tile_errors(to_f64(y), ref, ids, 128)
+        assert e.max() <= TOL[torch.bfloat16], e.max()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("K", [5, 8])
+def test_config5_heterogeneous_schedule(dtype, K):
+    """24 heavy-tailed matrices, the runtime tile schedule over successive calls."""
+    mats = workloads.heterogeneous(dtype, DEV)
+    rng = np.random.default_rng(5)
+    for T in (128, 64, 32):
+        announce(f"heterogeneous batch {dtype} K={K} T={T}")
+        outs = run(mats, T, K=K)
+        for i in (0, 9, 17):  # one matrix of each shape
+            S = to_f64(mats[i])
+            n = oracle.tile_count(*S.shape, T)
+            ids = np.sort(rng.choice(n, 12, replace=False))
+            ref = oracle.ns_tiles(S, T, K, *COEF32, ids)
+            e = sampled_tile_errors(to_f64(outs[i]), ref, ids, T)
+            assert e.max() <= TOL[mats[i].dtype], (T, i, e.max())
+
+
+@pytest.mark.parametrize("T", [128, 64, 32])
+def test_config5_fp32_K8_every_tile(T):
+    """Every tile of one heavy-tailed 2048x2048 fp32 matrix at K=8, where
+    ill-conditioned tiles amplify fp32 rounding the most."""
+    announce(f"2048x2048 fp32 Student-t K=8 T={T}, all tiles")
+    x = workloads.student_t(2048, 2048, 5017, "f32", DEV)
+    (y,) = run([x], T, K=8)
+    check_full(x, y, T, K=8)
+
+
+# ------------------------------------------------------------- edge cases
+
+RAGGED = [(100, 300), (257, 129), (33, 4096), (1, 1), (5, 700), (130, 2), (64, 64)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("T", [32, 64, 128])
+def test_ragged_heterogeneous_batch(dtype, T):
+    announce(f"ragged batch {dtype} T={T}")
+    mats = [workloads.gaussian(h, w, 40 + i, dtype, DEV) for i, (h, w) in enumerate(RAGGED)]
+    outs = run(mats, T)
+    for x, y in zip(mats, outs):
+        check_full(x, y, T)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_single_padded_tile_is_full_map(dtype):
+    """T >= max(H, W): one zero-padded tile, equal to Phi_K of the matrix."""
+    announce(f"single padded tile {dtype}")
+    x = workloads.gaussian(50, 120, 7, dtype, DEV)
+    (y,) = run([x], 128)
+    ref = oracle.phi_k(to_f64(x), 5, *COEF32)
+    e = np.linalg.norm(to_f64(y) - ref) / np.linalg.norm(ref)
+    assert e <= TOL[x.dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("K", [0, 1, 8])
+def test_step_counts(dtype, K):
+    announce(f"K={K} {dtype}")
+    x = workloads.student_t(300, 200, 8, dtype, DEV)
+    for T in (32, 64, 128):
+        (y,) = run([x], T, K=K)
+        check_full(x, y, T, K=K)
+
+
+@pytest.mark.parametrize("coeffs", [(1.5, -0.5, 0.0), (1.0, 0.0, 0.0), (2.0, -1.5, 0.5)])
+def test_other_coefficients(coeffs):
+    announce(f"coefficients {coeffs}")
+    coeffs = tuple(float(np.float32(v)) for v in coeffs)
+    x = workloads.gaussian(160, 96, 9, "f32", DEV)
+    for T in (32, 64, 128):
+        (y,) = run([x], T, K=6, coeffs=coeffs)
+        check_full(x, y, T, K=6, coeffs=coeffs)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_zero_and_nonfinite_tiles_stay_contained(dtype):
+    announce(f"zero / NaN / Inf tiles {dtype}")
+    x = workloads.gaussian(128, 192, 10, dtype, DEV)
+    x[0:64, 64:128] = 0
+    (clean,) = run([x], 64)
+    bad = x.clone()
+    bad[64:128, 0:64][3, 5] = float("nan")
+    bad[64:128, 128:192][0, 0] = float("inf")
+    (y,) = run([bad], 64)
+    assert torch.count_nonzero(clean[0:64, 64:128]) == 0
+    assert not torch.isfinite(y[64:128, 0:64]).all()
+    assert not torch.isfinite(y[64:128, 128:192]).all()
+    keep = torch.ones_like(x, dtype=torch.bool)
+    keep[64:128, 0:64] = False
+    keep[64:128, 128:192] = False
+    assert torch.equal(y[keep], clean[keep])
+    check_full(x, clean, 64)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_in_place_and_strided(dtype):
+    announce(f"in place and strided rows {dtype}")
+    big = workloads.gaussian(200, 300, 11, dtype, DEV)
+    x = big[:, 10:260]  # row stride 300, 250 columns, misaligned base
+    ref_in = x.clone()
+    (y,) = run([x], 64)
+    check_full(ref_in, y, 64)
+    z = ref_in.clone()
+    run([z], 64, outputs=[z])
+    assert torch.equal(z, y)
+    run([x], 64, outputs=[x])  # in place on the strided view
+    assert torch.equal(x, y)
+    assert torch.equal(big[:, :10], workloads.gaussian(200, 300, 11, dtype, DEV)[:, :10])
+
+
+# ---------------------------------------------------------- exact properties
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_batching_chunking_permutation_bitwise(dtype):
+    announce(f"batching / chunking / permutation bitwise {dtype}")
+    T = 32
+    mats = [workloads.student_t(h, w, 60 + i, dtype, DEV) for i, (h, w) in enumerate(RAGGED)]
+    base = run(mats, T)
+    for i, x in enumerate(mats):
+        (alone,) = run([x], T)
+        assert torch.equal(alone, base[i])
+    elem = 4 if dtype == "f32" else 2
+    for tiles in (1, 3, 50):
+        outs = run(mats, T, budget=tiles * 2 * T * T * elem)
+        for a, b in zip(outs, base):
+            assert torch.equal(a, b)
+    rev = run(mats[::-1], T)
+    for a, b in zip(rev[::-1], base):
+        assert torch.equal(a, b)
+    # permuting the tiles of a matrix permutes the output tiles
+    x = workloads.gaussian(4 * T, 3 * T, 70, dtype, DEV)
+    (y,) = run([x], T)
+    perm = np.random.default_rng(0).permutation(12)
+    xp = torch.empty_like(x)
+    yp = torch.empty_like(y)
+    for dst, src in enumerate(perm):
+        (dr, dc), (sr, sc) = divmod(dst, 3), divmod(int(src), 3)
+        xp[dr * T:(dr + 1) * T, dc * T:(dc + 1) * T] = x[sr * T:(sr + 1) * T, sc * T:(sc + 1) * T]
+        yp[dr * T:(dr + 1) * T, dc * T:(dc + 1) * T] = y[sr * T:(sr + 1) * T, sc * T:(sc + 1) * T]
+    (yq,) = run([xp], T)
+    assert torch.equal(yq, yp)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("T", [32, 64, 128])
+def test_determinism_scale_sign(dtype, T):
+    announce(f"determinism / 2^e scale / sign {dtype} T={T}")
+    x = workloads.student_t(256, 384, 80, dtype, DEV)
+    (y,) = run([x], T)
+    for _ in range(10):
+        (z,) = run([x], T)
+        assert torch.equal(z, y)
+    for e in (-40, -3, 5, 60):
+        (z,) = run([x * (2.0 ** e)], T)
+        assert torch.equal(z, y), e
+    (z,) = run([-x], T)
+    if dtype == "f32":
+        assert torch.equal(z, -y)
+    else:
+        # The 16-bit MFMA accumulates sign-asymmetrically in its last bits, so
+        # Phi(-S) and -Phi(S) may differ by rounding; both must meet the bar.
+        d = (z.float() + y.float()).abs().max().item()
+        print(f"max |Phi(-S) + Phi(S)| = {d:.3e}", flush=True)
+        assert d <= 1e-2 * y.float().abs().max().item()
+        check_full(-x, z, T)
+
+
+# ------------------------------------------------------------- full size
+
+@pytest.mark.slow
+def test_7b_stack_full_size_sampled():
+    """The benchmarked workload at full size and in the benchmarked launch
+    configuration (32 layers, 224 matrices, T=128, 16 GB chunk budget ->
+    two launches), checked on sampled tiles across the stack."""
+    announce("32-layer 7B stack bf16 T=128 K=5, 16 GB budget, sampled tiles")
+    mats = workloads.stack_7b(32, "bf16", DEV)
+    outs = run(mats, 128, budget=16 * 10 ** 9)
+    rng = np.random.default_rng(4)
+    worst = 0.0
+    for L in (0, 13, 31):
+        for j in range(7):
+            i = 7 * L + j
+            S = to_f64(mats[i])
+            n = oracle.tile_count(*S.shape, 128)
+            ids = np.sort(rng.choice(n, 3, replace=False))
+            ref = oracle.ns_tiles(S, 128, 5, *COEF32, ids)
+            e = sampled_tile_errors(to_f64(outs[i]), ref, ids, 128)
+            worst = max(worst, e.max())
+    assert worst <= TOL[torch.bfloat16], worst

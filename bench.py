@@ -1,0 +1,237 @@
+"""Throughput of the tiled Newton–Schulz map on one MI355X.
+
+    python bench.py [--steps 20] [--warmup 5] [--T 128] [--K 5] [--workload stack7b]
+
+One step is one ``himuon_ns_tiled`` call over the whole workload (every tile
+of every matrix: gather, normalise, K Newton–Schulz steps, write back), with
+the inputs already resident in HBM. The default workload is a 32-layer stack
+of 7B-style projection matrices (q, k, v, o 4096x4096; gate, up 11008x4096;
+down 4096x11008; 224 matrices, 6.48e9 bf16 entries), synthetic low-rank(64)
+plus noise, T=128, K=5, under a 16 GB chunk budget (two chunk launches).
+
+Throughput counts 6·H·W·T·K flops per matrix (three T³ products per tile per
+step). Rank 0 prints one JSON line on stdout; progress goes to stderr.
+The JSON also carries:
+  roofline      the fused kernel's algorithmic flops per launch over its mean
+                launch duration (HIP events on the launch stream), against the
+                published dense fp16/bf16 MFMA peak (2.5 PFLOP/s); `traffic` is
+                the HBM bytes per launch from rocprofv3 FETCH_SIZE/WRITE_SIZE
+                counters (profiles/ns_tiled_traffic.json) when they were taken
+                on the current kernel source, else null;
+  cpu_baseline  the fp64 oracle timed on the host cores on a bounded random
+                sample of the same workload's tiles (read back from the GPU).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}  # MI355X dense MFMA, published
+HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_27216_amd", "csrc", "ns_tiled_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ns_tiled_traffic.json")
+METRIC = "tiled-NS TFLOP/s (6·H·W·T·K) + % bf16 MFMA peak, 7B layer stack T=128 K=5"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def build_workload(name, device, dtype):
+    import workloads
+    if name == "stack7b":
+        desc = ("7B layer stack: 32 layers x (q,k,v,o 4096x4096; gate,up 11008x4096; down 4096x11008), "
+                "224 matrices, low-rank(64, sigma_i=1/i)+0.01 N(0,1)")
+        return desc, workloads.stack_7b(32, dtype, device)
+    if name == "layer7b":
+        return "one 7B layer: 7 matrices, low-rank(64)+noise", workloads.layer_7b(3000, dtype, device)
+    if name == "square4096":
+        return "one 4096x4096 low-rank(64)+noise", [workloads.lowrank_plus_noise(4096, 4096, 2, dtype, device)]
+    if name == "hetero":
+        return ("heterogeneous: 8 each of 1024x4096, 4096x1024, 2048x2048, 0.02 t(3)",
+                workloads.heterogeneous(dtype, device))
+    raise SystemExit(f"unknown workload {name}")
+
+
+def traffic_for_launch(T, K, dtype, compute, tiles_per_launch):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on this kernel source and this configuration."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    key = f"T{T}_K{K}_{dtype}_{compute}_tiles{tiles_per_launch}"
+    ent = rec.get("launches", {}).get(key)
+    if not ent:
+        return None
+    return ent["fetch_bytes"] + ent["write_bytes"]
+
+
+def cpu_baseline(mats, T, K, coeffs, budget_s, seed=0):
+    """The fp64 oracle on a random sample of tiles of the workload (host cores)."""
+    import numpy as np
+    import oracle
+
+    rng = np.random.default_rng(seed)
+    counts = [oracle.tile_count(x.shape[0], x.shape[1], T) for x in mats]
+    done = 0
+    elapsed = 0.0
+    batch = 16
+    while elapsed < budget_s:
+        i = int(rng.integers(len(mats)))
+        x = mats[i]
+        ids = np.sort(rng.choice(counts[i], batch, replace=False))
+        C = -(-x.shape[1] // T)
+        # read back only the rows those tiles touch
+        rows = sorted({int(t) // C for t in ids})
+        sub = {r: x[r * T:(r + 1) * T].float().cpu().double().numpy() for r in rows}
+        t0 = time.perf_counter()
+        for r in rows:
+            loc = [int(t) % C for t in ids if int(t) // C == r]
+            oracle.ns_tiles(sub[r], T, K, *coeffs, loc)
+        elapsed += time.perf_counter() - t0
+        done += batch
+    flops = 6.0 * T ** 3 * K * done
+    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{done} random {T}x{T} tiles of the same workload (fp64 oracle, {elapsed:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="stack7b", choices=["stack7b", "layer7b", "square4096", "hetero"])
+    ap.add_argument("--T", type=int, default=128)
+    ap.add_argument("--K", type=int, default=5)
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--compute", default="default", choices=["default", "f16", "bf16", "f32"])
+    ap.add_argument("--budget", type=float, default=16e9, help="chunk budget in bytes (0: one chunk)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB per launch (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the tiled map needs no communication, and this build measures "
+              "one GPU's share (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2606_27216_amd as hm
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup + args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copied {args.calib_copy_mib} MiB x {args.warmup + args.steps}")
+        return
+
+    coeffs = tuple(float(np.float32(v)) for v in hm.QUINTIC)
+    compute = {"default": hm.COMPUTE_DEFAULT, "f16": hm.COMPUTE_F16, "bf16": hm.COMPUTE_BF16,
+               "f32": hm.COMPUTE_F32}[args.compute]
+    resolved = hm.himuon_select_compute(hm.BF16 if args.dtype == "bf16" else hm.F32, compute, args.K, *coeffs)
+    op_name = {hm.COMPUTE_F32: "f32", hm.COMPUTE_F16: "f16", hm.COMPUTE_BF16: "bf16"}[resolved]
+
+    t0 = time.perf_counter()
+    desc, mats = build_workload(args.workload, dev, args.dtype)
+    torch.cuda.synchronize()
+    outs = [torch.empty_like(x) for x in mats]
+    log(f"workload ready in {time.perf_counter() - t0:.1f} s: {len(mats)} matrices")
+
+    rows = [x.shape[0] for x in mats]
+    cols = [x.shape[1] for x in mats]
+    code = hm.BF16 if args.dtype == "bf16" else hm.F32
+    total, bounds = hm.himuon_plan_chunks(rows, cols, args.T, code, int(args.budget))
+    launches = len(bounds) - 1
+    flops_step = sum(6.0 * h * w * args.T * args.K for h, w in zip(rows, cols))
+    elem = 2 if args.dtype == "bf16" else 4
+    bytes_step = sum(2.0 * h * w * elem for h, w in zip(rows, cols))
+
+    ws = torch.empty(hm.himuon_ns_tiled_workspace_size(len(mats)), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        hm.ns_tiled(mats, outputs=outs, T=args.T, K=args.K, coeffs=coeffs, compute=compute,
+                    chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    log(f"timed {args.steps} steps: wall {wall * 1e3:.2f} ms, event median {np.median(step_ms):.3f} ms/step")
+
+    ms_per_step = wall * 1e3 / args.steps
+    value = flops_step / (wall / args.steps) / 1e12
+    # per launch: a step is one descriptor upload plus `launches` kernel launches
+    launch_ms = float(np.mean(step_ms)) / launches
+    flops_launch = flops_step / launches
+    achieved = flops_launch / (launch_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[op_name]
+    tiles_launch = total // launches
+    traffic = traffic_for_launch(args.T, args.K, args.dtype, op_name, tiles_launch)
+
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": op_name,
+        "data": "synthetic",
+        "config": {
+            "workload": desc, "T": args.T, "K": args.K, "matrices": len(mats), "tiles": total,
+            "storage": args.dtype, "mfma_operands": op_name, "accumulate": "f32",
+            "chunk_budget_bytes": int(args.budget), "launches_per_step": launches,
+            "hbm_bytes_per_step": bytes_step, "hbm_GBps_algorithmic": round(bytes_step / (wall / args.steps) / 1e9, 1),
+        },
+        "roofline": {
+            "bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": traffic,
+            "flops_per_launch": flops_launch, "mean_launch_ms": round(launch_ms, 4),
+        },
+    }
+    if args.cpu_seconds > 0:
+        log(f"cpu baseline: oracle on sampled tiles for ~{args.cpu_seconds:.0f} s")
+        rec["cpu_baseline"] = cpu_baseline(mats, args.T, args.K, coeffs, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -107,11 +107,16 @@ int resolve_compute(int dtype, int compute, int K, float a, float b, float c)
     }
     if (compute == HIMUON_COMPUTE_F32) return HIMUON_ERR_UNSUPPORTED;
     if (compute == HIMUON_COMPUTE_BF16) return HIMUON_COMPUTE_BF16;
-    // fp16 operands: X (<= M), A and the A-operand of A^2 (<= M^2) and
-    // B = bA + cA^2 (<= |b| M^2 + |c| M^4) must stay far below 65504.
+    // fp16 operands (kernel state Z = X |c|^(1/4), H = Z Z^T): Z, H,
+    // H + sigma b' I and P = b' H + sigma H^2 must stay far below 65504, and
+    // so must the bf16-operand path's A = X X^T and B = bA + cA^2.
     const double M = 4.0 * iterate_bound(K, a, b, c);
+    const double zs = c != 0.f ? pow(fabs((double)c), 0.25) : 1.0;
+    const double bp = c != 0.f ? fabs((double)b) / sqrt(fabs((double)c)) : fabs((double)b);
+    const double Mz = M * zs, MH = Mz * Mz;
     const double M2 = M * M;
-    const double bound = fmax(fmax(M, M2), fabs((double)b) * M2 + fabs((double)c) * M2 * M2);
+    const double bound = fmax(fmax(fmax(Mz, MH + bp), bp * MH + MH * MH),
+                              fmax(M2, fabs((double)b) * M2 + fabs((double)c) * M2 * M2));
     const bool safe = bound < 16384.0;
     if (compute == HIMUON_COMPUTE_F16) return safe ? HIMUON_COMPUTE_F16 : HIMUON_ERR_RANGE;
     return safe ? HIMUON_COMPUTE_F16 : HIMUON_COMPUTE_BF16;
@@ -280,6 +285,18 @@ int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out
         ka.b = b;
         ka.c = c;
         ka.b_over_c = c != 0.f ? b / c : 0.f;
+        if (c != 0.f) {
+            const double ac = fabs((double)c);
+            ka.zscale = (float)pow(ac, 0.25);
+            ka.unscale = (float)(1.0 / pow(ac, 0.25));
+            ka.sigma = c > 0.f ? 1.f : -1.f;
+            ka.bq = (float)((double)ka.sigma * (double)b / sqrt(ac));
+        } else {
+            ka.zscale = 1.f;
+            ka.unscale = 1.f;
+            ka.sigma = 0.f;
+            ka.bq = b;
+        }
         for (int64_t i = 0; i < n_chunks && status == HIMUON_OK; ++i) {
             ka.tile_begin = chunk_bound(i, total, n_chunks);
             ka.tile_end = chunk_bound(i + 1, total, n_chunks);

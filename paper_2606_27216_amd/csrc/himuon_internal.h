@@ -38,6 +38,12 @@ struct KernelArgs {
     int32_t K;
     float a, b, c;
     float b_over_c;  // b / c, used when c != 0
+    // Rescaled state Z = X |c|^(1/4) (fp16-operand kernel; c != 0):
+    // Z <- aZ + sigma H (H + sigma b' I) Z with H = Z Z^T, b' = b / sqrt|c|.
+    float zscale;    // |c|^(1/4) (1 when c == 0)
+    float unscale;   // 1 / zscale
+    float bq;        // sigma * b' (c != 0) or b (c == 0)
+    float sigma;     // sign(c), 0 when c == 0
 };
 
 // Enqueue one chunk on `stream`. Returns hipErrorInvalidValue for a

@@ -68,15 +68,14 @@ template <> struct OperandTraits<Operand::F32> {
     static constexpr int kChains = 4;
 };
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to nearest even and packed (v_cvt_pk_{f16,bf16}_f32).
 template <Operand OP> HM_DEV uint32_t pack2(float x, float y)
 {
-    if constexpr (OP == Operand::F16) {
-        f16x2 h = {(_Float16)x, (_Float16)y};
-        return __builtin_bit_cast(uint32_t, h);
-    } else {
-        bf16x2 h = {(__bf16)x, (__bf16)y};
-        return __builtin_bit_cast(uint32_t, h);
-    }
+    const f32x2 v = {x, y};
+    if constexpr (OP == Operand::F16) return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2));
+    else return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 // Slot s of a row piece: values 8s..8s+7 (16-bit) or 4s..4s+3 (fp32).
@@ -107,6 +106,15 @@ template <Operand OP> HM_DEV void mma(const u32x4& a, const u32x4& b, f32x16 (&a
         for (int i = 0; i < 4; ++i)
             acc[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[i]), __uint_as_float(b[i]), acc[i], 0, 0, 0);
     }
+}
+
+// One 16-bit MFMA: acc + A_op * B_op.
+template <Operand OP> HM_DEV f32x16 mma1(const u32x4& a, const u32x4& b, const f32x16& acc)
+{
+    if constexpr (OP == Operand::F16)
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
 }
 
 // Sum of the chains, in a fixed pairwise order.
@@ -546,6 +554,282 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
     }
 }
 
+// ------------------------------------------------ fp16-operand kernel
+//
+// Same tile map, restructured so that almost no vector-ALU work is left in
+// the K loop. The state is Z = X |c|^(1/4) (exact rescaling of the iterate),
+// for which one step of eq. (ns_iteration) reads
+//     Z <- a Z + P Z,   P = sigma H (H + sigma b' I),   H = Z Z^T,
+// with b' = b / sqrt|c| and sigma = sign(c): the c-coefficient becomes +-1
+// and b' moves onto the diagonal of an MFMA operand, so the only per-element
+// multiply left is the fp32 a*Z that seeds the product accumulator (the a*Z
+// term stays in fp32, which keeps rounding out of the directions the
+// iteration amplifies). The normalisation multiplies by |c|^(1/4) and the
+// store by |c|^(-1/4). c = 0 takes P = b H.
+//
+// The B X operand (column pieces of Z) comes from a row-major fp16 copy of
+// the tile through ds_read_b64_tr_b16, which returns in every lane quad a
+// 4x4 transpose of four rows supplied by the other lanes of its 16-lane
+// group. The row stride (see kRowStride) spreads the eight rows one read
+// touches over all LDS banks. Gram-type operands of other waves' rows come
+// from 16-byte lane-ordered slots, which Z and then H share. A wave works
+// on the blocks of its row in the rotated order J = (p + j) mod NB, so its
+// own row block (j = 0) is taken from registers.
+
+HM_DEV u32x2 tr_read(const uint8_t* ptr)
+{
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s4* lds_s4p;
+    const s4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4p)(ptr));
+    return __builtin_bit_cast(u32x2, v);
+}
+
+// Descriptor of the matrix owning global tile `tile` (last tile_begin <= tile).
+HM_DEV const MatDesc& find_matrix(const KernelArgs& args, int64_t tile)
+{
+    int lo = 0, hi = args.n_mats - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (args.descs[mid].tile_begin <= tile) lo = mid;
+        else hi = mid - 1;
+    }
+    lo = __builtin_amdgcn_readfirstlane(lo);
+    return args.descs[lo];
+}
+
+// Row-major fp16 copy: bytes per row. A transposing read touches eight
+// consecutive rows, 64 bytes each; a stride of 32 or 64 bytes mod 256 puts
+// them on disjoint bank ranges (two passes of 256 bytes).
+template <int T> constexpr int kRowStride = (T == 32) ? 64 : 2 * T + 32;
+
+// CMODE: 0 for c > 0, 1 for c < 0, 2 for c = 0 (sign(c) and the c = 0
+// shortcut are compile-time, so no branch of the K loop is if-converted).
+template <int T, int CMODE>
+__global__ void __launch_bounds__(kThreads, 2) ns_tiled_f16_kernel(const KernelArgs args)
+{
+    constexpr Storage ST = Storage::BF16;
+    constexpr Operand OP = Operand::F16;
+    constexpr int NB = T / 32;  // row blocks per tile = waves per tile
+    constexpr int TPW = 4 / NB;
+    constexpr int S = 2;
+    constexpr int MAT = NB * NB * S * 64;
+    constexpr bool SHARED = NB > 1;
+    constexpr int RS = kRowStride<T>;
+    constexpr int RM = T * RS;
+
+    __shared__ u32x4 s_slots[SHARED ? TPW * MAT : 1];
+    __shared__ __attribute__((aligned(16))) uint8_t s_rm[TPW * RM];
+    __shared__ float s_red[2][4];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int tslot = wave / NB, p = wave % NB;
+    const int li = lane & 31, lh = lane >> 5;
+    u32x4* const slots = s_slots + (SHARED ? tslot * MAT : 0);
+    uint8_t* const rm = s_rm + tslot * RM;
+    // this lane writes 4-element chunks of row 32p + li at columns 32N + 8g + 4lh
+    uint8_t* const rm_wr = rm + (32 * p + li) * RS + 8 * lh;
+    // transposing reads: supplier lane 4q' + m of 16-lane group G addresses
+    // row 4(G/2) + m, columns 16(G%2) + 4q' of a 32x32 block
+    const int grp16 = lane >> 4;
+    const uint8_t* const rm_tr = rm + (4 * (grp16 >> 1) + ((lane & 15) >> 2)) * RS + 2 * (16 * (grp16 & 1) + 4 * (lane & 3));
+    // sigma b' on the diagonal of the own diagonal block (row piece of row li:
+    // column 8g + 4lh + e sits in register 4g + e)
+    f32x16 dvec;
+    {
+        const bool has_diag = lh == ((li >> 2) & 1);
+        const int vd = 4 * (li >> 3) + (li & 3);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dvec[v] = (has_diag && v == vd) ? args.bq : 0.f;
+    }
+
+    const int64_t n_tiles = args.tile_end - args.tile_begin;
+    const int64_t n_groups = (n_tiles + TPW - 1) / TPW;
+
+    for (int64_t gidx = blockIdx.x; gidx < n_groups; gidx += gridDim.x) {
+        const int64_t local = gidx * TPW + tslot;
+        const bool valid = local < n_tiles;
+        if constexpr (!SHARED || TPW == 1) {
+            if (!valid) continue;
+        }
+        const MatDesc& d = find_matrix(args, args.tile_begin + (valid ? local : 0));
+        const int64_t lt = args.tile_begin + (valid ? local : 0) - d.tile_begin;
+        const int64_t tr = lt / d.tiles_c;
+        const int64_t row0 = tr * T, col0 = (lt - tr * d.tiles_c) * T;
+        const bool full = row0 + T <= d.rows && col0 + T <= d.cols;
+        const bool vin = full && (d.flags & MAT_VEC_IN);
+        const bool vout = full && (d.flags & MAT_VEC_OUT);
+        const int64_t rows_eff = valid ? d.rows : 0;
+        const int64_t gr = row0 + 32 * p + li;
+
+        f32x16 Z[NB];
+#pragma unroll
+        for (int q = 0; q < NB; ++q)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const f32x4 v = load4<ST>(d.in, gr, col0 + 32 * q + 8 * g + 4 * lh, d.ld_in, rows_eff, d.cols, vin);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) Z[q][4 * g + e] = v[e];
+            }
+
+        // Z_0 = |c|^(1/4) S / ||S||_F (exact power-of-two pre-scale first)
+        float mx = 0.f;
+#pragma unroll
+        for (int q = 0; q < NB; ++q)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fabsf(Z[q][v]));
+        mx = wave_max(mx);
+        if constexpr (SHARED) {
+            if (lane == 0) s_red[0][wave] = mx;
+            __syncthreads();
+            mx = s_red[0][tslot * NB];
+#pragma unroll
+            for (int w = 1; w < NB; ++w) mx = fmaxf(mx, s_red[0][tslot * NB + w]);
+        }
+        int ex = 0;
+        (void)frexpf(mx, &ex);
+        const float s1 = ldexpf(1.f, -(ex / 2)), s2 = ldexpf(1.f, -(ex - ex / 2));
+        float ss = 0.f;
+#pragma unroll
+        for (int q = 0; q < NB; ++q)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float y = Z[q][v] * s1 * s2;
+                Z[q][v] = y;
+                ss = fmaf(y, y, ss);
+            }
+        ss = wave_sum(ss);
+        if constexpr (SHARED) {
+            if (lane == 0) s_red[1][wave] = ss;
+            __syncthreads();
+            ss = s_red[1][tslot * NB];
+#pragma unroll
+            for (int w = 1; w < NB; ++w) ss += s_red[1][tslot * NB + w];
+        }
+        const float inv = ss > 0.f ? args.zscale / sqrtf(ss) : 0.f;  // Phi_K(0) = 0
+#pragma unroll
+        for (int q = 0; q < NB; ++q) Z[q] *= inv;
+
+        for (int k = 0; k < args.K; ++k) {
+            u32x4 Zop[NB][S];
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int s = 0; s < S; ++s) Zop[q][s] = make_slot<OP>(Z[q], s);
+#pragma unroll
+            for (int N = 0; N < NB; ++N)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    *reinterpret_cast<u32x2*>(rm_wr + 64 * N + 16 * g) =
+                        u32x2{Zop[N][g >> 1][(g & 1) * 2], Zop[N][g >> 1][(g & 1) * 2 + 1]};
+            if constexpr (SHARED) {
+#pragma unroll
+                for (int q = 0; q < NB; ++q)
+#pragma unroll
+                    for (int s = 0; s < S; ++s) slots[((p * NB + q) * S + s) * 64 + lane] = Zop[q][s];
+                __syncthreads();
+            }
+
+            // H = Z Z^T; G[j] is the row piece of block (p, (p + j) mod NB)
+            f32x16 G[NB];
+#pragma unroll
+            for (int j = 0; j < NB; ++j) G[j] = f32x16{};
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int s = 0; s < S; ++s)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        const int J = (p + j) % NB;
+                        const u32x4 opa = j == 0 ? Zop[q][s] : slots[((J * NB + q) * S + s) * 64 + lane];
+                        G[j] = mma1<OP>(opa, Zop[q][s], G[j]);
+                    }
+
+            u32x4 Pop[NB][S];  // own rows of P (rotated blocks), fp16
+            if constexpr (CMODE != 2) {
+                u32x4 Hop[NB][S], Q0[S];
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Hop[j][s] = make_slot<OP>(G[j], s);
+                {
+                    const f32x16 g0 = G[0] + dvec;  // H + sigma b' I on the diagonal block
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Q0[s] = make_slot<OP>(g0, s);
+                }
+                if constexpr (SHARED) {
+                    __syncthreads();  // every wave is done reading Z from the slots
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) slots[((p * NB + (p + j) % NB) * S + s) * 64 + lane] = Hop[j][s];
+                    __syncthreads();
+                }
+                // P' = H (H + sigma b' I), block (p, (p + j) mod NB) in acc[j]
+                f32x16 acc[NB];
+#pragma unroll
+                for (int j = 0; j < NB; ++j) acc[j] = f32x16{};
+#pragma unroll
+                for (int jk = 0; jk < NB; ++jk)
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        const u32x4 opb = jk == 0 ? Q0[s] : Hop[jk][s];
+                        const int KB = (p + jk) % NB;
+#pragma unroll
+                        for (int j = 0; j < NB; ++j) {
+                            const int J = (p + j) % NB;
+                            const u32x4 opa = j == 0 ? Hop[jk][s] : slots[((J * NB + KB) * S + s) * 64 + lane];
+                            acc[j] = mma1<OP>(opa, opb, acc[j]);
+                        }
+                    }
+                if constexpr (CMODE == 0) {
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) Pop[j][s] = make_slot<OP>(acc[j], s);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) Pop[j][s] = make_slot<OP>(-acc[j], s);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Pop[j][s] = make_slot<OP>(G[j] * args.bq, s);
+            }
+
+            // Z <- a Z + P Z; the k-blocks of P follow the rotated order
+#pragma unroll
+            for (int N = 0; N < NB; ++N) Z[N] *= args.a;
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                const uint8_t* const kb = rm_tr + 32 * ((p + j) % NB) * RS;
+#pragma unroll
+                for (int s = 0; s < S; ++s)
+#pragma unroll
+                    for (int N = 0; N < NB; ++N) {
+                        const u32x2 lo = tr_read(kb + 16 * s * RS + 64 * N);
+                        const u32x2 hi = tr_read(kb + (16 * s + 8) * RS + 64 * N);
+                        Z[N] = mma1<OP>(u32x4{lo[0], lo[1], hi[0], hi[1]}, Pop[j][s], Z[N]);
+                    }
+            }
+            if constexpr (SHARED) __syncthreads();  // slots and the row-major copy are rewritten next step
+        }
+
+        if (valid) {
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f32x4 v = {Z[q][4 * g + 0], Z[q][4 * g + 1], Z[q][4 * g + 2], Z[q][4 * g + 3]};
+                    store4<ST>(d.out, gr, col0 + 32 * q + 8 * g + 4 * lh, d.ld_out, d.rows, d.cols, vout, v * args.unscale);
+                }
+        }
+    }
+}
+
 // ----------------------------------------------------------------- launch
 
 constexpr int kMaxDevices = 64;
@@ -578,6 +862,33 @@ hipError_t launch_one(const KernelArgs& args, hipStream_t stream)
     return hipGetLastError();
 }
 
+template <int T, int CMODE>
+hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
+{
+    constexpr int TPW = 4 / (T / 32);
+    static std::atomic<int> resident[kMaxDevices];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    int cap = resident[dev].load(std::memory_order_relaxed);
+    if (cap == 0) {
+        int per_cu = 0, cus = 0;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ns_tiled_f16_kernel<T, CMODE>, kThreads, 0);
+        if (e != hipSuccess) return e;
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        cap = (per_cu < 1 ? 1 : per_cu) * (cus < 1 ? 1 : cus);
+        resident[dev].store(cap, std::memory_order_relaxed);
+    }
+    const int64_t n = args.tile_end - args.tile_begin;
+    if (n <= 0) return hipSuccess;
+    const int64_t groups = (n + TPW - 1) / TPW;
+    const int grid = (int)(groups < cap ? groups : cap);
+    hipLaunchKernelGGL((ns_tiled_f16_kernel<T, CMODE>), dim3(grid), dim3(kThreads), 0, stream, args);
+    return hipGetLastError();
+}
+
 // Kernel choice per tile size: rows of a T <= 64 tile stay in one wave (no
 // workgroup barriers); a T = 128 tile is split over four waves.
 template <Storage ST, Operand OP>
@@ -605,7 +916,21 @@ hipError_t launch_ns_tiled(int T, Storage st, Operand op, const KernelArgs& args
 {
     if (!has_kernel(T, st, op)) return hipErrorInvalidValue;
     if (st == Storage::F32) return launch_T<Storage::F32, Operand::F32>(T, args, stream);
-    if (op == Operand::F16) return launch_T<Storage::BF16, Operand::F16>(T, args, stream);
+    if (op == Operand::F16) {
+        const int cm = args.c > 0.f ? 0 : (args.c < 0.f ? 1 : 2);
+        switch (T * 4 + cm) {
+        case 32 * 4 + 0: return launch_f16<32, 0>(args, stream);
+        case 32 * 4 + 1: return launch_f16<32, 1>(args, stream);
+        case 32 * 4 + 2: return launch_f16<32, 2>(args, stream);
+        case 64 * 4 + 0: return launch_f16<64, 0>(args, stream);
+        case 64 * 4 + 1: return launch_f16<64, 1>(args, stream);
+        case 64 * 4 + 2: return launch_f16<64, 2>(args, stream);
+        case 128 * 4 + 0: return launch_f16<128, 0>(args, stream);
+        case 128 * 4 + 1: return launch_f16<128, 1>(args, stream);
+        case 128 * 4 + 2: return launch_f16<128, 2>(args, stream);
+        default: return hipErrorInvalidValue;
+        }
+    }
     return launch_T<Storage::BF16, Operand::BF16>(T, args, stream);
 }
 

@@ -245,7 +245,9 @@ int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out
     if (s != HIMUON_OK) return s;
 
     // ---- descriptor table
-    const size_t align = dtype == HIMUON_BF16 ? 8 : 16;
+    // 16-byte accesses at every column multiple of 8 (bf16) or 4 (f32)
+    const size_t align = 16;
+    const int64_t ld_mult = dtype == HIMUON_BF16 ? 8 : 4;
     std::vector<MatDesc> descs((size_t)n_mats);
     for (int64_t m = 0; m < n_mats; ++m) {
         MatDesc& d = descs[(size_t)m];
@@ -258,8 +260,8 @@ int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out
         d.tile_begin = begin[(size_t)m];
         d.tiles_c = (int32_t)ceil_div(cols[m], T);
         d.flags = 0;
-        if ((uintptr_t)d.in % align == 0 && d.ld_in % 4 == 0) d.flags |= himuon::MAT_VEC_IN;
-        if ((uintptr_t)d.out % align == 0 && d.ld_out % 4 == 0) d.flags |= himuon::MAT_VEC_OUT;
+        if ((uintptr_t)d.in % align == 0 && d.ld_in % ld_mult == 0) d.flags |= himuon::MAT_VEC_IN;
+        if ((uintptr_t)d.out % align == 0 && d.ld_out % ld_mult == 0) d.flags |= himuon::MAT_VEC_OUT;
         if (ceil_div(cols[m], T) > INT32_MAX) return HIMUON_ERR_INVALID_ARG;
     }
 

@@ -21,8 +21,8 @@ struct alignas(64) MatDesc {
 };
 static_assert(sizeof(MatDesc) == 64, "descriptor layout");
 
-// Base pointer and leading dimension allow 4-element vector accesses at every
-// column that is a multiple of 4 (8-byte aligned for bf16, 16-byte for f32).
+// Base pointer and leading dimension allow 16-byte accesses at every column
+// that is a multiple of 8 (bf16) or 4 (f32).
 constexpr int32_t MAT_VEC_IN = 1;
 constexpr int32_t MAT_VEC_OUT = 2;
 

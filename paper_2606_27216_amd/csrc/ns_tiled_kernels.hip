@@ -37,6 +37,7 @@
 #include "himuon_internal.h"
 
 #include <atomic>
+#include <type_traits>
 #include <math.h>
 
 namespace himuon {
@@ -567,14 +568,73 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
 // iteration amplifies). The normalisation multiplies by |c|^(1/4) and the
 // store by |c|^(-1/4). c = 0 takes P = b H.
 //
-// The B X operand (column pieces of Z) comes from a row-major fp16 copy of
-// the tile through ds_read_b64_tr_b16, which returns in every lane quad a
-// 4x4 transpose of four rows supplied by the other lanes of its 16-lane
-// group. The row stride (see kRowStride) spreads the eight rows one read
-// touches over all LDS banks. Gram-type operands of other waves' rows come
-// from 16-byte lane-ordered slots, which Z and then H share. A wave works
-// on the blocks of its row in the rotated order J = (p + j) mod NB, so its
-// own row block (j = 0) is taken from registers.
+// Z is shared through one row-major fp16 copy of the tile (see kRowStride).
+// Gram operands of the other waves' rows are read from it as row pieces; the
+// B X operand (column pieces of Z) comes from it through ds_read_b64_tr_b16,
+// which returns in every lane quad a 4x4 transpose of four rows supplied by
+// the other lanes of its 16-lane group. H is shared through 16-byte
+// lane-ordered slots. A wave works on the blocks of its row in the rotated
+// order J = (p + j) mod NB, so its own row blocks come from registers.
+//
+// Tiles are processed in rounds; the HBM loads of a wave's next tile are
+// issued during the product of the current tile's last step.
+
+// 64-bit DPP move (both halves with the same control).
+template <int CTRL> HM_DEV double dpp_f64(double v)
+{
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)u, CTRL, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+HM_DEV double readlane_f64(double v, int l)
+{
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// Sum over the 64 lanes in a fixed order: butterflies inside each 16-lane
+// row (quad swaps, half-row and row mirrors), then the four row sums.
+HM_DEV double wave_sum_f64(double v)
+{
+    v += dpp_f64<0xB1>(v);   // quad_perm [1,0,3,2]
+    v += dpp_f64<0x4E>(v);   // quad_perm [2,3,0,1]
+    v += dpp_f64<0x141>(v);  // row_half_mirror
+    v += dpp_f64<0x140>(v);  // row_mirror
+    return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
+}
+
+// Matrix owning `tile`, searching from `hint` (the tiles one wave visits only
+// grow, so the owner of an earlier tile is a lower bound).
+HM_DEV int find_matrix_from(const KernelArgs& args, int64_t tile, int hint)
+{
+    if (hint + 1 >= args.n_mats || args.descs[hint + 1].tile_begin > tile) return hint;
+    int lo = hint + 1, hi = args.n_mats - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (args.descs[mid].tile_begin <= tile) lo = mid;
+        else hi = mid - 1;
+    }
+    return __builtin_amdgcn_readfirstlane(lo);
+}
+
+// Four consecutive bf16 elements of row gr (columns gc..gc+3) as two packed
+// words, zero outside the matrix (the zero padding of the tiling operator).
+HM_DEV u32x2 load_bf16x4(const void* base, int64_t gr, int64_t gc, int64_t ld, int64_t rows, int64_t cols, bool vec)
+{
+    const uint16_t* p = static_cast<const uint16_t*>(base) + gr * ld + gc;
+    if (vec) return *reinterpret_cast<const u32x2*>(p);
+    uint32_t h[4] = {0u, 0u, 0u, 0u};
+    if (gr < rows) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (gc + e < cols) h[e] = p[e];
+    }
+    return u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+}
 
 HM_DEV u32x2 tr_read(const uint8_t* ptr)
 {
@@ -584,249 +644,418 @@ HM_DEV u32x2 tr_read(const uint8_t* ptr)
     return __builtin_bit_cast(u32x2, v);
 }
 
-// Descriptor of the matrix owning global tile `tile` (last tile_begin <= tile).
-HM_DEV const MatDesc& find_matrix(const KernelArgs& args, int64_t tile)
-{
-    int lo = 0, hi = args.n_mats - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (args.descs[mid].tile_begin <= tile) lo = mid;
-        else hi = mid - 1;
-    }
-    lo = __builtin_amdgcn_readfirstlane(lo);
-    return args.descs[lo];
-}
+// Row-major fp16 copy of Z. Bytes per row: an odd multiple of 64, so the
+// eight consecutive rows a transposing read touches (64 bytes each) fall on
+// four distinct quarters of the 256-byte bank space, twice each. Within each
+// 64-byte segment (32 columns) the 8-byte chunk c of row r sits at chunk
+// c ^ 2((r >> 2) & 3): rows r, r+4, ..., r+28 share a quarter, and the XOR
+// spreads their row-piece chunks (2g + lh) over all eight chunks, so
+// row-piece reads and writes (32 rows x 16 bytes) are conflict-free as well.
+template <int T> constexpr int kRowStride = ((2 * T / 64) % 2 == 1) ? 2 * T : 2 * T + 64;
 
-// Row-major fp16 copy: bytes per row. A transposing read touches eight
-// consecutive rows, 64 bytes each; a stride of 32 or 64 bytes mod 256 puts
-// them on disjoint bank ranges (two passes of 256 bytes).
-template <int T> constexpr int kRowStride = (T == 32) ? 64 : 2 * T + 32;
+// A wave that owns two row blocks of a 128-tile needs more than 256
+// registers; everything else runs two waves per SIMD.
+template <int T, int RB> constexpr int kF16MinBlocks = (T / 32) / RB == 2 ? 1 : 2;
 
 // CMODE: 0 for c > 0, 1 for c < 0, 2 for c = 0 (sign(c) and the c = 0
 // shortcut are compile-time, so no branch of the K loop is if-converted).
-template <int T, int CMODE>
-__global__ void __launch_bounds__(kThreads, 2) ns_tiled_f16_kernel(const KernelArgs args)
+// RB: 32-row blocks owned by one wave; a tile is spread over NB / RB waves.
+// Every operand read from LDS feeds RB MFMAs.
+template <int T, int RB, int CMODE>
+__global__ void __launch_bounds__(kThreads, (kF16MinBlocks<T, RB>)) ns_tiled_f16_kernel(const KernelArgs args)
 {
     constexpr Storage ST = Storage::BF16;
     constexpr Operand OP = Operand::F16;
-    constexpr int NB = T / 32;  // row blocks per tile = waves per tile
-    constexpr int TPW = 4 / NB;
+    constexpr int NB = T / 32;      // row blocks per tile
+    constexpr int WT = NB / RB;     // waves per tile
+    static_assert(NB % RB == 0 && WT >= 1 && WT <= 4, "tile split");
+    constexpr int TPW = 4 / WT;     // tiles per workgroup
     constexpr int S = 2;
-    constexpr int MAT = NB * NB * S * 64;
-    constexpr bool SHARED = NB > 1;
+    constexpr int MAT = NB * NB * S * 64;  // 16-byte slots of H
+    constexpr bool SHARED = WT > 1;
+    static_assert(!SHARED || TPW == 1, "a workgroup that shares a tile runs one tile");
+    constexpr int NO = NB - RB;     // row blocks owned by the other waves of the tile
+    constexpr int NOA = NO > 0 ? NO : 1;
     constexpr int RS = kRowStride<T>;
     constexpr int RM = T * RS;
+    constexpr int IT = NB * S;      // k iterations of one product
 
     __shared__ u32x4 s_slots[SHARED ? TPW * MAT : 1];
     __shared__ __attribute__((aligned(16))) uint8_t s_rm[TPW * RM];
-    __shared__ float s_red[2][4];
+    __shared__ double s_red64[4];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int tslot = wave / NB, p = wave % NB;
+    const int tslot = wave / WT, p0 = (wave % WT) * RB;
     const int li = lane & 31, lh = lane >> 5;
     u32x4* const slots = s_slots + (SHARED ? tslot * MAT : 0);
     uint8_t* const rm = s_rm + tslot * RM;
-    // this lane writes 4-element chunks of row 32p + li at columns 32N + 8g + 4lh
-    uint8_t* const rm_wr = rm + (32 * p + li) * RS + 8 * lh;
-    // transposing reads: supplier lane 4q' + m of 16-lane group G addresses
-    // row 4(G/2) + m, columns 16(G%2) + 4q' of a 32x32 block
-    const int grp16 = lane >> 4;
-    const uint8_t* const rm_tr = rm + (4 * (grp16 >> 1) + ((lane & 15) >> 2)) * RS + 2 * (16 * (grp16 & 1) + 4 * (lane & 3));
-    // sigma b' on the diagonal of the own diagonal block (row piece of row li:
-    // column 8g + 4lh + e sits in register 4g + e)
-    f32x16 dvec;
-    {
-        const bool has_diag = lh == ((li >> 2) & 1);
-        const int vd = 4 * (li >> 3) + (li & 3);
+    // Row pieces: this lane's columns 32q + 8g + 4lh of row li of a block are
+    // chunk 2g + lh of the block's segment, stored at chunk 2(g ^ fl) + lh.
+    const int fl = (li >> 2) & 3;
+    int rp_off[4];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) dvec[v] = (has_diag && v == vd) ? args.bq : 0.f;
+    for (int g = 0; g < 4; ++g) rp_off[g] = li * RS + 16 * (g ^ fl) + 8 * lh;
+    // Transposing reads: supplier lane 4q' + m of 16-lane group G addresses
+    // row 4(G/2) + m (+ 8x) and logical chunk 4(G%2) + q' of a block segment.
+    const int grp16 = lane >> 4;
+    int tr_off[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        const int row = 8 * x + 4 * (grp16 >> 1) + ((lane & 15) >> 2);
+        const int chunk = 4 * (grp16 & 1) + (lane & 3);
+        tr_off[x] = row * RS + 8 * (chunk ^ (2 * ((row >> 2) & 3)));
     }
+    // A diagonal block holds row li's column 8g + 4lh + e in register 4g + e,
+    // so the diagonal entry of this lane (if any) is register vdiag.
+    const int vdiag = (lh == ((li >> 2) & 1)) ? 4 * (li >> 3) + (li & 3) : -1;
+    // the row blocks owned by the other waves, in rotated order: H slots and
+    // the rows of the row-major copy
+    u32x4* sl_row[NOA];
+    const uint8_t* rm_row[NOA];
+#pragma unroll
+    for (int jo = 0; jo < NOA; ++jo) {
+        sl_row[jo] = slots + (((p0 + RB + jo) % NB) * NB * S) * 64 + lane;
+        rm_row[jo] = rm + 32 * ((p0 + RB + jo) % NB) * RS;
+    }
+    auto rowpiece = [&](const uint8_t* blockrow, int q, int s) -> u32x4 {
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(blockrow + rp_off[2 * s] + 64 * q);
+        const u32x2 hi = *reinterpret_cast<const u32x2*>(blockrow + rp_off[2 * s + 1] + 64 * q);
+        return u32x4{lo[0], lo[1], hi[0], hi[1]};
+    };
 
     const int64_t n_tiles = args.tile_end - args.tile_begin;
-    const int64_t n_groups = (n_tiles + TPW - 1) / TPW;
 
-    for (int64_t gidx = blockIdx.x; gidx < n_groups; gidx += gridDim.x) {
-        const int64_t local = gidx * TPW + tslot;
-        const bool valid = local < n_tiles;
-        if constexpr (!SHARED || TPW == 1) {
-            if (!valid) continue;
-        }
-        const MatDesc& d = find_matrix(args, args.tile_begin + (valid ? local : 0));
-        const int64_t lt = args.tile_begin + (valid ? local : 0) - d.tile_begin;
-        const int64_t tr = lt / d.tiles_c;
-        const int64_t row0 = tr * T, col0 = (lt - tr * d.tiles_c) * T;
-        const bool full = row0 + T <= d.rows && col0 + T <= d.cols;
-        const bool vin = full && (d.flags & MAT_VEC_IN);
-        const bool vout = full && (d.flags & MAT_VEC_OUT);
-        const int64_t rows_eff = valid ? d.rows : 0;
-        const int64_t gr = row0 + 32 * p + li;
-
-        f32x16 Z[NB];
+    // Tile placement. The tile of the next round is located, and its HBM
+    // loads are issued, while the current tile is still in its last step.
+    struct TileLoc {
+        const MatDesc* d;
+        int64_t row0, col0;
+        bool vin, vout;
+    };
+    int mhint = 0;
+    auto locate = [&](int64_t local, TileLoc& L) {
+        const int64_t tile = args.tile_begin + local;
+        mhint = find_matrix_from(args, tile, mhint);
+        L.d = &args.descs[mhint];
+        const int64_t lt = tile - L.d->tile_begin;
+        const int64_t tr = lt / L.d->tiles_c;
+        L.row0 = tr * T;
+        L.col0 = (lt - tr * L.d->tiles_c) * T;
+        const bool full = L.row0 + T <= L.d->rows && L.col0 + T <= L.d->cols;
+        L.vin = full && (L.d->flags & MAT_VEC_IN);
+        L.vout = full && (L.d->flags & MAT_VEC_OUT);
+    };
+    // HBM traffic in whole row segments: a lane moves 16 bytes (8 bf16), a
+    // row takes LPR lanes and one wave instruction RPI rows. The wave's own
+    // RB row blocks take NI instructions; the row pieces are then reshaped
+    // through the wave's own rows of the row-major copy.
+    constexpr int LPR = T / 8;
+    constexpr int RPI = 64 / LPR;
+    constexpr int NI = 32 * RB / RPI;
+    const int io_row = lane / LPR, io_cc = lane % LPR;  // row within an instruction, 16-byte chunk
+    u32x4 raw[NI];
+    auto issue_loads = [&](const TileLoc& L) {
 #pragma unroll
-        for (int q = 0; q < NB; ++q)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const f32x4 v = load4<ST>(d.in, gr, col0 + 32 * q + 8 * g + 4 * lh, d.ld_in, rows_eff, d.cols, vin);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) Z[q][4 * g + e] = v[e];
-            }
-
-        // Z_0 = |c|^(1/4) S / ||S||_F (exact power-of-two pre-scale first)
-        float mx = 0.f;
-#pragma unroll
-        for (int q = 0; q < NB; ++q)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fabsf(Z[q][v]));
-        mx = wave_max(mx);
-        if constexpr (SHARED) {
-            if (lane == 0) s_red[0][wave] = mx;
-            __syncthreads();
-            mx = s_red[0][tslot * NB];
-#pragma unroll
-            for (int w = 1; w < NB; ++w) mx = fmaxf(mx, s_red[0][tslot * NB + w]);
-        }
-        int ex = 0;
-        (void)frexpf(mx, &ex);
-        const float s1 = ldexpf(1.f, -(ex / 2)), s2 = ldexpf(1.f, -(ex - ex / 2));
-        float ss = 0.f;
-#pragma unroll
-        for (int q = 0; q < NB; ++q)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const float y = Z[q][v] * s1 * s2;
-                Z[q][v] = y;
-                ss = fmaf(y, y, ss);
-            }
-        ss = wave_sum(ss);
-        if constexpr (SHARED) {
-            if (lane == 0) s_red[1][wave] = ss;
-            __syncthreads();
-            ss = s_red[1][tslot * NB];
-#pragma unroll
-            for (int w = 1; w < NB; ++w) ss += s_red[1][tslot * NB + w];
-        }
-        const float inv = ss > 0.f ? args.zscale / sqrtf(ss) : 0.f;  // Phi_K(0) = 0
-#pragma unroll
-        for (int q = 0; q < NB; ++q) Z[q] *= inv;
-
-        for (int k = 0; k < args.K; ++k) {
-            u32x4 Zop[NB][S];
-#pragma unroll
-            for (int q = 0; q < NB; ++q)
-#pragma unroll
-                for (int s = 0; s < S; ++s) Zop[q][s] = make_slot<OP>(Z[q], s);
-#pragma unroll
-            for (int N = 0; N < NB; ++N)
-#pragma unroll
-                for (int g = 0; g < 4; ++g)
-                    *reinterpret_cast<u32x2*>(rm_wr + 64 * N + 16 * g) =
-                        u32x2{Zop[N][g >> 1][(g & 1) * 2], Zop[N][g >> 1][(g & 1) * 2 + 1]};
-            if constexpr (SHARED) {
-#pragma unroll
-                for (int q = 0; q < NB; ++q)
-#pragma unroll
-                    for (int s = 0; s < S; ++s) slots[((p * NB + q) * S + s) * 64 + lane] = Zop[q][s];
-                __syncthreads();
-            }
-
-            // H = Z Z^T; G[j] is the row piece of block (p, (p + j) mod NB)
-            f32x16 G[NB];
-#pragma unroll
-            for (int j = 0; j < NB; ++j) G[j] = f32x16{};
-#pragma unroll
-            for (int q = 0; q < NB; ++q)
-#pragma unroll
-                for (int s = 0; s < S; ++s)
-#pragma unroll
-                    for (int j = 0; j < NB; ++j) {
-                        const int J = (p + j) % NB;
-                        const u32x4 opa = j == 0 ? Zop[q][s] : slots[((J * NB + q) * S + s) * 64 + lane];
-                        G[j] = mma1<OP>(opa, Zop[q][s], G[j]);
-                    }
-
-            u32x4 Pop[NB][S];  // own rows of P (rotated blocks), fp16
-            if constexpr (CMODE != 2) {
-                u32x4 Hop[NB][S], Q0[S];
-#pragma unroll
-                for (int j = 0; j < NB; ++j)
-#pragma unroll
-                    for (int s = 0; s < S; ++s) Hop[j][s] = make_slot<OP>(G[j], s);
-                {
-                    const f32x16 g0 = G[0] + dvec;  // H + sigma b' I on the diagonal block
-#pragma unroll
-                    for (int s = 0; s < S; ++s) Q0[s] = make_slot<OP>(g0, s);
-                }
-                if constexpr (SHARED) {
-                    __syncthreads();  // every wave is done reading Z from the slots
-#pragma unroll
-                    for (int j = 0; j < NB; ++j)
-#pragma unroll
-                        for (int s = 0; s < S; ++s) slots[((p * NB + (p + j) % NB) * S + s) * 64 + lane] = Hop[j][s];
-                    __syncthreads();
-                }
-                // P' = H (H + sigma b' I), block (p, (p + j) mod NB) in acc[j]
-                f32x16 acc[NB];
-#pragma unroll
-                for (int j = 0; j < NB; ++j) acc[j] = f32x16{};
-#pragma unroll
-                for (int jk = 0; jk < NB; ++jk)
-#pragma unroll
-                    for (int s = 0; s < S; ++s) {
-                        const u32x4 opb = jk == 0 ? Q0[s] : Hop[jk][s];
-                        const int KB = (p + jk) % NB;
-#pragma unroll
-                        for (int j = 0; j < NB; ++j) {
-                            const int J = (p + j) % NB;
-                            const u32x4 opa = j == 0 ? Hop[jk][s] : slots[((J * NB + KB) * S + s) * 64 + lane];
-                            acc[j] = mma1<OP>(opa, opb, acc[j]);
-                        }
-                    }
-                if constexpr (CMODE == 0) {
-#pragma unroll
-                    for (int j = 0; j < NB; ++j)
-#pragma unroll
-                        for (int s = 0; s < S; ++s) Pop[j][s] = make_slot<OP>(acc[j], s);
-                } else {
-#pragma unroll
-                    for (int j = 0; j < NB; ++j)
-#pragma unroll
-                        for (int s = 0; s < S; ++s) Pop[j][s] = make_slot<OP>(-acc[j], s);
-                }
+        for (int i = 0; i < NI; ++i) {
+            const int64_t gr = L.row0 + 32 * p0 + RPI * i + io_row;
+            const int64_t gc = L.col0 + 8 * io_cc;
+            const uint16_t* ptr = static_cast<const uint16_t*>(L.d->in) + gr * L.d->ld_in + gc;
+            if (L.vin) {
+                raw[i] = *reinterpret_cast<const u32x4*>(ptr);
             } else {
+                uint32_t h[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+                if (gr < L.d->rows) {
 #pragma unroll
-                for (int j = 0; j < NB; ++j)
-#pragma unroll
-                    for (int s = 0; s < S; ++s) Pop[j][s] = make_slot<OP>(G[j] * args.bq, s);
+                    for (int e = 0; e < 8; ++e)
+                        if (gc + e < L.d->cols) h[e] = ptr[e];
+                }
+                raw[i] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
             }
-
-            // Z <- a Z + P Z; the k-blocks of P follow the rotated order
-#pragma unroll
-            for (int N = 0; N < NB; ++N) Z[N] *= args.a;
-#pragma unroll
-            for (int j = 0; j < NB; ++j) {
-                const uint8_t* const kb = rm_tr + 32 * ((p + j) % NB) * RS;
-#pragma unroll
-                for (int s = 0; s < S; ++s)
-#pragma unroll
-                    for (int N = 0; N < NB; ++N) {
-                        const u32x2 lo = tr_read(kb + 16 * s * RS + 64 * N);
-                        const u32x2 hi = tr_read(kb + (16 * s + 8) * RS + 64 * N);
-                        Z[N] = mma1<OP>(u32x4{lo[0], lo[1], hi[0], hi[1]}, Pop[j][s], Z[N]);
-                    }
-            }
-            if constexpr (SHARED) __syncthreads();  // slots and the row-major copy are rewritten next step
         }
+    };
+    // byte offset of the 16-byte chunk io_cc of tile row `row` in the row-major copy
+    auto io_lds = [&](int row) -> int {
+        return row * RS + 64 * (io_cc >> 2) + 8 * ((2 * (io_cc & 3)) ^ (2 * ((row >> 2) & 3)));
+    };
 
-        if (valid) {
+    int64_t local = (int64_t)blockIdx.x * TPW + tslot;
+    if (local >= n_tiles) return;  // uniform over the waves that share a tile
+    TileLoc cur;
+    locate(local, cur);
+    issue_loads(cur);
+
+    for (;;) {
+        const int64_t nlocal = local + (int64_t)gridDim.x * TPW;
+        const bool has_next = nlocal < n_tiles;
+        TileLoc nxt = cur;
+        if (has_next) locate(nlocal, nxt);
+
+        // own rows into the row-major copy, then back as row pieces (bf16 -> fp32);
+        // only this wave touches these rows until its first step's barrier
+#pragma unroll
+        for (int i = 0; i < NI; ++i) *reinterpret_cast<u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row)) = raw[i];
+        f32x16 Z[RB][NB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int q = 0; q < NB; ++q)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
-                    const f32x4 v = {Z[q][4 * g + 0], Z[q][4 * g + 1], Z[q][4 * g + 2], Z[q][4 * g + 3]};
-                    store4<ST>(d.out, gr, col0 + 32 * q + 8 * g + 4 * lh, d.ld_out, d.rows, d.cols, vout, v * args.unscale);
+                    const u32x2 w = *reinterpret_cast<const u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q);
+                    Z[rb][q][4 * g + 0] = __uint_as_float(w[0] << 16);
+                    Z[rb][q][4 * g + 1] = __uint_as_float(w[0] & 0xffff0000u);
+                    Z[rb][q][4 * g + 2] = __uint_as_float(w[1] << 16);
+                    Z[rb][q][4 * g + 3] = __uint_as_float(w[1] & 0xffff0000u);
                 }
+
+        // Z_0 = |c|^(1/4) S / ||S||_F. The sum of squares is taken in fp64,
+        // whose range covers every bf16 tile; the scale is applied as an fp32
+        // mantissa times an exact power of two.
+        double ss = 0.0;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) ss = fma((double)Z[rb][q][v], (double)Z[rb][q][v], ss);
+        ss = wave_sum_f64(ss);
+        if constexpr (SHARED) {
+            if (lane == 0) s_red64[wave] = ss;
+            __syncthreads();
+            ss = s_red64[tslot * WT];
+#pragma unroll
+            for (int w = 1; w < WT; ++w) ss += s_red64[tslot * WT + w];
         }
+        {
+            const double nrm = sqrt(ss);
+            int ex = 0;
+            const float mant = nrm == 0.0 ? 0.f : (float)frexp((double)args.zscale / nrm, &ex);  // Phi_K(0) = 0
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int q = 0; q < NB; ++q)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) Z[rb][q][v] = ldexpf(Z[rb][q][v] * mant, ex);
+        }
+
+        // One Newton-Schulz step. The last one is a separate instance, so the
+        // registers of the next tile's loads are live only there.
+        auto ns_step = [&](auto last_tag) {
+            constexpr bool LAST = decltype(last_tag)::value;
+            u32x4 Zop[RB][NB][S];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int q = 0; q < NB; ++q)
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Zop[rb][q][s] = make_slot<OP>(Z[rb][q], s);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int N = 0; N < NB; ++N)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * N) =
+                            u32x2{Zop[rb][N][g >> 1][(g & 1) * 2], Zop[rb][N][g >> 1][(g & 1) * 2 + 1]};
+            if constexpr (SHARED) __syncthreads();
+
+            // H = Z Z^T; G[rb][j] is the row piece of block (p0 + rb, (p0 + j) mod NB).
+            // Iteration it = (q, s) reads the other waves' row pieces (q, s) from
+            // the row-major copy; those of iteration it + 1 are requested before
+            // its MFMAs issue.
+            f32x16 G[RB][NB];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int j = 0; j < NB; ++j) G[rb][j] = f32x16{};
+            {
+                u32x4 nxt_op[NOA];
+                if constexpr (NO > 0) {
+#pragma unroll
+                    for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = rowpiece(rm_row[jo], 0, 0);
+                }
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int q = it / S, s = it % S;
+                    u32x4 cur_op[NOA];
+#pragma unroll
+                    for (int jo = 0; jo < NOA; ++jo) cur_op[jo] = nxt_op[jo];
+                    if constexpr (NO > 0) {
+                        if (it + 1 < IT) {
+#pragma unroll
+                            for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = rowpiece(rm_row[jo], (it + 1) / S, (it + 1) % S);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of these MFMAs
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        const u32x4 opa = j < RB ? Zop[j < RB ? j : 0][q][s] : cur_op[j < RB ? 0 : j - RB];
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb) G[rb][j] = mma1<OP>(opa, Zop[rb][q][s], G[rb][j]);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+
+            u32x4 Pop[RB][NB][S];  // own rows of P (rotated k-blocks), fp16
+            if constexpr (CMODE != 2) {
+                u32x4 Hop[RB][NB][S], Q0[RB][S];
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) Hop[rb][j][s] = make_slot<OP>(G[rb][j], s);
+                    f32x16 gd = G[rb][rb];  // H + sigma b' I on the diagonal block (p0 + rb, p0 + rb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) gd[v] += v == vdiag ? args.bq : 0.f;
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Q0[rb][s] = make_slot<OP>(gd, s);
+                }
+                if constexpr (SHARED) {
+                    // the H slots were last read before the previous step's final barrier
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int j = 0; j < NB; ++j)
+#pragma unroll
+                            for (int s = 0; s < S; ++s)
+                                slots[(((p0 + rb) * NB + (p0 + j) % NB) * S + s) * 64 + lane] = Hop[rb][j][s];
+                    __syncthreads();
+                }
+                // P' = H (H + sigma b' I): acc[rb][j] is block (p0 + rb, (p0 + j) mod NB);
+                // iteration it = (jk, s) runs over the rotated k-blocks (p0 + jk) mod NB.
+                f32x16 acc[RB][NB];
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) acc[rb][j] = f32x16{};
+                auto h_slot = [&](int jo, int it) -> u32x4 {
+                    const int jk = it / S, s = it % S;
+                    return sl_row[jo][(((p0 + jk) % NB) * S + s) * 64];
+                };
+                u32x4 nxt_op[NOA];
+                if constexpr (NO > 0) {
+#pragma unroll
+                    for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = h_slot(jo, 0);
+                }
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int jk = it / S, s = it % S;
+                    u32x4 cur_op[NOA];
+#pragma unroll
+                    for (int jo = 0; jo < NOA; ++jo) cur_op[jo] = nxt_op[jo];
+                    if constexpr (NO > 0) {
+                        if (it + 1 < IT) {
+#pragma unroll
+                            for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = h_slot(jo, it + 1);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        const u32x4 opa = j < RB ? Hop[j < RB ? j : 0][jk][s] : cur_op[j < RB ? 0 : j - RB];
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb) {
+                            const u32x4 opb = jk == rb ? Q0[rb][s] : Hop[rb][jk][s];
+                            acc[rb][j] = mma1<OP>(opa, opb, acc[rb][j]);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) {
+                            if constexpr (CMODE == 0) Pop[rb][j][s] = make_slot<OP>(acc[rb][j], s);
+                            else Pop[rb][j][s] = make_slot<OP>(-acc[rb][j], s);
+                        }
+            } else {
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) Pop[rb][j][s] = make_slot<OP>(G[rb][j] * args.bq, s);
+            }
+
+            if (LAST && has_next) issue_loads(nxt);  // next tile, overlapping this product
+
+            // Z <- a Z + P Z; iteration it = (jk, s) needs the column pieces of
+            // k-block (p0 + jk) mod NB for every output block N (two transposing
+            // reads each), shared by the RB owned row blocks.
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int N = 0; N < NB; ++N) Z[rb][N] *= args.a;
+            {
+                auto col_piece = [&](int it, int N) -> u32x4 {
+                    const int jk = it / S, s = it % S;
+                    const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 16 * s * RS + 64 * N;
+                    const u32x2 lo = tr_read(kb + tr_off[0]);
+                    const u32x2 hi = tr_read(kb + tr_off[1]);
+                    return u32x4{lo[0], lo[1], hi[0], hi[1]};
+                };
+                u32x4 nxt_op[NB];
+#pragma unroll
+                for (int N = 0; N < NB; ++N) nxt_op[N] = col_piece(0, N);
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int jk = it / S, s = it % S;
+                    u32x4 cur_op[NB];
+#pragma unroll
+                    for (int N = 0; N < NB; ++N) cur_op[N] = nxt_op[N];
+                    if (it + 1 < IT) {
+#pragma unroll
+                        for (int N = 0; N < NB; ++N) nxt_op[N] = col_piece(it + 1, N);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int N = 0; N < NB; ++N)
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb) Z[rb][N] = mma1<OP>(cur_op[N], Pop[rb][jk][s], Z[rb][N]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+            if constexpr (SHARED) __syncthreads();  // the row-major copy and the H slots are rewritten next step
+        };
+        for (int k = 0; k + 1 < args.K; ++k) ns_step(std::false_type{});
+        if (args.K > 0) ns_step(std::true_type{});
+
+        if (args.K == 0 && has_next) issue_loads(nxt);
+        // row pieces (scaled back, rounded to bf16) into the own rows of the
+        // row-major copy, then whole row segments to HBM
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f32x4 v = f32x4{Z[rb][q][4 * g + 0], Z[rb][q][4 * g + 1], Z[rb][q][4 * g + 2],
+                                          Z[rb][q][4 * g + 3]} * args.unscale;
+                    *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q) =
+                        u32x2{pack2<Operand::BF16>(v[0], v[1]), pack2<Operand::BF16>(v[2], v[3])};
+                }
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const u32x4 w = *reinterpret_cast<const u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row));
+            const int64_t gr = cur.row0 + 32 * p0 + RPI * i + io_row;
+            const int64_t gc = cur.col0 + 8 * io_cc;
+            uint16_t* ptr = static_cast<uint16_t*>(cur.d->out) + gr * cur.d->ld_out + gc;
+            if (cur.vout) {
+                *reinterpret_cast<u32x4*>(ptr) = w;
+            } else if (gr < cur.d->rows) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (gc + e < cur.d->cols) ptr[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+            }
+        }
+        if (!has_next) break;
+        cur = nxt;
+        local = nlocal;
     }
 }
 
@@ -862,10 +1091,10 @@ hipError_t launch_one(const KernelArgs& args, hipStream_t stream)
     return hipGetLastError();
 }
 
-template <int T, int CMODE>
+template <int T, int RB, int CMODE>
 hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
 {
-    constexpr int TPW = 4 / (T / 32);
+    constexpr int TPW = 4 / ((T / 32) / RB);
     static std::atomic<int> resident[kMaxDevices];
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -874,7 +1103,7 @@ hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
     int cap = resident[dev].load(std::memory_order_relaxed);
     if (cap == 0) {
         int per_cu = 0, cus = 0;
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ns_tiled_f16_kernel<T, CMODE>, kThreads, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ns_tiled_f16_kernel<T, RB, CMODE>, kThreads, 0);
         if (e != hipSuccess) return e;
         e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
@@ -885,7 +1114,7 @@ hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
     if (n <= 0) return hipSuccess;
     const int64_t groups = (n + TPW - 1) / TPW;
     const int grid = (int)(groups < cap ? groups : cap);
-    hipLaunchKernelGGL((ns_tiled_f16_kernel<T, CMODE>), dim3(grid), dim3(kThreads), 0, stream, args);
+    hipLaunchKernelGGL((ns_tiled_f16_kernel<T, RB, CMODE>), dim3(grid), dim3(kThreads), 0, stream, args);
     return hipGetLastError();
 }
 
@@ -919,15 +1148,15 @@ hipError_t launch_ns_tiled(int T, Storage st, Operand op, const KernelArgs& args
     if (op == Operand::F16) {
         const int cm = args.c > 0.f ? 0 : (args.c < 0.f ? 1 : 2);
         switch (T * 4 + cm) {
-        case 32 * 4 + 0: return launch_f16<32, 0>(args, stream);
-        case 32 * 4 + 1: return launch_f16<32, 1>(args, stream);
-        case 32 * 4 + 2: return launch_f16<32, 2>(args, stream);
-        case 64 * 4 + 0: return launch_f16<64, 0>(args, stream);
-        case 64 * 4 + 1: return launch_f16<64, 1>(args, stream);
-        case 64 * 4 + 2: return launch_f16<64, 2>(args, stream);
-        case 128 * 4 + 0: return launch_f16<128, 0>(args, stream);
-        case 128 * 4 + 1: return launch_f16<128, 1>(args, stream);
-        case 128 * 4 + 2: return launch_f16<128, 2>(args, stream);
+        case 32 * 4 + 0: return launch_f16<32, 1, 0>(args, stream);
+        case 32 * 4 + 1: return launch_f16<32, 1, 1>(args, stream);
+        case 32 * 4 + 2: return launch_f16<32, 1, 2>(args, stream);
+        case 64 * 4 + 0: return launch_f16<64, 2, 0>(args, stream);
+        case 64 * 4 + 1: return launch_f16<64, 2, 1>(args, stream);
+        case 64 * 4 + 2: return launch_f16<64, 2, 2>(args, stream);
+        case 128 * 4 + 0: return launch_f16<128, 1, 0>(args, stream);
+        case 128 * 4 + 1: return launch_f16<128, 1, 1>(args, stream);
+        case 128 * 4 + 2: return launch_f16<128, 1, 2>(args, stream);
         default: return hipErrorInvalidValue;
         }
     }

@@ -51,6 +51,8 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// 16-byte vectors in the global address space (global_load / global_store)
+typedef __attribute__((address_space(1))) u32x4 gbl_u32x4;
 
 #define HM_DEV __device__ __forceinline__
 
@@ -577,7 +579,7 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
 // order J = (p + j) mod NB, so its own row blocks come from registers.
 //
 // Tiles are processed in rounds; the HBM loads of a wave's next tile are
-// issued during the product of the current tile's last step.
+// issued before the current tile is written back.
 
 // 64-bit DPP move (both halves with the same control).
 template <int CTRL> HM_DEV double dpp_f64(double v)
@@ -727,7 +729,7 @@ __global__ void __launch_bounds__(kThreads, (kF16MinBlocks<T, RB>)) ns_tiled_f16
     const int64_t n_tiles = args.tile_end - args.tile_begin;
 
     // Tile placement. The tile of the next round is located, and its HBM
-    // loads are issued, while the current tile is still in its last step.
+    // loads are issued, before the current tile is written back.
     struct TileLoc {
         const MatDesc* d;
         int64_t row0, col0;
@@ -756,14 +758,18 @@ __global__ void __launch_bounds__(kThreads, (kF16MinBlocks<T, RB>)) ns_tiled_f16
     const int io_row = lane / LPR, io_cc = lane % LPR;  // row within an instruction, 16-byte chunk
     u32x4 raw[NI];
     auto issue_loads = [&](const TileLoc& L) {
+        const int64_t gr0 = L.row0 + 32 * p0 + io_row;
+        const int64_t gc = L.col0 + 8 * io_cc;
+        if (L.vin) {  // whole tile inside, 16-byte aligned: straight vector loads
+            const gbl_u32x4* src = (const gbl_u32x4*)(static_cast<const uint16_t*>(L.d->in) + gr0 * L.d->ld_in + gc);
+            const int64_t step = (int64_t)RPI * L.d->ld_in / 8;  // u32x4 per RPI rows
 #pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const int64_t gr = L.row0 + 32 * p0 + RPI * i + io_row;
-            const int64_t gc = L.col0 + 8 * io_cc;
-            const uint16_t* ptr = static_cast<const uint16_t*>(L.d->in) + gr * L.d->ld_in + gc;
-            if (L.vin) {
-                raw[i] = *reinterpret_cast<const u32x4*>(ptr);
-            } else {
+            for (int i = 0; i < NI; ++i) raw[i] = src[i * step];
+        } else {
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int64_t gr = gr0 + RPI * i;
+                const uint16_t* ptr = static_cast<const uint16_t*>(L.d->in) + gr * L.d->ld_in + gc;
                 uint32_t h[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
                 if (gr < L.d->rows) {
 #pragma unroll
@@ -839,10 +845,8 @@ __global__ void __launch_bounds__(kThreads, (kF16MinBlocks<T, RB>)) ns_tiled_f16
                     for (int v = 0; v < 16; ++v) Z[rb][q][v] = ldexpf(Z[rb][q][v] * mant, ex);
         }
 
-        // One Newton-Schulz step. The last one is a separate instance, so the
-        // registers of the next tile's loads are live only there.
-        auto ns_step = [&](auto last_tag) {
-            constexpr bool LAST = decltype(last_tag)::value;
+        // One Newton-Schulz step.
+        auto ns_step = [&]() {
             u32x4 Zop[RB][NB][S];
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
@@ -982,7 +986,6 @@ __global__ void __launch_bounds__(kThreads, (kF16MinBlocks<T, RB>)) ns_tiled_f16
                         for (int s = 0; s < S; ++s) Pop[rb][j][s] = make_slot<OP>(G[rb][j] * args.bq, s);
             }
 
-            if (LAST && has_next) issue_loads(nxt);  // next tile, overlapping this product
 
             // Z <- a Z + P Z; iteration it = (jk, s) needs the column pieces of
             // k-block (p0 + jk) mod NB for every output block N (two transposing
@@ -1022,12 +1025,11 @@ __global__ void __launch_bounds__(kThreads, (kF16MinBlocks<T, RB>)) ns_tiled_f16
             }
             if constexpr (SHARED) __syncthreads();  // the row-major copy and the H slots are rewritten next step
         };
-        for (int k = 0; k + 1 < args.K; ++k) ns_step(std::false_type{});
-        if (args.K > 0) ns_step(std::true_type{});
+        for (int k = 0; k < args.K; ++k) ns_step();
 
-        if (args.K == 0 && has_next) issue_loads(nxt);
         // row pieces (scaled back, rounded to bf16) into the own rows of the
-        // row-major copy, then whole row segments to HBM
+        // row-major copy, then whole row segments to HBM; the next tile's loads
+        // are issued in between, once the state registers are free
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -1039,18 +1041,34 @@ __global__ void __launch_bounds__(kThreads, (kF16MinBlocks<T, RB>)) ns_tiled_f16
                     *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q) =
                         u32x2{pack2<Operand::BF16>(v[0], v[1]), pack2<Operand::BF16>(v[2], v[3])};
                 }
+        // (raw is defined on both paths, so the values staged at the top of
+        // this round are dead across its steps)
+        if (has_next) {
+            issue_loads(nxt);
+        } else {
 #pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const u32x4 w = *reinterpret_cast<const u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row));
-            const int64_t gr = cur.row0 + 32 * p0 + RPI * i + io_row;
+            for (int i = 0; i < NI; ++i) raw[i] = u32x4{};
+        }
+        {
+            const int64_t gr0 = cur.row0 + 32 * p0 + io_row;
             const int64_t gc = cur.col0 + 8 * io_cc;
-            uint16_t* ptr = static_cast<uint16_t*>(cur.d->out) + gr * cur.d->ld_out + gc;
             if (cur.vout) {
-                *reinterpret_cast<u32x4*>(ptr) = w;
-            } else if (gr < cur.d->rows) {
+                gbl_u32x4* dst = (gbl_u32x4*)(static_cast<uint16_t*>(cur.d->out) + gr0 * cur.d->ld_out + gc);
+                const int64_t step = (int64_t)RPI * cur.d->ld_out / 8;
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    if (gc + e < cur.d->cols) ptr[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+                for (int i = 0; i < NI; ++i) dst[i * step] = *reinterpret_cast<const u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row));
+            } else {
+#pragma unroll
+                for (int i = 0; i < NI; ++i) {
+                    const u32x4 w = *reinterpret_cast<const u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row));
+                    const int64_t gr = gr0 + RPI * i;
+                    uint16_t* ptr = static_cast<uint16_t*>(cur.d->out) + gr * cur.d->ld_out + gc;
+                    if (gr < cur.d->rows) {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (gc + e < cur.d->cols) ptr[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+                    }
+                }
             }
         }
         if (!has_next) break;

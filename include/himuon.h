@@ -13,8 +13,8 @@
  *     a tile, X_0 = S/||S||_F (Phi_K(0) = 0), and applies K steps of
  *     X <- (aI + bA + cA^2) X with A = X X^T;
  *   - tiles of every matrix in the call are batched into shared launches
- *     ("cross-layer batching", Sec. 4.3) and split into the fewest balanced
- *     chunks that fit a memory budget ("memory-bounded chunking", Sec. 4.3).
+ *     ("cross-layer batching", Sec. 4.4.2) and split into the fewest balanced
+ *     chunks that fit a memory budget (memory-bounded chunking, Sec. 4.4.2).
  *
  * All entry points are plain C: host pointers for the small per-matrix
  * arrays, device pointers for matrix data and workspace, and a HIP stream
@@ -87,7 +87,7 @@ size_t himuon_ns_tiled_workspace_size(int64_t n_mats);
  *                          may be NULL, meaning contiguous rows (ld = cols).
  * T                        tile size, one of 32, 64, 128, 256. A matrix with
  *                          T >= max(H, W) is one zero-padded tile, which gives
- *                          Phi_K of the whole matrix (Sec. 4.3).
+ *                          Phi_K of the whole matrix (Sec. 4.4.3).
  * K                        Newton-Schulz steps (>= 0). K = 0 returns S/||S||_F
  *                          per tile.
  * a, b, c                  the polynomial coefficients (finite), e.g. Muon's

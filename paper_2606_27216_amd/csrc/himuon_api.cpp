@@ -1,8 +1,8 @@
 // C ABI of the tiled Newton–Schulz library: argument validation, the tile
 // and chunk plan, descriptor upload, and one kernel launch per chunk.
 //
-// Plan (Sec. 4.3 "cross-layer batching" and "memory-bounded chunking";
-// Sec. 4.4 "runtime tile-size reconfiguration"): every matrix of a call
+// Plan (Sec. 4.4.2, "cross-layer batching" with memory-bounded chunking;
+// Sec. 4.4.3, "runtime tile-size reconfiguration"): every matrix of a call
 // contributes its R x C tiles to one global, densely numbered tile set; the
 // set is split into the fewest chunks whose staged bytes fit the budget,
 // balanced to within one tile. The plan is O(#matrices) integer work and is

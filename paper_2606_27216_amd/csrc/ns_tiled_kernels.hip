@@ -2,7 +2,7 @@
 //
 // One launch evaluates Phi_K (Sec. 2.2, eqs. ns_iteration / ns_quintic /
 // phi_k_def) on every tile of a chunk of the batched tile set (Sec. 4.1,
-// eq. tiled_ns; Sec. 4.3 cross-layer batching). Each tile is read from HBM
+// eq. tiled_ns; Sec. 4.4.2, cross-layer batching). Each tile is read from HBM
 // once, kept on chip (registers + LDS) for all K steps, and written once.
 //
 // Data layout on chip. A tile is a grid of 32x32 blocks (NB = T/32 per side).

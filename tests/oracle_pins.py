@@ -12,7 +12,7 @@ relative error it saw. The routes:
   1×1 and scaled-orthogonal inputs;
 * the tiling operator of Sec. 2.1 applied with numpy slicing, each block then
   checked against the SVD closed form (zero padding leaves Φ_K unchanged,
-  Sec. 4.3: padded rows and columns stay zero and do not change the norm);
+  Sec. 4.4.3: padded rows and columns stay zero and do not change the norm);
 * invariances that any correct implementation obeys: transposition,
   orthogonal equivariance, odd homogeneity of degree 0, tile permutation;
 * the textbook special case: cubic Newton–Schulz (1.5, −0.5, 0) converges to
@@ -229,7 +229,7 @@ def pin_invariances(lib=None):
 
 def pin_tile_permutation(lib=None):
     """Tiles are independent: permuting the tiles of the input permutes the
-    tiles of Φ_{K,T} the same way (Sec. 4.3, cross-layer batching)."""
+    tiles of Φ_{K,T} the same way (Sec. 4.4.2, cross-layer batching)."""
     rng = np.random.default_rng(20)
     T, R, C = 8, 3, 4
     S = rng.standard_normal((R * T, C * T))
@@ -245,7 +245,7 @@ def pin_tile_permutation(lib=None):
 
 
 def pin_single_tile_is_full_map(lib=None):
-    """T ≥ max(H, W) gives one padded tile and Φ_{K,T} = Φ_K (Sec. 4.3);
+    """T ≥ max(H, W) gives one padded tile and Φ_{K,T} = Φ_K (Sec. 4.4.3);
     T = H = W is full-matrix Muon Newton–Schulz."""
     rng = np.random.default_rng(21)
     S = rng.standard_normal((24, 24))

@@ -35,6 +35,7 @@ def check_full(x, y, T, K=5, coeffs=COEF32, tol=None):
     e = tile_errors(to_f64(y), R, T)
     tol = TOL[x.dtype] if tol is None else tol
     assert np.all(np.isfinite(e)), "non-finite tile"
+    print(f"[gpu-err] {len(e)} tiles: max {e.max():.3e} p50 {np.median(e):.3e} (bar {tol:.0e})", flush=True)
     assert e.max() <= tol, f"max per-tile error {e.max():.3e} > {tol:.1e} (p50 {np.median(e):.3e})"
     return e
 
@@ -76,6 +77,7 @@ def test_config3_one_layer_sampled():
         ids = np.sort(rng.choice(n, 24, replace=False))
         ref = oracle.ns_tiles(S, 128, 5, *COEF32, ids)
         e = sampled_tile_errors(to_f64(y), ref, ids, 128)
+        print(f"[gpu-err] {x.shape[0]}x{x.shape[1]} sampled: max {e.max():.3e}", flush=True)
         assert e.max() <= TOL[torch.bfloat16], e.max()
 
 
@@ -94,6 +96,7 @@ def test_config5_heterogeneous_schedule(dtype, K):
             ids = np.sort(rng.choice(n, 12, replace=False))
             ref = oracle.ns_tiles(S, T, K, *COEF32, ids)
             e = sampled_tile_errors(to_f64(outs[i]), ref, ids, T)
+            print(f"[gpu-err] matrix {i} T={T} sampled: max {e.max():.3e}", flush=True)
             assert e.max() <= TOL[mats[i].dtype], (T, i, e.max())
 
 
@@ -267,4 +270,5 @@ def test_7b_stack_full_size_sampled():
             ref = oracle.ns_tiles(S, 128, 5, *COEF32, ids)
             e = sampled_tile_errors(to_f64(outs[i]), ref, ids, 128)
             worst = max(worst, e.max())
+    print(f"[gpu-err] 63 sampled tiles across the stack: max {worst:.3e}", flush=True)
     assert worst <= TOL[torch.bfloat16], worst

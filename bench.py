@@ -36,7 +36,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}  # MI355X dense MFMA, published
 HBM_PEAK_GBS = 8000.0
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_27216_amd", "csrc", "ns_tiled_kernels.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_27216_amd", "csrc", f)
+                  for f in ("ns_device.h", "ns_tiled_kernels.hip", "ns_tiled_f16.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ns_tiled_traffic.json")
 METRIC = "tiled-NS TFLOP/s (6·H·W·T·K) + % bf16 MFMA peak, 7B layer stack T=128 K=5"
 
@@ -46,9 +47,9 @@ def log(msg):
 
 
 def kernel_source_hash() -> str:
-    """Hash of the kernel source's code: comments and whitespace removed, so
+    """Hash of the kernel sources' code: comments and whitespace removed, so
     that only a change of the code invalidates recorded counters."""
-    src = open(KERNEL_SOURCE, encoding="utf-8").read()
+    src = "".join(open(f, encoding="utf-8").read() for f in KERNEL_SOURCES)
     src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
     src = re.sub(r"//[^\n]*", " ", src)
     return hashlib.sha256("".join(src.split()).encode()).hexdigest()[:16]

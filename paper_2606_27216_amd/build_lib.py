@@ -17,14 +17,22 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIBRARY = os.path.join(PKG, "libhimuon.so")
-SOURCES = [os.path.join(CSRC, "ns_tiled_kernels.hip"), os.path.join(CSRC, "himuon_api.cpp")]
+BUILD_DIR = os.path.join(PKG, "_build")
 ARCH = "gfx950"
 
-FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+COMMON = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
     "-I", os.path.join(ROOT, "include"),
+]
+# (source, extra flags). The fp16 kernel keeps its MFMA accumulators in
+# architectural VGPRs, where the vector ALU converts them after each product;
+# the fp32/bf16 kernels keep the compiler's default register classes.
+SOURCES = [
+    ("ns_tiled_kernels.hip", []),
+    ("ns_tiled_f16.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form"]),
+    ("himuon_api.cpp", []),
 ]
 
 
@@ -35,9 +43,7 @@ def hipcc() -> str:
     return "hipcc"
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIBRARY + ".tmp"
-    cmd = [hipcc()] + FLAGS + SOURCES + ["-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -47,6 +53,17 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{msgs}")
     if msgs.strip() and verbose:
         print(msgs)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    objs = []
+    for src, extra in SOURCES:
+        obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
+        _run([hipcc()] + COMMON + extra + ["-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        objs.append(obj)
+    tmp = LIBRARY + ".tmp"
+    _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC"] + objs + ["-o", tmp], verbose)
     os.replace(tmp, LIBRARY)
     return LIBRARY
 

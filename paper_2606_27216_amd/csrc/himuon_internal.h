@@ -53,4 +53,7 @@ hipError_t launch_ns_tiled(int T, Storage st, Operand op, const KernelArgs& args
 // True when a kernel exists for the triple (no HIP call).
 bool has_kernel(int T, Storage st, Operand op);
 
+// The fp16-operand kernel family (bf16 storage), T in {32, 64, 128}.
+hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream);
+
 }  // namespace himuon

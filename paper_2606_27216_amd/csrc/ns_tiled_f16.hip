@@ -1,0 +1,675 @@
+// fp16-operand tiled Newton–Schulz kernel for gfx950 (MI355X), bf16 storage.
+//
+// Evaluates Phi_K (Sec. 2.2, eqs. ns_iteration / ns_quintic / phi_k_def) on
+// every tile of a chunk of the batched tile set (Sec. 4.1, eq. tiled_ns;
+// Sec. 4.4.2). Built with MFMA results kept in architectural VGPRs
+// (-amdgpu-mfma-vgpr-form): every accumulator is converted by vector ALU
+// instructions right after its product, and AGPR-resident accumulators
+// would need a copy for each conversion.
+#include "ns_device.h"
+
+#include <atomic>
+
+namespace himuon {
+namespace {
+
+using namespace dev;
+
+// ------------------------------------------------ fp16-operand kernel
+//
+// Same tile map, restructured so that almost no vector-ALU work is left in
+// the K loop. The state is Z = X |c|^(1/4) (exact rescaling of the iterate),
+// for which one step of eq. (ns_iteration) reads
+//     Z <- a Z + P Z,   P = sigma H (H + sigma b' I),   H = Z Z^T,
+// with b' = b / sqrt|c| and sigma = sign(c): the c-coefficient becomes +-1
+// and b' moves onto the diagonal of an MFMA operand, so the only per-element
+// multiply left is the fp32 a*Z that seeds the product accumulator (the a*Z
+// term stays in fp32, which keeps rounding out of the directions the
+// iteration amplifies). The normalisation multiplies by |c|^(1/4) and the
+// store by |c|^(-1/4). c = 0 takes P = b H.
+//
+// Z is shared through one row-major fp16 copy of the tile (see kRowStride).
+// Gram operands of the other waves' rows are read from it as row pieces; the
+// B X operand (column pieces of Z) comes from it through ds_read_b64_tr_b16,
+// which returns in every lane quad a 4x4 transpose of four rows supplied by
+// the other lanes of its 16-lane group. H is shared through 16-byte
+// lane-ordered slots. A wave works on the blocks of its row in the rotated
+// order J = (p + j) mod NB, so its own row blocks come from registers.
+//
+// Tiles are processed in rounds; the HBM loads of a wave's next tile are
+// issued before the current tile is written back.
+
+// Sum over the 64 lanes in a fixed order: butterflies inside each 16-lane
+// row (quad swaps, half-row and row mirrors), then the four row sums.
+HM_DEV float wave_sum_f32(float v)
+{
+    v += __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(v), 0xB1, 0xF, 0xF, false));
+    v += __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(v), 0x4E, 0xF, 0xF, false));
+    v += __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(v), 0x141, 0xF, 0xF, false));
+    v += __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(v), 0x140, 0xF, 0xF, false));
+    const float r0 = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 0));
+    const float r1 = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 16));
+    const float r2 = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 32));
+    const float r3 = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
+HM_DEV uint32_t wave_max_u32(uint32_t v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
+    return v;
+}
+
+// Matrix owning `tile`, searching from `hint` (the tiles one wave visits only
+// grow, so the owner of an earlier tile is a lower bound).
+HM_DEV int find_matrix_from(const KernelArgs& args, int64_t tile, int hint)
+{
+    const ConstDesc* const descs = desc_table(args);
+    if (hint + 1 >= args.n_mats || descs[hint + 1].tile_begin > tile) return hint;
+    int lo = hint + 1, hi = args.n_mats - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (descs[mid].tile_begin <= tile) lo = mid;
+        else hi = mid - 1;
+    }
+    return __builtin_amdgcn_readfirstlane(lo);
+}
+
+// Four consecutive bf16 elements of row gr (columns gc..gc+3) as two packed
+// words, zero outside the matrix (the zero padding of the tiling operator).
+HM_DEV u32x2 load_bf16x4(const void* base, int64_t gr, int64_t gc, int64_t ld, int64_t rows, int64_t cols, bool vec)
+{
+    const uint16_t* p = static_cast<const uint16_t*>(base) + gr * ld + gc;
+    if (vec) return *reinterpret_cast<const u32x2*>(p);
+    uint32_t h[4] = {0u, 0u, 0u, 0u};
+    if (gr < rows) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (gc + e < cols) h[e] = p[e];
+    }
+    return u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+}
+
+HM_DEV u32x2 tr_read(const uint8_t* ptr)
+{
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s4* lds_s4p;
+    const s4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4p)(ptr));
+    return __builtin_bit_cast(u32x2, v);
+}
+
+// Row-major fp16 copy of Z. Bytes per row: an odd multiple of 64, so the
+// eight consecutive rows a transposing read touches (64 bytes each) fall on
+// four distinct quarters of the 256-byte bank space, twice each. Within each
+// 64-byte segment (32 columns) the 8-byte chunk c of row r sits at chunk
+// c ^ 2((r >> 2) & 3): rows r, r+4, ..., r+28 share a quarter, and the XOR
+// spreads their row-piece chunks (2g + lh) over all eight chunks, so
+// row-piece reads and writes (32 rows x 16 bytes) are conflict-free as well.
+template <int T> constexpr int kRowStride = ((2 * T / 64) % 2 == 1) ? 2 * T : 2 * T + 64;
+
+// Workgroup shape of the fp16 kernel. A tile split over WT > 1 waves is
+// one workgroup of WT waves; tiles kept by one wave come four to a
+// workgroup. A wave that owns two row blocks of a 128-tile keeps its state,
+// accumulators and the next tile's prefetched rows in up to 512 registers
+// (one wave per SIMD); everything else runs two waves per SIMD.
+template <int T, int RB> struct F16Shape {
+    static constexpr int NB = T / 32;
+    static constexpr int WT = NB / RB;
+    static constexpr int TPW = WT > 1 ? 1 : 4;
+    static constexpr int kThreads = 64 * WT * TPW;
+    static constexpr bool kWide = T == 128 && RB == 2;
+    static constexpr int kMinWavesPerEU = kWide ? 1 : 2;
+    // next tile's loads issued before the K loop (registers permitting)
+    static constexpr bool kEarlyPrefetch = kWide;
+};
+
+// CMODE: 0 for c > 0, 1 for c < 0, 2 for c = 0 (sign(c) and the c = 0
+// shortcut are compile-time, so no branch of the K loop is if-converted).
+// RB: 32-row blocks owned by one wave; a tile is spread over NB / RB waves.
+// Every operand read from LDS feeds RB MFMAs.
+template <int T, int RB, int CMODE>
+__global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>::kMinWavesPerEU)) ns_tiled_f16_kernel(const KernelArgs args)
+{
+    constexpr Storage ST = Storage::BF16;
+    constexpr Operand OP = Operand::F16;
+    constexpr int NB = T / 32;      // row blocks per tile
+    constexpr int WT = NB / RB;     // waves per tile
+    static_assert(NB % RB == 0 && WT >= 1 && WT <= 4, "tile split");
+    constexpr int TPW = F16Shape<T, RB>::TPW;  // tiles per workgroup
+    constexpr bool EARLY = F16Shape<T, RB>::kEarlyPrefetch;
+    constexpr int S = 2;
+    constexpr int MAT = NB * NB * S * 64;  // 16-byte slots of H
+    constexpr bool SHARED = WT > 1;
+    static_assert(!SHARED || TPW == 1, "a workgroup that shares a tile runs one tile");
+    constexpr int NO = NB - RB;     // row blocks owned by the other waves of the tile
+    constexpr int NOA = NO > 0 ? NO : 1;
+    constexpr int RS = kRowStride<T>;
+    constexpr int RM = T * RS;
+    constexpr int IT = NB * S;      // k iterations of one product
+
+    __shared__ u32x4 s_slots[SHARED ? TPW * MAT : 1];
+    __shared__ __attribute__((aligned(16))) uint8_t s_rm[TPW * RM];
+    __shared__ float s_red[6][SHARED ? WT : 1];  // 2 tile parities x 3 reductions
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int tslot = wave / WT, p0 = (wave % WT) * RB;
+    const int li = lane & 31, lh = lane >> 5;
+    u32x4* const slots = s_slots + (SHARED ? tslot * MAT : 0);
+    uint8_t* const rm = s_rm + tslot * RM;
+    // Row pieces: this lane's columns 32q + 8g + 4lh of row li of a block are
+    // chunk 2g + lh of the block's segment, stored at chunk 2(g ^ fl) + lh.
+    const int fl = (li >> 2) & 3;
+    int rp_off[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) rp_off[g] = li * RS + 16 * (g ^ fl) + 8 * lh;
+    // Transposing reads: supplier lane 4q' + m of 16-lane group G addresses
+    // row 4(G/2) + m (+ 8x) and logical chunk 4(G%2) + q' of a block segment.
+    const int grp16 = lane >> 4;
+    int tr_off[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        const int row = 8 * x + 4 * (grp16 >> 1) + ((lane & 15) >> 2);
+        const int chunk = 4 * (grp16 & 1) + (lane & 3);
+        tr_off[x] = row * RS + 8 * (chunk ^ (2 * ((row >> 2) & 3)));
+    }
+    // A diagonal block holds row li's column 8g + 4lh + e in register 4g + e,
+    // so the diagonal entry of this lane (if any) is register vdiag.
+    const int vdiag = (lh == ((li >> 2) & 1)) ? 4 * (li >> 3) + (li & 3) : -1;
+    // sigma a I as a diagonal block (the seed of the aI + P accumulators)
+    f32x16 diag_a = {};
+#pragma unroll
+    for (int v = 0; v < 16; ++v) diag_a[v] = v == vdiag ? (CMODE == 1 ? -args.a : args.a) : 0.f;
+    // the row blocks owned by the other waves, in rotated order: H slots and
+    // the rows of the row-major copy
+    u32x4* sl_row[NOA];
+    const uint8_t* rm_row[NOA];
+#pragma unroll
+    for (int jo = 0; jo < NOA; ++jo) {
+        sl_row[jo] = slots + (((p0 + RB + jo) % NB) * NB * S) * 64 + lane;
+        rm_row[jo] = rm + 32 * ((p0 + RB + jo) % NB) * RS;
+    }
+    auto rowpiece = [&](const uint8_t* blockrow, int q, int s) -> u32x4 {
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(blockrow + rp_off[2 * s] + 64 * q);
+        const u32x2 hi = *reinterpret_cast<const u32x2*>(blockrow + rp_off[2 * s + 1] + 64 * q);
+        return u32x4{lo[0], lo[1], hi[0], hi[1]};
+    };
+
+    const int64_t n_tiles = args.tile_end - args.tile_begin;
+
+    // Tile placement. The tile of the next round is located, and its HBM
+    // loads are issued, before the current tile is written back.
+    struct TileLoc {
+        const void* in;
+        void* out;
+        int64_t rows, cols, ld_in, ld_out;
+        int64_t row0, col0;
+        bool vin, vout;
+    };
+    int mhint = 0;
+    auto locate = [&](int64_t local, TileLoc& L) {
+        const int64_t tile = args.tile_begin + local;
+        mhint = find_matrix_from(args, tile, mhint);
+        const ConstDesc& D = desc_table(args)[mhint];
+        L.in = D.in;
+        L.out = D.out;
+        L.rows = D.rows;
+        L.cols = D.cols;
+        L.ld_in = D.ld_in;
+        L.ld_out = D.ld_out;
+        const int64_t lt = tile - D.tile_begin;
+        const int64_t tr = lt / D.tiles_c;
+        L.row0 = tr * T;
+        L.col0 = (lt - tr * D.tiles_c) * T;
+        const bool full = L.row0 + T <= L.rows && L.col0 + T <= L.cols;
+        L.vin = full && (D.flags & MAT_VEC_IN);
+        L.vout = full && (D.flags & MAT_VEC_OUT);
+    };
+    // HBM traffic in whole row segments: a lane moves 16 bytes (8 bf16), a
+    // row takes LPR lanes and one wave instruction RPI rows. The wave's own
+    // RB row blocks take NI instructions; the row pieces are then reshaped
+    // through the wave's own rows of the row-major copy.
+    constexpr int LPR = T / 8;
+    constexpr int RPI = 64 / LPR;
+    constexpr int NI = 32 * RB / RPI;
+    const int io_row = lane / LPR, io_cc = lane % LPR;  // row within an instruction, 16-byte chunk
+    u32x4 raw[NI];
+    auto issue_loads = [&](const TileLoc& L) {
+        const int64_t gr0 = L.row0 + 32 * p0 + io_row;
+        const int64_t gc = L.col0 + 8 * io_cc;
+        if (L.vin) {  // whole tile inside, 16-byte aligned: straight vector loads
+            const gbl_u32x4* src = (const gbl_u32x4*)(static_cast<const uint16_t*>(L.in) + gr0 * L.ld_in + gc);
+            const int64_t step = (int64_t)RPI * L.ld_in / 8;  // u32x4 per RPI rows
+#pragma unroll
+            for (int i = 0; i < NI; ++i) raw[i] = src[i * step];
+        } else {
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int64_t gr = gr0 + RPI * i;
+                const uint16_t* ptr = static_cast<const uint16_t*>(L.in) + gr * L.ld_in + gc;
+                uint32_t h[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+                if (gr < L.rows) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (gc + e < L.cols) h[e] = ptr[e];
+                }
+                raw[i] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+            }
+        }
+    };
+    // byte offset of the 16-byte chunk io_cc of tile row `row` in the row-major copy
+    auto io_lds = [&](int row) -> int {
+        return row * RS + 64 * (io_cc >> 2) + 8 * ((2 * (io_cc & 3)) ^ (2 * ((row >> 2) & 3)));
+    };
+
+    // Whole row segments of the own rows to HBM (16-byte chunks read back from
+    // the row-major copy into `outv`).
+    auto store_rows = [&](const TileLoc& L, const u32x4 (&outv)[NI]) {
+        const int64_t gr0 = L.row0 + 32 * p0 + io_row;
+        const int64_t gc = L.col0 + 8 * io_cc;
+        if (L.vout) {
+            gbl_u32x4* dst = (gbl_u32x4*)(static_cast<uint16_t*>(L.out) + gr0 * L.ld_out + gc);
+            const int64_t step = (int64_t)RPI * L.ld_out / 8;
+#pragma unroll
+            for (int i = 0; i < NI; ++i) dst[i * step] = outv[i];
+        } else {
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int64_t gr = gr0 + RPI * i;
+                uint16_t* ptr = static_cast<uint16_t*>(L.out) + gr * L.ld_out + gc;
+                if (gr < L.rows) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (gc + e < L.cols) ptr[e] = (uint16_t)(outv[i][e >> 1] >> (16 * (e & 1)));
+                }
+            }
+        }
+    };
+
+    // Sum of squares of the tile from its packed bf16 words: per-lane fp32
+    // dot products, then a fixed-order reduction over the lanes and the
+    // waves of the tile (slot set `rs` of the exchange array).
+    auto tile_sumsq = [&](const uint32_t (&W)[RB][NB][8], int rs) -> float {
+        float v = 0.f;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    v = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, W[rb][q][i]),
+                                                       __builtin_bit_cast(bf16x2, W[rb][q][i]), v, false);
+        v = wave_sum_f32(v);
+        if constexpr (SHARED) {
+            if (lane == 0) s_red[rs][wave] = v;
+            __syncthreads();
+            v = s_red[rs][tslot * WT];
+#pragma unroll
+            for (int w = 1; w < WT; ++w) v += s_red[rs][tslot * WT + w];
+        }
+        return v;
+    };
+
+    int64_t local = (int64_t)blockIdx.x * TPW + tslot;
+    if (local >= n_tiles) return;  // uniform over the waves that share a tile
+    TileLoc cur;
+    locate(local, cur);
+    issue_loads(cur);
+    // The previous tile's results wait in `outv` until this tile's rows have
+    // left the prefetch registers: the prefetch wait then never waits on
+    // stores (loads and stores share one memory counter).
+    u32x4 outv[NI];
+    TileLoc prv = cur;
+    bool pending = false;
+    int parity = 0;  // alternates the reduction slots between tiles
+
+    for (;;) {
+        const int64_t nlocal = local + (int64_t)gridDim.x * TPW;
+        const bool has_next = nlocal < n_tiles;
+        TileLoc nxt = cur;
+        if (has_next) locate(nlocal, nxt);
+
+        // own rows into the row-major copy, then back as row pieces of packed
+        // bf16 words; only this wave touches these rows until its first
+        // step's barrier
+#pragma unroll
+        for (int i = 0; i < NI; ++i) *reinterpret_cast<u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row)) = raw[i];
+        if (pending) store_rows(prv, outv);
+        if constexpr (EARLY) {
+            if (has_next) issue_loads(nxt);  // in flight for the whole K loop
+        }
+        uint32_t W[RB][NB][8];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const u32x2 w = *reinterpret_cast<const u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q);
+                    W[rb][q][2 * g] = w[0];
+                    W[rb][q][2 * g + 1] = w[1];
+                }
+
+        // Z_0 = |c|^(1/4) S / ||S||_F (Phi_K(0) = 0). The fp32 sum of squares
+        // is exact enough whenever it lands in [2^-60, 2^100]; otherwise the
+        // tile is first scaled by 2^-k, k the exponent of its largest entry
+        // (exact, so Phi(2^e S) = Phi(S) bit for bit on either path), and the
+        // same sum is taken again.
+        float ss = tile_sumsq(W, 3 * parity);
+        float sc = 0.f;
+        if (ss != 0.f) {
+            if (!(ss >= 0x1p-60f && ss <= 0x1p100f)) {
+                uint32_t mb = 0;
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int q = 0; q < NB; ++q)
+#pragma unroll
+                        for (int i = 0; i < 8; ++i)
+                            mb = max(mb, max(W[rb][q][i] & 0x7fffu, (W[rb][q][i] >> 16) & 0x7fffu));
+                mb = wave_max_u32(mb);
+                if constexpr (SHARED) {
+                    if (lane == 0) s_red[3 * parity + 1][wave] = __uint_as_float(mb);
+                    __syncthreads();
+#pragma unroll
+                    for (int w = 0; w < WT; ++w) mb = max(mb, __float_as_uint(s_red[3 * parity + 1][tslot * WT + w]));
+                }
+                const int k = (int)((mb >> 7) & 0xffu) - 127;
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int q = 0; q < NB; ++q)
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) {
+                            const float lo = ldexpf(__uint_as_float(W[rb][q][i] << 16), -k);
+                            const float hi = ldexpf(__uint_as_float(W[rb][q][i] & 0xffff0000u), -k);
+                            W[rb][q][i] = (__float_as_uint(hi) & 0xffff0000u) | (__float_as_uint(lo) >> 16);
+                        }
+                ss = tile_sumsq(W, 3 * parity + 2);
+            }
+            sc = args.zscale / sqrtf(ss);
+        }
+        parity ^= 1;
+        f32x16 Z[RB][NB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    Z[rb][q][2 * i] = __uint_as_float(W[rb][q][i] << 16) * sc;
+                    Z[rb][q][2 * i + 1] = __uint_as_float(W[rb][q][i] & 0xffff0000u) * sc;
+                }
+
+        // One Newton-Schulz step.
+        auto ns_step = [&]() {
+            u32x4 Zop[RB][NB][S];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int q = 0; q < NB; ++q)
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Zop[rb][q][s] = make_slot<OP>(Z[rb][q], s);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int N = 0; N < NB; ++N)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * N) =
+                            u32x2{Zop[rb][N][g >> 1][(g & 1) * 2], Zop[rb][N][g >> 1][(g & 1) * 2 + 1]};
+            if constexpr (SHARED) __syncthreads();
+
+            // H = Z Z^T; G[rb][j] is the row piece of block (p0 + rb, (p0 + j) mod NB).
+            // Iteration it = (q, s) reads the other waves' row pieces (q, s) from
+            // the row-major copy; those of iteration it + 1 are requested before
+            // its MFMAs issue.
+            f32x16 G[RB][NB];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int j = 0; j < NB; ++j) G[rb][j] = f32x16{};
+            {
+                u32x4 nxt_op[NOA];
+                if constexpr (NO > 0) {
+#pragma unroll
+                    for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = rowpiece(rm_row[jo], 0, 0);
+                }
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int q = it / S, s = it % S;
+                    u32x4 cur_op[NOA];
+#pragma unroll
+                    for (int jo = 0; jo < NOA; ++jo) cur_op[jo] = nxt_op[jo];
+                    if constexpr (NO > 0) {
+                        if (it + 1 < IT) {
+#pragma unroll
+                            for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = rowpiece(rm_row[jo], (it + 1) / S, (it + 1) % S);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of these MFMAs
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        const u32x4 opa = j < RB ? Zop[j < RB ? j : 0][q][s] : cur_op[j < RB ? 0 : j - RB];
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb) G[rb][j] = mma1<OP>(opa, Zop[rb][q][s], G[rb][j]);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+
+            u32x4 Pop[RB][NB][S];  // own rows of P (rotated k-blocks), fp16
+            if constexpr (CMODE != 2) {
+                u32x4 Hop[RB][NB][S], Q0[RB][S];
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) Hop[rb][j][s] = make_slot<OP>(G[rb][j], s);
+                    f32x16 gd = G[rb][rb];  // H + sigma b' I on the diagonal block (p0 + rb, p0 + rb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) gd[v] += v == vdiag ? args.bq : 0.f;
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Q0[rb][s] = make_slot<OP>(gd, s);
+                }
+                if constexpr (SHARED) {
+                    // the H slots were last read before the previous step's final barrier
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int j = 0; j < NB; ++j)
+#pragma unroll
+                            for (int s = 0; s < S; ++s)
+                                slots[(((p0 + rb) * NB + (p0 + j) % NB) * S + s) * 64 + lane] = Hop[rb][j][s];
+                    __syncthreads();
+                }
+                // acc = H (H + sigma b' I) + sigma a I, so that sigma acc = a I + P:
+                // acc[rb][j] is block (p0 + rb, (p0 + j) mod NB), the diagonal
+                // blocks (j = rb) start from sigma a I; iteration it = (jk, s)
+                // runs over the rotated k-blocks (p0 + jk) mod NB.
+                f32x16 acc[RB][NB];
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) acc[rb][j] = j == rb ? diag_a : f32x16{};
+                auto h_slot = [&](int jo, int it) -> u32x4 {
+                    const int jk = it / S, s = it % S;
+                    return sl_row[jo][(((p0 + jk) % NB) * S + s) * 64];
+                };
+                u32x4 nxt_op[NOA];
+                if constexpr (NO > 0) {
+#pragma unroll
+                    for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = h_slot(jo, 0);
+                }
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int jk = it / S, s = it % S;
+                    u32x4 cur_op[NOA];
+#pragma unroll
+                    for (int jo = 0; jo < NOA; ++jo) cur_op[jo] = nxt_op[jo];
+                    if constexpr (NO > 0) {
+                        if (it + 1 < IT) {
+#pragma unroll
+                            for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = h_slot(jo, it + 1);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        const u32x4 opa = j < RB ? Hop[j < RB ? j : 0][jk][s] : cur_op[j < RB ? 0 : j - RB];
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb) {
+                            const u32x4 opb = jk == rb ? Q0[rb][s] : Hop[rb][jk][s];
+                            acc[rb][j] = mma1<OP>(opa, opb, acc[rb][j]);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) {
+                            if constexpr (CMODE == 0) Pop[rb][j][s] = make_slot<OP>(acc[rb][j], s);
+                            else Pop[rb][j][s] = make_slot<OP>(-acc[rb][j], s);
+                        }
+            } else {
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        const f32x16 pj = j == rb ? G[rb][j] * args.bq + diag_a : G[rb][j] * args.bq;
+#pragma unroll
+                        for (int s = 0; s < S; ++s) Pop[rb][j][s] = make_slot<OP>(pj, s);
+                    }
+            }
+
+
+            // Z <- (a I + P) Z, from zero accumulators; iteration it = (jk, s)
+            // needs the column pieces of k-block (p0 + jk) mod NB for every
+            // output block N (two transposing reads each), shared by the RB
+            // owned row blocks.
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int N = 0; N < NB; ++N) Z[rb][N] = f32x16{};
+            {
+                auto col_piece = [&](int it, int N) -> u32x4 {
+                    const int jk = it / S, s = it % S;
+                    const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 16 * s * RS + 64 * N;
+                    const u32x2 lo = tr_read(kb + tr_off[0]);
+                    const u32x2 hi = tr_read(kb + tr_off[1]);
+                    return u32x4{lo[0], lo[1], hi[0], hi[1]};
+                };
+                u32x4 nxt_op[NB];
+#pragma unroll
+                for (int N = 0; N < NB; ++N) nxt_op[N] = col_piece(0, N);
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int jk = it / S, s = it % S;
+                    u32x4 cur_op[NB];
+#pragma unroll
+                    for (int N = 0; N < NB; ++N) cur_op[N] = nxt_op[N];
+                    if (it + 1 < IT) {
+#pragma unroll
+                        for (int N = 0; N < NB; ++N) nxt_op[N] = col_piece(it + 1, N);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int N = 0; N < NB; ++N)
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb) Z[rb][N] = mma1<OP>(cur_op[N], Pop[rb][jk][s], Z[rb][N]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+            if constexpr (SHARED) __syncthreads();  // the row-major copy and the H slots are rewritten next step
+        };
+        for (int k = 0; k < args.K; ++k) ns_step();
+
+        // row pieces (scaled back, rounded to bf16) into the own rows of the
+        // row-major copy, then read back as whole 16-byte row chunks
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f32x4 v = f32x4{Z[rb][q][4 * g + 0], Z[rb][q][4 * g + 1], Z[rb][q][4 * g + 2],
+                                          Z[rb][q][4 * g + 3]} * args.unscale;
+                    *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q) =
+                        u32x2{pack2<Operand::BF16>(v[0], v[1]), pack2<Operand::BF16>(v[2], v[3])};
+                }
+#pragma unroll
+        for (int i = 0; i < NI; ++i) outv[i] = *reinterpret_cast<const u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row));
+        prv = cur;
+        pending = true;
+        // (raw is defined on both paths, so the values staged at the top of
+        // this round are dead across its steps)
+        if constexpr (!EARLY) {
+            if (has_next) {
+                issue_loads(nxt);
+            } else {
+#pragma unroll
+                for (int i = 0; i < NI; ++i) raw[i] = u32x4{};
+            }
+        }
+        if (!has_next) break;
+        cur = nxt;
+        local = nlocal;
+    }
+    store_rows(prv, outv);
+}
+
+constexpr int kMaxDevices = 64;
+
+template <int T, int RB, int CMODE>
+hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
+{
+    constexpr int TPW = F16Shape<T, RB>::TPW;
+    constexpr int NT = F16Shape<T, RB>::kThreads;
+    static std::atomic<int> resident[kMaxDevices];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    int cap = resident[dev].load(std::memory_order_relaxed);
+    if (cap == 0) {
+        int per_cu = 0, cus = 0;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ns_tiled_f16_kernel<T, RB, CMODE>, NT, 0);
+        if (e != hipSuccess) return e;
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        cap = (per_cu < 1 ? 1 : per_cu) * (cus < 1 ? 1 : cus);
+        resident[dev].store(cap, std::memory_order_relaxed);
+    }
+    const int64_t n = args.tile_end - args.tile_begin;
+    if (n <= 0) return hipSuccess;
+    const int64_t groups = (n + TPW - 1) / TPW;
+    const int grid = (int)(groups < cap ? groups : cap);
+    hipLaunchKernelGGL((ns_tiled_f16_kernel<T, RB, CMODE>), dim3(grid), dim3(NT), 0, stream, args);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream)
+{
+    const int cm = args.c > 0.f ? 0 : (args.c < 0.f ? 1 : 2);
+    switch (T * 4 + cm) {
+    case 32 * 4 + 0: return launch_f16<32, 1, 0>(args, stream);
+    case 32 * 4 + 1: return launch_f16<32, 1, 1>(args, stream);
+    case 32 * 4 + 2: return launch_f16<32, 1, 2>(args, stream);
+    case 64 * 4 + 0: return launch_f16<64, 2, 0>(args, stream);
+    case 64 * 4 + 1: return launch_f16<64, 2, 1>(args, stream);
+    case 64 * 4 + 2: return launch_f16<64, 2, 2>(args, stream);
+    case 128 * 4 + 0: return launch_f16<128, 2, 0>(args, stream);
+    case 128 * 4 + 1: return launch_f16<128, 2, 1>(args, stream);
+    case 128 * 4 + 2: return launch_f16<128, 2, 2>(args, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace himuon

@@ -402,6 +402,256 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     Z[rb][q][2 * i + 1] = __uint_as_float(W[rb][q][i] & 0xffff0000u) * sc;
                 }
 
+        // The K steps of a tile split over two waves (a 128-tile, two row
+        // blocks per wave). Work that needs only the wave's own rows is issued
+        // on both sides of each exchange barrier, and each accumulator
+        // conversion is spread over the MFMAs of the next product that does
+        // not depend on it:
+        //   Gram own blocks | barrier | own Z rows to LDS | Gram own blocks |
+        //   barrier | Gram other blocks (+ own H conversion) | other H
+        //   conversion | own H rows to LDS | P own blocks | barrier | P own
+        //   blocks | P other blocks (+ own P conversion) | other P conversion |
+        //   PZ, columns of the first half | PZ, second half (+ conversion of
+        //   the first half into the next step's operands).
+        // The first barrier of a step keeps the other wave's reads of the
+        // previous Z copy ahead of this wave's overwrite of its own rows.
+        auto ns_steps_wide = [&]() {
+          if constexpr (F16Shape<T, RB>::kWide) {
+            constexpr int HIT = IT / 2;
+            constexpr int NH = NB / 2;  // output column blocks per PZ half
+            u32x4 Zop[RB][NB][S];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int q = 0; q < NB; ++q)
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Zop[rb][q][s] = make_slot<OP>(Z[rb][q], s);
+            for (int k = 0; k < args.K; ++k) {
+                // ---- H = Z Z^T; G[rb][j] is block (p0 + rb, (p0 + j) mod NB)
+                f32x16 G[RB][NB];
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) G[rb][j] = f32x16{};
+                auto gram_own = [&](int it) {
+                    const int q = it / S, s = it % S;
+#pragma unroll
+                    for (int j = 0; j < RB; ++j)
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb) G[rb][j] = mma1<OP>(Zop[j][q][s], Zop[rb][q][s], G[rb][j]);
+                };
+#pragma unroll
+                for (int it = 0; it < HIT; ++it) gram_own(it);
+                __builtin_amdgcn_sched_barrier(0);
+                if (k > 0) __syncthreads();
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int N = 0; N < NB; ++N)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g)
+                            *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * N) =
+                                u32x2{Zop[rb][N][g >> 1][(g & 1) * 2], Zop[rb][N][g >> 1][(g & 1) * 2 + 1]};
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int it = HIT; it < IT; ++it) gram_own(it);
+                __builtin_amdgcn_sched_barrier(0);
+                __syncthreads();
+
+                // Gram other blocks; the own blocks' conversions (H slots and
+                // the diagonal H + sigma b' I) ride along, one slot per iteration
+                u32x4 Hop[RB][NB][S], Q0[RB][S];
+                auto conv_own_h = [&](int c) {  // c = 0 .. RB*RB*S + RB*S - 1
+                    if (c < RB * RB * S) {
+                        const int rb = c / (RB * S), j = (c / S) % RB, s = c % S;
+                        Hop[rb][j][s] = make_slot<OP>(G[rb][j], s);
+                    } else {
+                        const int rb = (c - RB * RB * S) / S, s = c % S;
+                        f32x16 gd = G[rb][rb];
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) gd[v] += v == vdiag ? args.bq : 0.f;
+                        Q0[rb][s] = make_slot<OP>(gd, s);
+                    }
+                };
+                constexpr int NCH = RB * RB * S + RB * S;  // own-block conversions
+                {
+                    u32x4 nxt_op[NOA];
+#pragma unroll
+                    for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = rowpiece(rm_row[jo], 0, 0);
+#pragma unroll
+                    for (int it = 0; it < IT; ++it) {
+                        const int q = it / S, s = it % S;
+                        u32x4 cur_op[NOA];
+#pragma unroll
+                        for (int jo = 0; jo < NO; ++jo) cur_op[jo] = nxt_op[jo];
+                        if (it + 1 < IT) {
+#pragma unroll
+                            for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = rowpiece(rm_row[jo], (it + 1) / S, (it + 1) % S);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int jo = 0; jo < NO; ++jo)
+#pragma unroll
+                            for (int rb = 0; rb < RB; ++rb)
+                                G[rb][RB + jo] = mma1<OP>(cur_op[jo], Zop[rb][q][s], G[rb][RB + jo]);
+                        // conversions it * NCH / IT .. (it + 1) * NCH / IT - 1
+#pragma unroll
+                        for (int c = it * NCH / IT; c < (it + 1) * NCH / IT; ++c) conv_own_h(c);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int jo = 0; jo < NO; ++jo)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) Hop[rb][RB + jo][s] = make_slot<OP>(G[rb][RB + jo], s);
+
+                u32x4 Pop[RB][NB][S];
+                if constexpr (CMODE != 2) {
+                    // ---- acc = H (H + sigma b' I) + sigma a I (so sigma acc = aI + P)
+                    f32x16 acc[RB][NB];
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int j = 0; j < NB; ++j) acc[rb][j] = j == rb ? diag_a : f32x16{};
+                    auto p_opb = [&](int rb, int jk, int s) -> u32x4 { return jk == rb ? Q0[rb][s] : Hop[rb][jk][s]; };
+                    auto p_own = [&](int it) {
+                        const int jk = it / S, s = it % S;
+#pragma unroll
+                        for (int j = 0; j < RB; ++j)
+#pragma unroll
+                            for (int rb = 0; rb < RB; ++rb) acc[rb][j] = mma1<OP>(Hop[j][jk][s], p_opb(rb, jk, s), acc[rb][j]);
+                    };
+                    // own H rows to the slots, one slot per own-block MFMA pair
+                    constexpr int NHW = RB * NB * S;
+#pragma unroll
+                    for (int it = 0; it < HIT; ++it) {
+                        p_own(it);
+#pragma unroll
+                        for (int c = it * NHW / HIT; c < (it + 1) * NHW / HIT; ++c) {
+                            const int rb = c / (NB * S), j = (c / S) % NB, s = c % S;
+                            slots[(((p0 + rb) * NB + (p0 + j) % NB) * S + s) * 64 + lane] = Hop[rb][j][s];
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                    __syncthreads();
+                    auto h_slot = [&](int jo, int it) -> u32x4 {
+                        const int jk = it / S, s = it % S;
+                        return sl_row[jo][(((p0 + jk) % NB) * S + s) * 64];
+                    };
+                    u32x4 nxt_op[NOA];
+#pragma unroll
+                    for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = h_slot(jo, 0);
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int it = HIT; it < IT; ++it) p_own(it);
+                    __builtin_amdgcn_sched_barrier(0);
+                    // P other blocks; the own blocks' conversions ride along
+                    constexpr int NCP = RB * RB * S;
+#pragma unroll
+                    for (int it = 0; it < IT; ++it) {
+                        const int jk = it / S, s = it % S;
+                        u32x4 cur_op[NOA];
+#pragma unroll
+                        for (int jo = 0; jo < NO; ++jo) cur_op[jo] = nxt_op[jo];
+                        if (it + 1 < IT) {
+#pragma unroll
+                            for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = h_slot(jo, it + 1);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int jo = 0; jo < NO; ++jo)
+#pragma unroll
+                            for (int rb = 0; rb < RB; ++rb)
+                                acc[rb][RB + jo] = mma1<OP>(cur_op[jo], p_opb(rb, jk, s), acc[rb][RB + jo]);
+#pragma unroll
+                        for (int c = it * NCP / IT; c < (it + 1) * NCP / IT; ++c) {
+                            const int rb = c / (RB * S), j = (c / S) % RB, sc2 = c % S;
+                            if constexpr (CMODE == 0) Pop[rb][j][sc2] = make_slot<OP>(acc[rb][j], sc2);
+                            else Pop[rb][j][sc2] = make_slot<OP>(-acc[rb][j], sc2);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int jo = 0; jo < NO; ++jo)
+#pragma unroll
+                            for (int s = 0; s < S; ++s) {
+                                if constexpr (CMODE == 0) Pop[rb][RB + jo][s] = make_slot<OP>(acc[rb][RB + jo], s);
+                                else Pop[rb][RB + jo][s] = make_slot<OP>(-acc[rb][RB + jo], s);
+                            }
+                } else {
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int j = 0; j < NB; ++j) {
+                            const f32x16 pj = j == rb ? G[rb][j] * args.bq + diag_a : G[rb][j] * args.bq;
+#pragma unroll
+                            for (int s = 0; s < S; ++s) Pop[rb][j][s] = make_slot<OP>(pj, s);
+                        }
+                }
+
+                // ---- Z <- (a I + P) Z by halves of the output columns; the
+                // first half's conversion into next-step operands rides along
+                // with the second half
+                auto col_piece = [&](int it, int N) -> u32x4 {
+                    const int jk = it / S, s = it % S;
+                    const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 16 * s * RS + 64 * N;
+                    const u32x2 lo = tr_read(kb + tr_off[0]);
+                    const u32x2 hi = tr_read(kb + tr_off[1]);
+                    return u32x4{lo[0], lo[1], hi[0], hi[1]};
+                };
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int n = 0; n < NH; ++n) Z[rb][NH * h + n] = f32x16{};
+                    u32x4 nxt_op[NH];
+#pragma unroll
+                    for (int n = 0; n < NH; ++n) nxt_op[n] = col_piece(0, NH * h + n);
+                    constexpr int NCZ = RB * NH * S;
+#pragma unroll
+                    for (int it = 0; it < IT; ++it) {
+                        const int jk = it / S, s = it % S;
+                        u32x4 cur_op[NH];
+#pragma unroll
+                        for (int n = 0; n < NH; ++n) cur_op[n] = nxt_op[n];
+                        if (it + 1 < IT) {
+#pragma unroll
+                            for (int n = 0; n < NH; ++n) nxt_op[n] = col_piece(it + 1, NH * h + n);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int n = 0; n < NH; ++n)
+#pragma unroll
+                            for (int rb = 0; rb < RB; ++rb)
+                                Z[rb][NH * h + n] = mma1<OP>(cur_op[n], Pop[rb][jk][s], Z[rb][NH * h + n]);
+                        if (h == 1) {  // (after the last step these operands go unused)
+#pragma unroll
+                            for (int c = it * NCZ / IT; c < (it + 1) * NCZ / IT; ++c) {
+                                const int rb = c / (NH * S), n = (c / S) % NH, sc2 = c % S;
+                                Zop[rb][n][sc2] = make_slot<OP>(Z[rb][n], sc2);
+                            }
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int n = NH; n < NB; ++n)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) Zop[rb][n][s] = make_slot<OP>(Z[rb][n], s);
+            }
+            // the other wave's last reads of this wave's rows come before the
+            // write-back reuses them
+            if (args.K > 0) __syncthreads();
+          }
+        };
+
         // One Newton-Schulz step.
         auto ns_step = [&]() {
             u32x4 Zop[RB][NB][S];
@@ -587,7 +837,9 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             }
             if constexpr (SHARED) __syncthreads();  // the row-major copy and the H slots are rewritten next step
         };
-        for (int k = 0; k < args.K; ++k) ns_step();
+        if constexpr (F16Shape<T, RB>::kWide) ns_steps_wide();
+        else
+            for (int k = 0; k < args.K; ++k) ns_step();
 
         // row pieces (scaled back, rounded to bf16) into the own rows of the
         // row-major copy, then read back as whole 16-byte row chunks

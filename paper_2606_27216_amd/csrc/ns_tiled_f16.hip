@@ -119,7 +119,9 @@ template <int T, int RB> struct F16Shape {
     static constexpr int TPW = WT > 1 ? 1 : 4;
     static constexpr int kThreads = 64 * WT * TPW;
     static constexpr bool kWide = T == 128 && RB == 2;
-    static constexpr int kMinWavesPerEU = kWide ? 1 : 2;
+    // a 256-tile: one per CU, four waves of two row blocks, chain-form step
+    static constexpr bool kChain = T == 256;
+    static constexpr int kMinWavesPerEU = (kWide || kChain) ? 1 : 2;
     // next tile's loads issued before the K loop (registers permitting)
     static constexpr bool kEarlyPrefetch = kWide;
 };
@@ -148,7 +150,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     constexpr int RM = T * RS;
     constexpr int IT = NB * S;      // k iterations of one product
 
-    __shared__ u32x4 s_slots[SHARED ? TPW * MAT : 1];
+    __shared__ u32x4 s_slots[(SHARED && !F16Shape<T, RB>::kChain) ? TPW * MAT : 1];
     __shared__ __attribute__((aligned(16))) uint8_t s_rm[TPW * RM];
     __shared__ float s_red[6][SHARED ? WT : 1];  // 2 tile parities x 3 reductions
 
@@ -392,6 +394,12 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         }
         parity ^= 1;
         f32x16 Z[RB][NB];
+        // the result as packed bf16 row pieces (word 2g + i: columns 8g + 4lh + 2i, +1)
+        uint32_t OB[RB][NB][8];
+        auto pack_out = [&](const f32x16& z, uint32_t (&ob)[8]) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ob[i] = pack2<Operand::BF16>(z[2 * i] * args.unscale, z[2 * i + 1] * args.unscale);
+        };
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -652,6 +660,222 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
           }
         };
 
+        // The K steps of a 256-tile (one tile per CU, four waves of two row
+        // blocks each). Its fp16 copy fills the LDS, so H is never exchanged:
+        // each step is evaluated in the equivalent chain form
+        //     Y = sigma (H + sigma b' I) Z,   Z <- a Z + H Y,
+        // with H's own rows kept in registers. Column block N of Y depends
+        // only on column block N of Z, so Y replaces Z in the row-major copy
+        // one column half at a time:
+        //   Z own rows to LDS | barrier | Gram | Y, first half | barrier |
+        //   Y first half to LDS | Y, second half | barrier | Y second half to
+        //   LDS | HY, first half | barrier | HY, second half.
+        // Products run on groups of NG column blocks, which bounds the
+        // accumulators to 64 registers; each HY group is converted at once
+        // into the next step's fp16 operands, from which the bf16 output is
+        // rounded after the last step (for K = 0 too, so that no fp32 copy of
+        // the tile stays live across the steps). The barrier at the top of each later step keeps
+        // the other waves' reads of Y ahead of this wave's overwrite of its rows.
+        auto ns_steps_chain = [&]() {
+          if constexpr (F16Shape<T, RB>::kChain) {
+            constexpr int NG = 2;       // column blocks per product group
+            constexpr int NGR = NB / NG;
+            constexpr int NH = NB / 2;  // column blocks per half
+            u32x4 Zop[RB][NB][S];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int q = 0; q < NB; ++q)
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Zop[rb][q][s] = make_slot<OP>(Z[rb][q], s);
+            // own rows (row pieces) of a 16-bit operand matrix into the copy
+            auto put_rows = [&](const u32x4 (&V)[RB][NB][S], int n0, int n1) {
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int N = n0; N < n1; ++N)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g)
+                            *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * N) =
+                                u32x2{V[rb][N][g >> 1][(g & 1) * 2], V[rb][N][g >> 1][(g & 1) * 2 + 1]};
+            };
+            auto col_piece = [&](int it, int N) -> u32x4 {
+                const int jk = it / S, s = it % S;
+                const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 16 * s * RS + 64 * N;
+                const u32x2 lo = tr_read(kb + tr_off[0]);
+                const u32x2 hi = tr_read(kb + tr_off[1]);
+                return u32x4{lo[0], lo[1], hi[0], hi[1]};
+            };
+            // acc[rb][n] += sum over the rotated k-blocks of col(., n0 + n) x B(rb, jk, s)
+            auto col_product = [&](f32x16 (&acc)[RB][NG], int n0, auto&& bop) {
+                u32x4 nxt_op[NG];
+#pragma unroll
+                for (int n = 0; n < NG; ++n) nxt_op[n] = col_piece(0, n0 + n);
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int jk = it / S, s = it % S;
+                    u32x4 cur_op[NG];
+#pragma unroll
+                    for (int n = 0; n < NG; ++n) cur_op[n] = nxt_op[n];
+                    if (it + 1 < IT) {
+#pragma unroll
+                        for (int n = 0; n < NG; ++n) nxt_op[n] = col_piece(it + 1, n0 + n);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int n = 0; n < NG; ++n)
+#pragma unroll
+                        for (int rb = 0; rb < RB; ++rb) acc[rb][n] = mma1<OP>(cur_op[n], bop(rb, jk, s), acc[rb][n]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            };
+            for (int k = 0; k < args.K; ++k) {
+                if (k > 0) __syncthreads();
+                put_rows(Zop, 0, NB);
+                __syncthreads();
+
+                // ---- H = Z Z^T by groups of NG rotated column blocks;
+                // G[rb][jj] is block (p0 + rb, (p0 + NG gq + jj) mod NB)
+                u32x4 Hop[RB][NB][S], Q0[RB][S];
+#pragma unroll
+                for (int gq = 0; gq < NGR; ++gq) {
+                    f32x16 G[RB][NG];
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int jj = 0; jj < NG; ++jj) G[rb][jj] = f32x16{};
+                    auto opa = [&](int j, int q, int s) -> u32x4 {
+                        return j < RB ? Zop[j < RB ? j : 0][q][s] : rowpiece(rm_row[j < RB ? 0 : j - RB], q, s);
+                    };
+                    u32x4 nxt_op[NG];
+#pragma unroll
+                    for (int jj = 0; jj < NG; ++jj) nxt_op[jj] = opa(NG * gq + jj, 0, 0);
+#pragma unroll
+                    for (int it = 0; it < IT; ++it) {
+                        const int q = it / S, s = it % S;
+                        u32x4 cur_op[NG];
+#pragma unroll
+                        for (int jj = 0; jj < NG; ++jj) cur_op[jj] = nxt_op[jj];
+                        if (it + 1 < IT) {
+#pragma unroll
+                            for (int jj = 0; jj < NG; ++jj) nxt_op[jj] = opa(NG * gq + jj, (it + 1) / S, (it + 1) % S);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int jj = 0; jj < NG; ++jj)
+#pragma unroll
+                            for (int rb = 0; rb < RB; ++rb) G[rb][jj] = mma1<OP>(cur_op[jj], Zop[rb][q][s], G[rb][jj]);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int jj = 0; jj < NG; ++jj) {
+                            const int j = NG * gq + jj;
+                            const f32x16 gj = CMODE == 2 ? G[rb][jj] * args.bq : G[rb][jj];
+#pragma unroll
+                            for (int s = 0; s < S; ++s) Hop[rb][j][s] = make_slot<OP>(gj, s);
+                            if (CMODE != 2 && j == rb) {
+                                f32x16 gd = G[rb][jj];
+#pragma unroll
+                                for (int v = 0; v < 16; ++v) gd[v] += v == vdiag ? args.bq : 0.f;
+#pragma unroll
+                                for (int s = 0; s < S; ++s) Q0[rb][s] = make_slot<OP>(gd, s);
+                            }
+                        }
+                }
+                auto hb = [&](int rb, int jk, int s) -> u32x4 { return Hop[rb][jk][s]; };
+                auto hqb = [&](int rb, int jk, int s) -> u32x4 { return jk == rb ? Q0[rb][s] : Hop[rb][jk][s]; };
+                // a Z (fp16 state, exact products) as the seed of the last product
+                auto seed = [&](f32x16 (&acc)[RB][NG], int n0) {
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int n = 0; n < NG; ++n)
+#pragma unroll
+                            for (int s = 0; s < S; ++s)
+#pragma unroll
+                                for (int w = 0; w < 4; ++w) {
+                                    // (copied out first: a bit cast of a vector element
+                                    // would read the vector's first element)
+                                    const uint32_t wv = Zop[rb][n0 + n][s][w];
+                                    const f16x2 pr = __builtin_bit_cast(f16x2, wv);
+                                    acc[rb][n][8 * s + 2 * w] = args.a * (float)pr[0];
+                                    acc[rb][n][8 * s + 2 * w + 1] = args.a * (float)pr[1];
+                                }
+                };
+                // a finished group of Z becomes next step's operands (after the
+                // last step, the output is rounded from these fp16 values)
+                auto finish = [&](f32x16 (&acc)[RB][NG], int n0) {
+#pragma unroll
+                    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                        for (int n = 0; n < NG; ++n)
+#pragma unroll
+                            for (int s = 0; s < S; ++s) Zop[rb][n0 + n][s] = make_slot<OP>(acc[rb][n], s);
+                };
+                auto hy_group = [&](int gq) {
+                    f32x16 acc[RB][NG];
+                    seed(acc, NG * gq);
+                    col_product(acc, NG * gq, hb);
+                    finish(acc, NG * gq);
+                };
+                if constexpr (CMODE == 2) {
+                    // c = 0: Z <- a Z + b H Z, the H Z product reading Z itself
+#pragma unroll
+                    for (int gq = 0; gq < NGR; ++gq) hy_group(gq);
+                } else {
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        u32x4 Yop[RB][NB][S];  // (only column half h is set)
+#pragma unroll
+                        for (int gq = h * NGR / 2; gq < (h + 1) * NGR / 2; ++gq) {
+                            f32x16 acc[RB][NG];
+#pragma unroll
+                            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                                for (int n = 0; n < NG; ++n) acc[rb][n] = f32x16{};
+                            col_product(acc, NG * gq, hqb);
+#pragma unroll
+                            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                                for (int n = 0; n < NG; ++n)
+#pragma unroll
+                                    for (int s = 0; s < S; ++s)
+                                        Yop[rb][NG * gq + n][s] = make_slot<OP>(CMODE == 1 ? -acc[rb][n] : acc[rb][n], s);
+                        }
+                        __syncthreads();  // every wave is done reading this column half of Z
+                        put_rows(Yop, NH * h, NH * (h + 1));
+                    }
+                    // Z <- a Z + H Y, by column halves
+#pragma unroll
+                    for (int gq = 0; gq < NGR / 2; ++gq) hy_group(gq);
+                    __syncthreads();  // the second half of Y is visible
+#pragma unroll
+                    for (int gq = NGR / 2; gq < NGR; ++gq) hy_group(gq);
+                }
+            }
+            // the other waves' last reads of this wave's rows come before the
+            // write-back reuses them
+            {
+                if (args.K > 0) __syncthreads();
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int q = 0; q < NB; ++q)
+#pragma unroll
+                        for (int s = 0; s < S; ++s)
+#pragma unroll
+                            for (int w = 0; w < 4; ++w) {
+                                const uint32_t wv = Zop[rb][q][s][w];
+                                const f16x2 pr = __builtin_bit_cast(f16x2, wv);
+                                OB[rb][q][4 * s + w] = pack2<Operand::BF16>((float)pr[0] * args.unscale,
+                                                                            (float)pr[1] * args.unscale);
+                            }
+            }
+          }
+        };
+
         // One Newton-Schulz step.
         auto ns_step = [&]() {
             u32x4 Zop[RB][NB][S];
@@ -838,22 +1062,26 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             if constexpr (SHARED) __syncthreads();  // the row-major copy and the H slots are rewritten next step
         };
         if constexpr (F16Shape<T, RB>::kWide) ns_steps_wide();
+        else if constexpr (F16Shape<T, RB>::kChain) ns_steps_chain();
         else
             for (int k = 0; k < args.K; ++k) ns_step();
 
         // row pieces (scaled back, rounded to bf16) into the own rows of the
         // row-major copy, then read back as whole 16-byte row chunks
+        if constexpr (!F16Shape<T, RB>::kChain) {  // (the chain step packs its own output)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int q = 0; q < NB; ++q) pack_out(Z[rb][q], OB[rb][q]);
+        }
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int q = 0; q < NB; ++q)
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const f32x4 v = f32x4{Z[rb][q][4 * g + 0], Z[rb][q][4 * g + 1], Z[rb][q][4 * g + 2],
-                                          Z[rb][q][4 * g + 3]} * args.unscale;
+                for (int g = 0; g < 4; ++g)
                     *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q) =
-                        u32x2{pack2<Operand::BF16>(v[0], v[1]), pack2<Operand::BF16>(v[2], v[3])};
-                }
+                        u32x2{OB[rb][q][2 * g], OB[rb][q][2 * g + 1]};
 #pragma unroll
         for (int i = 0; i < NI; ++i) outv[i] = *reinterpret_cast<const u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row));
         prv = cur;
@@ -920,6 +1148,9 @@ hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream
     case 128 * 4 + 0: return launch_f16<128, 2, 0>(args, stream);
     case 128 * 4 + 1: return launch_f16<128, 2, 1>(args, stream);
     case 128 * 4 + 2: return launch_f16<128, 2, 2>(args, stream);
+    case 256 * 4 + 0: return launch_f16<256, 2, 0>(args, stream);
+    case 256 * 4 + 1: return launch_f16<256, 2, 1>(args, stream);
+    case 256 * 4 + 2: return launch_f16<256, 2, 2>(args, stream);
     default: return hipErrorInvalidValue;
     }
 }

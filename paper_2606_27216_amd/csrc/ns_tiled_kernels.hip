@@ -410,6 +410,7 @@ hipError_t launch_T(int T, const KernelArgs& args, hipStream_t stream)
 
 bool has_kernel(int T, Storage st, Operand op)
 {
+    if (T == 256) return st == Storage::BF16 && op == Operand::F16;  // fp16-operand kernel only
     const bool t_ok = T == 32 || T == 64 || T == 128;
     if (!t_ok) return false;
     if (st == Storage::F32) return op == Operand::F32;

@@ -29,6 +29,12 @@ def run(mats, T, K=5, coeffs=COEF32, compute=hm.COMPUTE_DEFAULT, budget=0, outpu
     return out
 
 
+def tile_sizes(dtype):
+    """Tile sizes with a kernel for this storage type: T = 256 exists for bf16
+    storage (fp16 operands) only."""
+    return (32, 64, 128, 256) if dtype == "bf16" else (32, 64, 128)
+
+
 def check_full(x, y, T, K=5, coeffs=COEF32, tol=None):
     S = to_f64(x)
     R = oracle.ns_tiled(S, T, K, *coeffs)
@@ -50,7 +56,7 @@ def test_config1_fp32_T32():
     assert len(e) == 64
 
 
-@pytest.mark.parametrize("T", [32, 64, 128])
+@pytest.mark.parametrize("T", [32, 64, 128, 256])
 def test_config2_bf16(T):
     announce(f"4096x4096 bf16 low-rank+noise seed 2, T={T}, K=5")
     x = workloads.lowrank_plus_noise(4096, 4096, 2, "bf16", DEV)
@@ -87,7 +93,9 @@ def test_config5_heterogeneous_schedule(dtype, K):
     """24 heavy-tailed matrices, the runtime tile schedule over successive calls."""
     mats = workloads.heterogeneous(dtype, DEV)
     rng = np.random.default_rng(5)
-    for T in (128, 64, 32):
+    # the schedule T = 256 -> 128 -> 64; fp32 storage has no T = 256 kernel
+    # and runs 128 -> 64 -> 32
+    for T in ((256, 128, 64) if dtype == "bf16" else (128, 64, 32)):
         announce(f"heterogeneous batch {dtype} K={K} T={T}")
         outs = run(mats, T, K=K)
         for i in (0, 9, 17):  # one matrix of each shape
@@ -115,8 +123,7 @@ def test_config5_fp32_K8_every_tile(T):
 RAGGED = [(100, 300), (257, 129), (33, 4096), (1, 1), (5, 700), (130, 2), (64, 64)]
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("T", [32, 64, 128])
+@pytest.mark.parametrize("dtype,T", [(d, T) for d in ("f32", "bf16") for T in tile_sizes(d)])
 def test_ragged_heterogeneous_batch(dtype, T):
     announce(f"ragged batch {dtype} T={T}")
     mats = [workloads.gaussian(h, w, 40 + i, dtype, DEV) for i, (h, w) in enumerate(RAGGED)]
@@ -134,6 +141,13 @@ def test_single_padded_tile_is_full_map(dtype):
     ref = oracle.phi_k(to_f64(x), 5, *COEF32)
     e = np.linalg.norm(to_f64(y) - ref) / np.linalg.norm(ref)
     assert e <= TOL[x.dtype]
+    if dtype == "bf16":
+        x = workloads.gaussian(200, 256, 12, dtype, DEV)
+        (y,) = run([x], 256)
+        ref = oracle.phi_k(to_f64(x), 5, *COEF32)
+        e = np.linalg.norm(to_f64(y) - ref) / np.linalg.norm(ref)
+        print(f"[gpu-err] 200x256 as one 256-tile: {e:.3e}", flush=True)
+        assert e <= TOL[x.dtype]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -141,7 +155,7 @@ def test_single_padded_tile_is_full_map(dtype):
 def test_step_counts(dtype, K):
     announce(f"K={K} {dtype}")
     x = workloads.student_t(300, 200, 8, dtype, DEV)
-    for T in (32, 64, 128):
+    for T in tile_sizes(dtype):
         (y,) = run([x], T, K=K)
         check_full(x, y, T, K=K)
 
@@ -156,24 +170,44 @@ def test_other_coefficients(coeffs):
         check_full(x, y, T, K=6, coeffs=coeffs)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_zero_and_nonfinite_tiles_stay_contained(dtype):
-    announce(f"zero / NaN / Inf tiles {dtype}")
-    x = workloads.gaussian(128, 192, 10, dtype, DEV)
-    x[0:64, 64:128] = 0
-    (clean,) = run([x], 64)
+@pytest.mark.parametrize("coeffs", [(1.5, -0.5, 0.0), (1.5, -0.25, -0.25), (2.0, -1.5, 0.5)])
+def test_other_coefficients_bf16(coeffs):
+    """bf16 storage: the fp16 kernels specialise on sign(c) (c > 0, c < 0,
+    c = 0); every specialisation at every tile size."""
+    announce(f"coefficients {coeffs} bf16")
+    coeffs = tuple(float(np.float32(v)) for v in coeffs)
+    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 6, *coeffs) == hm.COMPUTE_F16
+    x = workloads.gaussian(300, 520, 13, "bf16", DEV)
+    for T in tile_sizes("bf16"):
+        (y,) = run([x], T, K=6, coeffs=coeffs)
+        check_full(x, y, T, K=6, coeffs=coeffs)
+
+
+def test_fp32_storage_has_no_256_kernel():
+    x = workloads.gaussian(256, 256, 14, "f32", DEV)
+    with pytest.raises(hm.HimuonError) as err:
+        run([x], 256)
+    assert err.value.status == hm.ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("dtype,T", [("f32", 64), ("bf16", 64), ("bf16", 256)])
+def test_zero_and_nonfinite_tiles_stay_contained(dtype, T):
+    announce(f"zero / NaN / Inf tiles {dtype} T={T}")
+    x = workloads.gaussian(2 * T, 3 * T, 10, dtype, DEV)
+    x[0:T, T:2 * T] = 0
+    (clean,) = run([x], T)
     bad = x.clone()
-    bad[64:128, 0:64][3, 5] = float("nan")
-    bad[64:128, 128:192][0, 0] = float("inf")
-    (y,) = run([bad], 64)
-    assert torch.count_nonzero(clean[0:64, 64:128]) == 0
-    assert not torch.isfinite(y[64:128, 0:64]).all()
-    assert not torch.isfinite(y[64:128, 128:192]).all()
+    bad[T:2 * T, 0:T][3, 5] = float("nan")
+    bad[T:2 * T, 2 * T:3 * T][0, 0] = float("inf")
+    (y,) = run([bad], T)
+    assert torch.count_nonzero(clean[0:T, T:2 * T]) == 0
+    assert not torch.isfinite(y[T:2 * T, 0:T]).all()
+    assert not torch.isfinite(y[T:2 * T, 2 * T:3 * T]).all()
     keep = torch.ones_like(x, dtype=torch.bool)
-    keep[64:128, 0:64] = False
-    keep[64:128, 128:192] = False
+    keep[T:2 * T, 0:T] = False
+    keep[T:2 * T, 2 * T:3 * T] = False
     assert torch.equal(y[keep], clean[keep])
-    check_full(x, clean, 64)
+    check_full(x, clean, T)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -225,8 +259,7 @@ def test_batching_chunking_permutation_bitwise(dtype):
     assert torch.equal(yq, yp)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("T", [32, 64, 128])
+@pytest.mark.parametrize("dtype,T", [(d, T) for d in ("f32", "bf16") for T in tile_sizes(d)])
 def test_determinism_scale_sign(dtype, T):
     announce(f"determinism / 2^e scale / sign {dtype} T={T}")
     x = workloads.student_t(256, 384, 80, dtype, DEV)

@@ -108,15 +108,17 @@ int resolve_compute(int dtype, int compute, int K, float a, float b, float c)
     if (compute == HIMUON_COMPUTE_F32) return HIMUON_ERR_UNSUPPORTED;
     if (compute == HIMUON_COMPUTE_BF16) return HIMUON_COMPUTE_BF16;
     // fp16 operands (kernel state Z = X |c|^(1/4), H = Z Z^T): Z, H,
-    // H + sigma b' I and P = b' H + sigma H^2 must stay far below 65504, and
-    // so must the bf16-operand path's A = X X^T and B = bA + cA^2.
+    // H + sigma b' I, the step operator a I + sigma H (H + sigma b' I), and
+    // the 256-tile chain operand Y = sigma (H + sigma b' I) Z must stay far
+    // below 65504, and so must the bf16-operand path's A = X X^T and
+    // B = bA + cA^2. Entries are bounded by spectral norms.
     const double M = 4.0 * iterate_bound(K, a, b, c);
     const double zs = c != 0.f ? pow(fabs((double)c), 0.25) : 1.0;
     const double bp = c != 0.f ? fabs((double)b) / sqrt(fabs((double)c)) : fabs((double)b);
     const double Mz = M * zs, MH = Mz * Mz;
     const double M2 = M * M;
-    const double bound = fmax(fmax(fmax(Mz, MH + bp), bp * MH + MH * MH),
-                              fmax(M2, fabs((double)b) * M2 + fabs((double)c) * M2 * M2));
+    const double fp16_ops = fmax(fmax(Mz, MH + bp), fmax(fabs((double)a) + bp * MH + MH * MH, (MH + bp) * Mz));
+    const double bound = fmax(fp16_ops, fmax(M2, fabs((double)b) * M2 + fabs((double)c) * M2 * M2));
     const bool safe = bound < 16384.0;
     if (compute == HIMUON_COMPUTE_F16) return safe ? HIMUON_COMPUTE_F16 : HIMUON_ERR_RANGE;
     return safe ? HIMUON_COMPUTE_F16 : HIMUON_COMPUTE_BF16;

@@ -17,24 +17,27 @@ using namespace dev;
 
 // ------------------------------------------------ fp16-operand kernel
 //
-// Same tile map, restructured so that almost no vector-ALU work is left in
-// the K loop. The state is Z = X |c|^(1/4) (exact rescaling of the iterate),
-// for which one step of eq. (ns_iteration) reads
-//     Z <- a Z + P Z,   P = sigma H (H + sigma b' I),   H = Z Z^T,
-// with b' = b / sqrt|c| and sigma = sign(c): the c-coefficient becomes +-1
-// and b' moves onto the diagonal of an MFMA operand, so the only per-element
-// multiply left is the fp32 a*Z that seeds the product accumulator (the a*Z
-// term stays in fp32, which keeps rounding out of the directions the
-// iteration amplifies). The normalisation multiplies by |c|^(1/4) and the
-// store by |c|^(-1/4). c = 0 takes P = b H.
+// Same tile map, restructured so that no vector-ALU work but the fp16
+// conversions is left in the K loop. The state is Z = X |c|^(1/4) (exact
+// rescaling of the iterate), for which one step of eq. (ns_iteration) reads
+//     Z <- (a I + P) Z,   P = sigma H (H + sigma b' I),   H = Z Z^T,
+// with b' = b / sqrt|c| and sigma = sign(c): the c-coefficient becomes +-1,
+// b' moves onto the diagonal of an MFMA operand, and a I seeds the diagonal
+// blocks of the P accumulator, so a step is three MFMA products. Between
+// steps the iterate is held as fp16 operands only (near convergence a I + P
+// has eigenvalues of order one, so rounding its product does not amplify).
+// The normalisation multiplies by |c|^(1/4) and the store by |c|^(-1/4).
+// c = 0 takes a I + b H.
 //
 // Z is shared through one row-major fp16 copy of the tile (see kRowStride).
 // Gram operands of the other waves' rows are read from it as row pieces; the
-// B X operand (column pieces of Z) comes from it through ds_read_b64_tr_b16,
-// which returns in every lane quad a 4x4 transpose of four rows supplied by
-// the other lanes of its 16-lane group. H is shared through 16-byte
-// lane-ordered slots. A wave works on the blocks of its row in the rotated
-// order J = (p + j) mod NB, so its own row blocks come from registers.
+// column operands of the third product come from it through
+// ds_read_b64_tr_b16, which returns in every lane quad a 4x4 transpose of
+// four rows supplied by the other lanes of its 16-lane group. H is shared
+// through 16-byte lane-ordered slots (a 256-tile has no room for them and
+// uses a regrouped step, see ns_steps_chain). A wave works on the blocks of
+// its row in the rotated order J = (p + j) mod NB, so its own row blocks come
+// from registers.
 //
 // Tiles are processed in rounds; the HBM loads of a wave's next tile are
 // issued before the current tile is written back.

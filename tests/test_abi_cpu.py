@@ -93,6 +93,10 @@ def test_select_compute():
     assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_F16, 20, 2.0, 0.0, 0.0) == hm.ERR_RANGE
     # the textbook cubic iteration stays bounded
     assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 60, 1.5, -0.5, 0.0) == hm.COMPUTE_F16
+    # one step's operator a I + P carries |a| itself: a large a alone must
+    # move the call off fp16 operands
+    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 1, 20000.0, 0.0, 0.0) == hm.COMPUTE_BF16
+    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_F16, 1, 20000.0, 0.0, 0.0) == hm.ERR_RANGE
 
 
 def _qwen(model):

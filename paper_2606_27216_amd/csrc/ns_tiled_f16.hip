@@ -102,13 +102,22 @@ HM_DEV u32x2 tr_read(const uint8_t* ptr)
     return __builtin_bit_cast(u32x2, v);
 }
 
-// Row-major fp16 copy of Z. Bytes per row: an odd multiple of 64, so the
-// eight consecutive rows a transposing read touches (64 bytes each) fall on
-// four distinct quarters of the 256-byte bank space, twice each. Within each
-// 64-byte segment (32 columns) the 8-byte chunk c of row r sits at chunk
-// c ^ 2((r >> 2) & 3): rows r, r+4, ..., r+28 share a quarter, and the XOR
-// spreads their row-piece chunks (2g + lh) over all eight chunks, so
-// row-piece reads and writes (32 rows x 16 bytes) are conflict-free as well.
+// Row-major fp16 copy of Z. Bytes per row: an odd multiple of 64 (or 64
+// past an even one), so that the row offset modulo the 256-byte bank space
+// steps by a quarter (64 bytes) between consecutive rows. Within each 64-byte
+// segment (32 columns) the 8-byte chunk c of row r sits at chunk
+// c ^ rm_swz(r). On gfx950 (measured with the LDS bank-conflict counter):
+// ds_read_b64 and ds_read_b64_tr_b16 serve 32 lanes per pass from 64 banks,
+// ds_write_b64 16 consecutive lanes per pass from 32 banks (128 bytes), and
+// ds_read_b128 16 lanes per pass, lanes {0-7, 24-31} and {8-15, 16-23} of
+// each half wave together. A row-piece access touches one chunk of each of
+// 32 consecutive rows: the row offset separates rows by r mod 4 (reads) or
+// r mod 2 (writes), and the swizzle takes eight distinct values over the
+// remaining row bits of each pass (bits 2-4 resp. 1-3), so both are
+// conflict-free. A transposing read touches 8 chunks of 4 consecutive rows
+// per pass, which the row offset alone separates.
+HM_DEV int rm_swz(int r) { return ((r >> 1) & 7) ^ ((r >> 4) & 1); }
+
 template <int T> constexpr int kRowStride = ((2 * T / 64) % 2 == 1) ? 2 * T : 2 * T + 64;
 
 // Workgroup shape of the fp16 kernel. A tile split over WT > 1 waves is
@@ -164,21 +173,23 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     u32x4* const slots = s_slots + (SHARED ? tslot * MAT : 0);
     uint8_t* const rm = s_rm + tslot * RM;
     // Row pieces: this lane's columns 32q + 8g + 4lh of row li of a block are
-    // chunk 2g + lh of the block's segment, stored at chunk 2(g ^ fl) + lh.
-    const int fl = (li >> 2) & 3;
+    // chunk 2g + lh of the block's segment q.
     int rp_off[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) rp_off[g] = li * RS + 16 * (g ^ fl) + 8 * lh;
+    for (int g = 0; g < 4; ++g) rp_off[g] = li * RS + 8 * ((2 * g + lh) ^ rm_swz(li));
     // Transposing reads: supplier lane 4q' + m of 16-lane group G addresses
-    // row 4(G/2) + m (+ 8x) and logical chunk 4(G%2) + q' of a block segment.
+    // row 16s + 4(G/2) + m (+ 8x) and logical chunk 4(G%2) + q' of a block
+    // segment, for the k half s of the block.
     const int grp16 = lane >> 4;
-    int tr_off[2];
+    int tr_off[S][2];
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-        const int row = 8 * x + 4 * (grp16 >> 1) + ((lane & 15) >> 2);
-        const int chunk = 4 * (grp16 & 1) + (lane & 3);
-        tr_off[x] = row * RS + 8 * (chunk ^ (2 * ((row >> 2) & 3)));
-    }
+    for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            const int row = 16 * s + 8 * x + 4 * (grp16 >> 1) + ((lane & 15) >> 2);
+            const int chunk = 4 * (grp16 & 1) + (lane & 3);
+            tr_off[s][x] = row * RS + 8 * (chunk ^ rm_swz(row));
+        }
     // A diagonal block holds row li's column 8g + 4lh + e in register 4g + e,
     // so the diagonal entry of this lane (if any) is register vdiag.
     const int vdiag = (lh == ((li >> 2) & 1)) ? 4 * (li >> 3) + (li & 3) : -1;
@@ -263,9 +274,14 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             }
         }
     };
-    // byte offset of the 16-byte chunk io_cc of tile row `row` in the row-major copy
+    // byte offset of the 16-byte chunk io_cc of tile row `row` in the row-major
+    // copy: its two 8-byte halves sit in one aligned 16-byte pair, swapped
+    // when rm_swz(row) is odd (io_swap exchanges them in registers)
     auto io_lds = [&](int row) -> int {
-        return row * RS + 64 * (io_cc >> 2) + 8 * ((2 * (io_cc & 3)) ^ (2 * ((row >> 2) & 3)));
+        return row * RS + 64 * (io_cc >> 2) + 16 * ((io_cc & 3) ^ (rm_swz(row) >> 1));
+    };
+    auto io_swap = [&](const u32x4& v, int row) -> u32x4 {
+        return (rm_swz(row) & 1) ? u32x4{v[2], v[3], v[0], v[1]} : v;
     };
 
     // Whole row segments of the own rows to HBM (16-byte chunks read back from
@@ -339,7 +355,10 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         // bf16 words; only this wave touches these rows until its first
         // step's barrier
 #pragma unroll
-        for (int i = 0; i < NI; ++i) *reinterpret_cast<u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row)) = raw[i];
+        for (int i = 0; i < NI; ++i) {
+            const int row = 32 * p0 + RPI * i + io_row;
+            *reinterpret_cast<u32x4*>(rm + io_lds(row)) = io_swap(raw[i], row);
+        }
         if (pending) store_rows(prv, outv);
         if constexpr (EARLY) {
             if (has_next) issue_loads(nxt);  // in flight for the whole K loop
@@ -609,9 +628,9 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                 // with the second half
                 auto col_piece = [&](int it, int N) -> u32x4 {
                     const int jk = it / S, s = it % S;
-                    const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 16 * s * RS + 64 * N;
-                    const u32x2 lo = tr_read(kb + tr_off[0]);
-                    const u32x2 hi = tr_read(kb + tr_off[1]);
+                    const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 64 * N;
+                    const u32x2 lo = tr_read(kb + tr_off[s][0]);
+                    const u32x2 hi = tr_read(kb + tr_off[s][1]);
                     return u32x4{lo[0], lo[1], hi[0], hi[1]};
                 };
 #pragma unroll
@@ -704,9 +723,9 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             };
             auto col_piece = [&](int it, int N) -> u32x4 {
                 const int jk = it / S, s = it % S;
-                const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 16 * s * RS + 64 * N;
-                const u32x2 lo = tr_read(kb + tr_off[0]);
-                const u32x2 hi = tr_read(kb + tr_off[1]);
+                const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 64 * N;
+                const u32x2 lo = tr_read(kb + tr_off[s][0]);
+                const u32x2 hi = tr_read(kb + tr_off[s][1]);
                 return u32x4{lo[0], lo[1], hi[0], hi[1]};
             };
             // acc[rb][n] += sum over the rotated k-blocks of col(., n0 + n) x B(rb, jk, s)
@@ -1036,9 +1055,9 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             {
                 auto col_piece = [&](int it, int N) -> u32x4 {
                     const int jk = it / S, s = it % S;
-                    const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 16 * s * RS + 64 * N;
-                    const u32x2 lo = tr_read(kb + tr_off[0]);
-                    const u32x2 hi = tr_read(kb + tr_off[1]);
+                    const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 64 * N;
+                    const u32x2 lo = tr_read(kb + tr_off[s][0]);
+                    const u32x2 hi = tr_read(kb + tr_off[s][1]);
                     return u32x4{lo[0], lo[1], hi[0], hi[1]};
                 };
                 u32x4 nxt_op[NB];
@@ -1086,7 +1105,10 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q) =
                         u32x2{OB[rb][q][2 * g], OB[rb][q][2 * g + 1]};
 #pragma unroll
-        for (int i = 0; i < NI; ++i) outv[i] = *reinterpret_cast<const u32x4*>(rm + io_lds(32 * p0 + RPI * i + io_row));
+        for (int i = 0; i < NI; ++i) {
+            const int row = 32 * p0 + RPI * i + io_row;
+            outv[i] = io_swap(*reinterpret_cast<const u32x4*>(rm + io_lds(row)), row);
+        }
         prv = cur;
         pending = true;
         // (raw is defined on both paths, so the values staged at the top of

@@ -33,11 +33,12 @@ using namespace dev;
 // Gram operands of the other waves' rows are read from it as row pieces; the
 // column operands of the third product come from it through
 // ds_read_b64_tr_b16, which returns in every lane quad a 4x4 transpose of
-// four rows supplied by the other lanes of its 16-lane group. H is shared
-// through 16-byte lane-ordered slots (a 256-tile has no room for them and
-// uses a regrouped step, see ns_steps_chain). A wave works on the blocks of
-// its row in the rotated order J = (p + j) mod NB, so its own row blocks come
-// from registers.
+// four rows supplied by the other lanes of its 16-lane group. A 128-tile
+// computes only the upper blocks of the symmetric H and aI + P and shares
+// them as 32x32 fp16 blocks (see ns_steps_sym); a 256-tile has no room for
+// them and uses a regrouped step (see ns_steps_chain). Tiles of one wave
+// need no sharing. A wave works on the blocks of its row in the rotated
+// order J = (p + j) mod NB, so its own row blocks come from registers.
 //
 // Tiles are processed in rounds; the HBM loads of a wave's next tile are
 // issued before the current tile is written back.
@@ -133,6 +134,8 @@ template <int T, int RB> struct F16Shape {
     static constexpr bool kWide = T == 128 && RB == 2;
     // a 256-tile: one per CU, four waves of two row blocks, chain-form step
     static constexpr bool kChain = T == 256;
+    // a 128-tile evaluates only the upper blocks of the symmetric H and aI + P
+    static constexpr bool kSym = kWide;
     static constexpr int kMinWavesPerEU = (kWide || kChain) ? 1 : 2;
     // next tile's loads issued before the K loop (registers permitting)
     static constexpr bool kEarlyPrefetch = kWide;
@@ -432,249 +435,361 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     Z[rb][q][2 * i + 1] = __uint_as_float(W[rb][q][i] & 0xffff0000u) * sc;
                 }
 
-        // The K steps of a tile split over two waves (a 128-tile, two row
-        // blocks per wave). Work that needs only the wave's own rows is issued
-        // on both sides of each exchange barrier, and each accumulator
-        // conversion is spread over the MFMAs of the next product that does
-        // not depend on it:
-        //   Gram own blocks | barrier | own Z rows to LDS | Gram own blocks |
-        //   barrier | Gram other blocks (+ own H conversion) | other H
-        //   conversion | own H rows to LDS | P own blocks | barrier | P own
-        //   blocks | P other blocks (+ own P conversion) | other P conversion |
-        //   PZ, columns of the first half | PZ, second half (+ conversion of
-        //   the first half into the next step's operands).
-        // The first barrier of a step keeps the other wave's reads of the
-        // previous Z copy ahead of this wave's overwrite of its own rows.
-        auto ns_steps_wide = [&]() {
-          if constexpr (F16Shape<T, RB>::kWide) {
-            constexpr int HIT = IT / 2;
-            constexpr int NH = NB / 2;  // output column blocks per PZ half
-            u32x4 Zop[RB][NB][S];
+        // The K steps of a 128-tile split over two waves, using the symmetry
+        // of H = Z Z^T and of aI + P (a polynomial in H): of the 16 blocks
+        // of each, only the ten on and above the block diagonal are
+        // computed, five per wave. Wave w owns row blocks r0 = 2w, r1 = r0+1
+        // and computes blocks (r0,r0), (r0,r1), (r1,r1), (r0,o_w) and
+        // (r1,o_{1-w}), o_0 < o_1 being the other wave's row blocks; the
+        // other wave's cross blocks are then (o_0, r_{1-w}) and (o_1, r_w),
+        // so each upper block is computed exactly once. Blocks are stored in
+        // LDS as 32x32 fp16 arrays (64-byte rows, the Z copy's chunk
+        // swizzle); a block needed in the other orientation is read with
+        // ds_read_b64_tr_b16. Diagonal H blocks are stored with the shift
+        // sigma b' I, the form in which the other wave uses them. Per step:
+        //   Gram (r0,r0), part of (r0,r1), with the conversion of Z into
+        //   operands | barrier | own Z rows to LDS + rest of the own Gram
+        //   blocks | barrier | Gram cross blocks (+ own H conversions and
+        //   stores) | cross H stores | P terms on own blocks | barrier | P
+        //   terms on the other wave's blocks (+ conversions) | P stores | PZ
+        //   over the own k-blocks | barrier | PZ over the other k-blocks.
+        auto ns_steps_sym = [&]() {
+          if constexpr (F16Shape<T, RB>::kSym) {
+            static_assert(NB == 4 && RB == 2 && S == 2, "two waves of two 32-row blocks");
+            const int w = p0 / RB, wo = 1 - w;
+            const int ot = 2 * wo + w;      // o_t: the other block of this wave's (r0, .) cross block
+            const int on = 2 * wo + 1 - w;  // o_{1-t}: that of (r1, .)
+            uint8_t* const hb = reinterpret_cast<uint8_t*>(slots);
+            // H blocks of wave v: 0 (r0,r0)', 1 (r0,r1), 2 (r1,r1)', 3 (r0,o_t), 4 (r1,o_{1-t});
+            // P blocks: 0 (r0,r1), 1 (r0,o_t), 2 (r1,o_{1-t})
+            auto hblk = [&](int v, int e) -> uint8_t* { return hb + 2048 * (5 * v + e); };
+            auto pblk = [&](int v, int e) -> uint8_t* { return hb + 2048 * (10 + 3 * v + e); };
+            int bp_off[4];
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
+            for (int g = 0; g < 4; ++g) bp_off[g] = li * 64 + 8 * ((2 * g + lh) ^ rm_swz(li));
+            int btr_off[S][2];
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+#pragma unroll
+                for (int x = 0; x < 2; ++x) {
+                    const int row = 16 * s + 8 * x + 4 * (grp16 >> 1) + ((lane & 15) >> 2);
+                    const int chunk = 4 * (grp16 & 1) + (lane & 3);
+                    btr_off[s][x] = row * 64 + 8 * (chunk ^ rm_swz(row));
+                }
+            // slot s of a stored block: its rows (lane = row), or the rows of its transpose
+            auto blk_rows = [&](const uint8_t* b, int s) -> u32x4 {
+                const u32x2 lo = *reinterpret_cast<const u32x2*>(b + bp_off[2 * s]);
+                const u32x2 hi = *reinterpret_cast<const u32x2*>(b + bp_off[2 * s + 1]);
+                return u32x4{lo[0], lo[1], hi[0], hi[1]};
+            };
+            auto blk_tr = [&](const uint8_t* b, int s) -> u32x4 {
+                const u32x2 lo = tr_read(b + btr_off[s][0]);
+                const u32x2 hi = tr_read(b + btr_off[s][1]);
+                return u32x4{lo[0], lo[1], hi[0], hi[1]};
+            };
+            // write quarter g (columns 8g + 4lh .. +3 of each row) of a block given as two slots
+            auto blk_put = [&](uint8_t* b, const u32x4 (&v)[S], int g) {
+                *reinterpret_cast<u32x2*>(b + bp_off[g]) = u32x2{v[g >> 1][(g & 1) * 2], v[g >> 1][(g & 1) * 2 + 1]};
+            };
+            // column pieces of Z's row block `br`, k half s, output block n
+            auto zcol = [&](int br, int s, int n) -> u32x4 {
+                const uint8_t* const kb = rm + 32 * br * RS + 64 * n;
+                const u32x2 lo = tr_read(kb + tr_off[s][0]);
+                const u32x2 hi = tr_read(kb + tr_off[s][1]);
+                return u32x4{lo[0], lo[1], hi[0], hi[1]};
+            };
+            auto zrow = [&](int br, int q, int s) -> u32x4 { return rowpiece(rm + 32 * br * RS, q, s); };
+            auto shifted = [&](const f32x16& gd) -> f32x16 {
+                f32x16 r = gd;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) r[v] += v == vdiag ? args.bq : 0.f;
+                return r;
+            };
+
+            for (int k = 0; k < args.K; ++k) {
+                // ---- Gram. The operands of the current Z are made here, each
+                // right before its first product.
+                u32x4 Zop[RB][NB][S];
+                f32x16 g[5];
+#pragma unroll
+                for (int e = 0; e < 5; ++e) g[e] = f32x16{};
 #pragma unroll
                 for (int q = 0; q < NB; ++q)
 #pragma unroll
-                    for (int s = 0; s < S; ++s) Zop[rb][q][s] = make_slot<OP>(Z[rb][q], s);
-            for (int k = 0; k < args.K; ++k) {
-                // ---- H = Z Z^T; G[rb][j] is block (p0 + rb, (p0 + j) mod NB)
-                f32x16 G[RB][NB];
+                    for (int s = 0; s < S; ++s) {
+                        Zop[0][q][s] = make_slot<OP>(Z[0][q], s);
+                        g[0] = mma1<OP>(Zop[0][q][s], Zop[0][q][s], g[0]);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
+                for (int q = 0; q < 2; ++q)
 #pragma unroll
-                    for (int j = 0; j < NB; ++j) G[rb][j] = f32x16{};
-                auto gram_own = [&](int it) {
-                    const int q = it / S, s = it % S;
+                    for (int s = 0; s < S; ++s) {
+                        Zop[1][q][s] = make_slot<OP>(Z[1][q], s);
+                        g[1] = mma1<OP>(Zop[1][q][s], Zop[0][q][s], g[1]);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
 #pragma unroll
-                    for (int j = 0; j < RB; ++j)
+                for (int q = 2; q < NB; ++q)
 #pragma unroll
-                        for (int rb = 0; rb < RB; ++rb) G[rb][j] = mma1<OP>(Zop[j][q][s], Zop[rb][q][s], G[rb][j]);
-                };
+                    for (int s = 0; s < S; ++s) Zop[1][q][s] = make_slot<OP>(Z[1][q], s);
+                // the other wave's reads of the previous Z copy are done
+                __syncthreads();
+                // own Z rows into the copy (32 stores), spread over the 12
+                // remaining own-block products
 #pragma unroll
-                for (int it = 0; it < HIT; ++it) gram_own(it);
-                __builtin_amdgcn_sched_barrier(0);
-                if (k > 0) __syncthreads();
+                for (int c = 0; c < 12; ++c) {
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                    for (int N = 0; N < NB; ++N)
-#pragma unroll
-                        for (int g = 0; g < 4; ++g)
-                            *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * N) =
-                                u32x2{Zop[rb][N][g >> 1][(g & 1) * 2], Zop[rb][N][g >> 1][(g & 1) * 2 + 1]};
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int it = HIT; it < IT; ++it) gram_own(it);
-                __builtin_amdgcn_sched_barrier(0);
+                    for (int i = c * 32 / 12; i < (c + 1) * 32 / 12; ++i) {
+                        const int rb = i / 16, N = (i / 4) % 4, gq = i % 4;
+                        *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[gq] + 64 * N) =
+                            u32x2{Zop[rb][N][gq >> 1][(gq & 1) * 2], Zop[rb][N][gq >> 1][(gq & 1) * 2 + 1]};
+                    }
+                    if (c < 4) {
+                        const int q = 2 + c / 2, s = c % 2;
+                        g[1] = mma1<OP>(Zop[1][q][s], Zop[0][q][s], g[1]);
+                    } else {
+                        const int q = (c - 4) / 2, s = c % 2;
+                        g[2] = mma1<OP>(Zop[1][q][s], Zop[1][q][s], g[2]);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
                 __syncthreads();
 
-                // Gram other blocks; the own blocks' conversions (H slots and
-                // the diagonal H + sigma b' I) ride along, one slot per iteration
-                u32x4 Hop[RB][NB][S], Q0[RB][S];
-                auto conv_own_h = [&](int c) {  // c = 0 .. RB*RB*S + RB*S - 1
-                    if (c < RB * RB * S) {
-                        const int rb = c / (RB * S), j = (c / S) % RB, s = c % S;
-                        Hop[rb][j][s] = make_slot<OP>(G[rb][j], s);
-                    } else {
-                        const int rb = (c - RB * RB * S) / S, s = c % S;
-                        f32x16 gd = G[rb][rb];
-#pragma unroll
-                        for (int v = 0; v < 16; ++v) gd[v] += v == vdiag ? args.bq : 0.f;
-                        Q0[rb][s] = make_slot<OP>(gd, s);
-                    }
-                };
-                constexpr int NCH = RB * RB * S + RB * S;  // own-block conversions
+                // ---- Gram cross blocks (r0, o_t), (r1, o_{1-t}) from the other
+                // wave's Z rows; the own blocks' conversions and stores ride along
+                u32x4 hs[5][S], qs[2][S];
                 {
-                    u32x4 nxt_op[NOA];
-#pragma unroll
-                    for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = rowpiece(rm_row[jo], 0, 0);
+                    u32x4 nxt[2] = {zrow(ot, 0, 0), zrow(on, 0, 0)};
 #pragma unroll
                     for (int it = 0; it < IT; ++it) {
                         const int q = it / S, s = it % S;
-                        u32x4 cur_op[NOA];
-#pragma unroll
-                        for (int jo = 0; jo < NO; ++jo) cur_op[jo] = nxt_op[jo];
+                        const u32x4 c0 = nxt[0], c1 = nxt[1];
                         if (it + 1 < IT) {
-#pragma unroll
-                            for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = rowpiece(rm_row[jo], (it + 1) / S, (it + 1) % S);
+                            nxt[0] = zrow(ot, (it + 1) / S, (it + 1) % S);
+                            nxt[1] = zrow(on, (it + 1) / S, (it + 1) % S);
                         }
                         __builtin_amdgcn_sched_barrier(0);
+                        g[3] = mma1<OP>(c0, Zop[0][q][s], g[3]);
+                        g[4] = mma1<OP>(c1, Zop[1][q][s], g[4]);
+                        if constexpr (CMODE != 2) {
+                            if (it == 0) {
 #pragma unroll
-                        for (int jo = 0; jo < NO; ++jo)
+                                for (int x = 0; x < S; ++x) hs[0][x] = make_slot<OP>(g[0], x);
+                            } else if (it == 1) {
+                                const f32x16 gd = shifted(g[0]);
 #pragma unroll
-                            for (int rb = 0; rb < RB; ++rb)
-                                G[rb][RB + jo] = mma1<OP>(cur_op[jo], Zop[rb][q][s], G[rb][RB + jo]);
-                        // conversions it * NCH / IT .. (it + 1) * NCH / IT - 1
+                                for (int x = 0; x < S; ++x) qs[0][x] = make_slot<OP>(gd, x);
+                            } else if (it == 2) {
 #pragma unroll
-                        for (int c = it * NCH / IT; c < (it + 1) * NCH / IT; ++c) conv_own_h(c);
+                                for (int x = 0; x < S; ++x) hs[1][x] = make_slot<OP>(g[1], x);
+                            } else if (it == 3) {
+#pragma unroll
+                                for (int x = 0; x < S; ++x) hs[2][x] = make_slot<OP>(g[2], x);
+                            } else if (it == 4) {
+                                const f32x16 gd = shifted(g[2]);
+#pragma unroll
+                                for (int x = 0; x < S; ++x) qs[1][x] = make_slot<OP>(gd, x);
+                            } else if (it == 5) {
+#pragma unroll
+                                for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 0), qs[0], gq);
+                            } else if (it == 6) {
+#pragma unroll
+                                for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 1), hs[1], gq);
+                            } else {
+#pragma unroll
+                                for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 2), qs[1], gq);
+                            }
+                        }
                         __builtin_amdgcn_sched_barrier(0);
                     }
                 }
-#pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                    for (int jo = 0; jo < NO; ++jo)
-#pragma unroll
-                        for (int s = 0; s < S; ++s) Hop[rb][RB + jo][s] = make_slot<OP>(G[rb][RB + jo], s);
 
-                u32x4 Pop[RB][NB][S];
+                u32x4 pop[5][S];
                 if constexpr (CMODE != 2) {
-                    // ---- acc = H (H + sigma b' I) + sigma a I (so sigma acc = aI + P)
-                    f32x16 acc[RB][NB];
 #pragma unroll
-                    for (int rb = 0; rb < RB; ++rb)
+                    for (int x = 0; x < S; ++x) hs[3][x] = make_slot<OP>(g[3], x);
 #pragma unroll
-                        for (int j = 0; j < NB; ++j) acc[rb][j] = j == rb ? diag_a : f32x16{};
-                    auto p_opb = [&](int rb, int jk, int s) -> u32x4 { return jk == rb ? Q0[rb][s] : Hop[rb][jk][s]; };
-                    auto p_own = [&](int it) {
-                        const int jk = it / S, s = it % S;
+                    for (int x = 0; x < S; ++x) hs[4][x] = make_slot<OP>(g[4], x);
+                    // ---- P (as acc = H (H + sigma b' I) + sigma a I): block (i, j)
+                    // accumulates H'[j, k] x H[i, k] over the k-blocks
+                    f32x16 pa[5];
+                    pa[0] = diag_a;
+                    pa[1] = f32x16{};
+                    pa[2] = diag_a;
+                    pa[3] = f32x16{};
+                    pa[4] = f32x16{};
+                    u32x4 la1[S];  // H[r1, r0]
 #pragma unroll
-                        for (int j = 0; j < RB; ++j)
+                    for (int s = 0; s < S; ++s) la1[s] = blk_tr(hblk(w, 1), s);
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                            for (int rb = 0; rb < RB; ++rb) acc[rb][j] = mma1<OP>(Hop[j][jk][s], p_opb(rb, jk, s), acc[rb][j]);
-                    };
-                    // own H rows to the slots, one slot per own-block MFMA pair
-                    constexpr int NHW = RB * NB * S;
+                    for (int s = 0; s < S; ++s) {
+                        pa[0] = mma1<OP>(qs[0][s], hs[0][s], pa[0]);  // k = r0
+                        pa[1] = mma1<OP>(qs[1][s], hs[1][s], pa[1]);  // k = r1
+                        pa[2] = mma1<OP>(qs[1][s], hs[2][s], pa[2]);  // k = r1
+                        pa[0] = mma1<OP>(hs[1][s], hs[1][s], pa[0]);  // k = r1
+                        pa[1] = mma1<OP>(la1[s], hs[0][s], pa[1]);    // k = r0
+                        pa[2] = mma1<OP>(la1[s], la1[s], pa[2]);      // k = r0
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
 #pragma unroll
-                    for (int it = 0; it < HIT; ++it) {
-                        p_own(it);
+                    for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 3), hs[3], gq);
 #pragma unroll
-                        for (int c = it * NHW / HIT; c < (it + 1) * NHW / HIT; ++c) {
-                            const int rb = c / (NB * S), j = (c / S) % NB, s = c % S;
-                            slots[(((p0 + rb) * NB + (p0 + j) % NB) * S + s) * 64 + lane] = Hop[rb][j][s];
-                        }
+                    for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 4), hs[4], gq);
+                    u32x4 lb1[S], lb6[S];  // H[o_t, r0], H[o_{1-t}, r1]
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        lb1[s] = blk_tr(hblk(w, 3), s);
+                        lb6[s] = blk_tr(hblk(w, 4), s);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        pa[0] = mma1<OP>(hs[3][s], hs[3][s], pa[0]);  // k = o_t
+                        pa[2] = mma1<OP>(hs[4][s], hs[4][s], pa[2]);  // k = o_{1-t}
+                        pa[3] = mma1<OP>(lb1[s], hs[0][s], pa[3]);    // (r0, o_t), k = r0
+                        pa[4] = mma1<OP>(lb6[s], hs[2][s], pa[4]);    // (r1, o_{1-t}), k = r1
                         __builtin_amdgcn_sched_barrier(0);
                     }
                     __syncthreads();
-                    auto h_slot = [&](int jo, int it) -> u32x4 {
-                        const int jk = it / S, s = it % S;
-                        return sl_row[jo][(((p0 + jk) % NB) * S + s) * 64];
+                    // the other wave's blocks
+                    u32x4 la2[S], la3[S], lb2[S], lb3[S], lb4[S], lb5[S], lb7[S], lb8[S];
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        la2[s] = blk_tr(hblk(wo, 4 - w), s);     // H[r0, o_{1-t}]
+                        la3[s] = blk_tr(hblk(wo, 3 + w), s);     // H[r1, o_t]
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        lb2[s] = blk_rows(hblk(wo, 3 + w), s);      // H[o_t, r1]
+                        lb3[s] = blk_rows(hblk(wo, 2 * w), s);      // H'[o_t, o_t]
+                        const u32x4 nrm = blk_rows(hblk(wo, 1), s); // H[o_0, o_1]
+                        const u32x4 trn = blk_tr(hblk(wo, 1), s);   // H[o_1, o_0]
+                        lb4[s] = w ? trn : nrm;                     // H[o_t, o_{1-t}]
+                        lb7[s] = w ? nrm : trn;                     // H[o_{1-t}, o_t]
+                        lb5[s] = blk_rows(hblk(wo, 4 - w), s);      // H[o_{1-t}, r0]
+                        lb8[s] = blk_rows(hblk(wo, 2 - 2 * w), s);  // H'[o_{1-t}, o_{1-t}]
+                    }
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        pa[0] = mma1<OP>(la2[s], la2[s], pa[0]);    // k = o_{1-t}
+                        pa[1] = mma1<OP>(la3[s], hs[3][s], pa[1]);  // k = o_t
+                        pa[2] = mma1<OP>(la3[s], la3[s], pa[2]);    // k = o_t
+                        pa[1] = mma1<OP>(hs[4][s], la2[s], pa[1]);  // k = o_{1-t}
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                    auto pconv = [&](int e) {
+#pragma unroll
+                        for (int x = 0; x < S; ++x) {
+                            if constexpr (CMODE == 0) pop[e][x] = make_slot<OP>(pa[e], x);
+                            else pop[e][x] = make_slot<OP>(-pa[e], x);
+                        }
                     };
-                    u32x4 nxt_op[NOA];
 #pragma unroll
-                    for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = h_slot(jo, 0);
-                    __builtin_amdgcn_sched_barrier(0);
+                    for (int s = 0; s < S; ++s) {
+                        pa[3] = mma1<OP>(lb2[s], hs[1][s], pa[3]);  // (r0, o_t), k = r1
+                        pa[4] = mma1<OP>(lb5[s], la1[s], pa[4]);    // (r1, o_{1-t}), k = r0
+                        pa[3] = mma1<OP>(lb3[s], hs[3][s], pa[3]);  // k = o_t
+                        pa[4] = mma1<OP>(lb7[s], la3[s], pa[4]);    // k = o_t
+                        pa[3] = mma1<OP>(lb4[s], la2[s], pa[3]);    // k = o_{1-t}
+                        pa[4] = mma1<OP>(lb8[s], hs[4][s], pa[4]);  // k = o_{1-t}
+                        if (s == 0) {
+                            pconv(0);
+                            pconv(1);
+                        } else {
+                            pconv(2);
 #pragma unroll
-                    for (int it = HIT; it < IT; ++it) p_own(it);
-                    __builtin_amdgcn_sched_barrier(0);
-                    // P other blocks; the own blocks' conversions ride along
-                    constexpr int NCP = RB * RB * S;
-#pragma unroll
-                    for (int it = 0; it < IT; ++it) {
-                        const int jk = it / S, s = it % S;
-                        u32x4 cur_op[NOA];
-#pragma unroll
-                        for (int jo = 0; jo < NO; ++jo) cur_op[jo] = nxt_op[jo];
-                        if (it + 1 < IT) {
-#pragma unroll
-                            for (int jo = 0; jo < NO; ++jo) nxt_op[jo] = h_slot(jo, it + 1);
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                        for (int jo = 0; jo < NO; ++jo)
-#pragma unroll
-                            for (int rb = 0; rb < RB; ++rb)
-                                acc[rb][RB + jo] = mma1<OP>(cur_op[jo], p_opb(rb, jk, s), acc[rb][RB + jo]);
-#pragma unroll
-                        for (int c = it * NCP / IT; c < (it + 1) * NCP / IT; ++c) {
-                            const int rb = c / (RB * S), j = (c / S) % RB, sc2 = c % S;
-                            if constexpr (CMODE == 0) Pop[rb][j][sc2] = make_slot<OP>(acc[rb][j], sc2);
-                            else Pop[rb][j][sc2] = make_slot<OP>(-acc[rb][j], sc2);
+                            for (int gq = 0; gq < 4; ++gq) blk_put(pblk(w, 0), pop[1], gq);
                         }
                         __builtin_amdgcn_sched_barrier(0);
                     }
-#pragma unroll
-                    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                        for (int jo = 0; jo < NO; ++jo)
-#pragma unroll
-                            for (int s = 0; s < S; ++s) {
-                                if constexpr (CMODE == 0) Pop[rb][RB + jo][s] = make_slot<OP>(acc[rb][RB + jo], s);
-                                else Pop[rb][RB + jo][s] = make_slot<OP>(-acc[rb][RB + jo], s);
-                            }
+                    pconv(3);
+                    pconv(4);
                 } else {
+                    // c = 0: aI + P = a I + b H, straight from the Gram blocks
 #pragma unroll
-                    for (int rb = 0; rb < RB; ++rb)
+                    for (int e = 0; e < 5; ++e) {
+                        const f32x16 pe = (e == 0 || e == 2) ? g[e] * args.bq + diag_a : g[e] * args.bq;
 #pragma unroll
-                        for (int j = 0; j < NB; ++j) {
-                            const f32x16 pj = j == rb ? G[rb][j] * args.bq + diag_a : G[rb][j] * args.bq;
-#pragma unroll
-                            for (int s = 0; s < S; ++s) Pop[rb][j][s] = make_slot<OP>(pj, s);
-                        }
-                }
-
-                // ---- Z <- (a I + P) Z by halves of the output columns; the
-                // first half's conversion into next-step operands rides along
-                // with the second half
-                auto col_piece = [&](int it, int N) -> u32x4 {
-                    const int jk = it / S, s = it % S;
-                    const uint8_t* const kb = rm + 32 * ((p0 + jk) % NB) * RS + 64 * N;
-                    const u32x2 lo = tr_read(kb + tr_off[s][0]);
-                    const u32x2 hi = tr_read(kb + tr_off[s][1]);
-                    return u32x4{lo[0], lo[1], hi[0], hi[1]};
-                };
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-#pragma unroll
-                    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                        for (int n = 0; n < NH; ++n) Z[rb][NH * h + n] = f32x16{};
-                    u32x4 nxt_op[NH];
-#pragma unroll
-                    for (int n = 0; n < NH; ++n) nxt_op[n] = col_piece(0, NH * h + n);
-                    constexpr int NCZ = RB * NH * S;
-#pragma unroll
-                    for (int it = 0; it < IT; ++it) {
-                        const int jk = it / S, s = it % S;
-                        u32x4 cur_op[NH];
-#pragma unroll
-                        for (int n = 0; n < NH; ++n) cur_op[n] = nxt_op[n];
-                        if (it + 1 < IT) {
-#pragma unroll
-                            for (int n = 0; n < NH; ++n) nxt_op[n] = col_piece(it + 1, NH * h + n);
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                        for (int n = 0; n < NH; ++n)
-#pragma unroll
-                            for (int rb = 0; rb < RB; ++rb)
-                                Z[rb][NH * h + n] = mma1<OP>(cur_op[n], Pop[rb][jk][s], Z[rb][NH * h + n]);
-                        if (h == 1) {  // (after the last step these operands go unused)
-#pragma unroll
-                            for (int c = it * NCZ / IT; c < (it + 1) * NCZ / IT; ++c) {
-                                const int rb = c / (NH * S), n = (c / S) % NH, sc2 = c % S;
-                                Zop[rb][n][sc2] = make_slot<OP>(Z[rb][n], sc2);
-                            }
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
+                        for (int x = 0; x < S; ++x) pop[e][x] = make_slot<OP>(pe, x);
                     }
+#pragma unroll
+                    for (int gq = 0; gq < 4; ++gq) blk_put(pblk(w, 0), pop[1], gq);
                 }
+#pragma unroll
+                for (int gq = 0; gq < 4; ++gq) blk_put(pblk(w, 1), pop[3], gq);
+#pragma unroll
+                for (int gq = 0; gq < 4; ++gq) blk_put(pblk(w, 2), pop[4], gq);
+
+                // ---- Z <- (a I + P) Z. k-blocks r0 and r1 need only this
+                // wave's blocks ((aI + P)[r1, r0] is the transpose of its own
+                // (r0, r1) block); o_t and o_{1-t} follow the barrier.
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-                    for (int n = NH; n < NB; ++n)
+                    for (int n = 0; n < NB; ++n) Z[rb][n] = f32x16{};
+                u32x4 lp1[S];  // (aI + P)[r1, r0]
 #pragma unroll
-                        for (int s = 0; s < S; ++s) Zop[rb][n][s] = make_slot<OP>(Z[rb][n], s);
+                for (int s = 0; s < S; ++s) lp1[s] = blk_tr(pblk(w, 0), s);
+                {
+                    u32x4 nxt[NB];
+#pragma unroll
+                    for (int n = 0; n < NB; ++n) nxt[n] = zcol(p0, 0, n);
+#pragma unroll
+                    for (int it = 0; it < 2 * S; ++it) {
+                        const int kb = it / S, s = it % S;  // k-block r0 + kb
+                        u32x4 cur[NB];
+#pragma unroll
+                        for (int n = 0; n < NB; ++n) cur[n] = nxt[n];
+                        if (it + 1 < 2 * S) {
+#pragma unroll
+                            for (int n = 0; n < NB; ++n) nxt[n] = zcol(p0 + (it + 1) / S, (it + 1) % S, n);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                        const u32x4 a0 = kb == 0 ? pop[0][s] : pop[1][s];
+                        const u32x4 a1 = kb == 0 ? lp1[s] : pop[2][s];
+#pragma unroll
+                        for (int n = 0; n < NB; ++n) {
+                            Z[0][n] = mma1<OP>(cur[n], a0, Z[0][n]);
+                            Z[1][n] = mma1<OP>(cur[n], a1, Z[1][n]);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+                __syncthreads();
+                {
+                    u32x4 lp2[S], lp3[S];  // (aI + P)[r0, o_{1-t}], (aI + P)[r1, o_t]
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        lp2[s] = blk_tr(pblk(wo, 2 - w), s);
+                        lp3[s] = blk_tr(pblk(wo, 1 + w), s);
+                    }
+                    u32x4 nxt[NB];
+#pragma unroll
+                    for (int n = 0; n < NB; ++n) nxt[n] = zcol(ot, 0, n);
+#pragma unroll
+                    for (int it = 0; it < 2 * S; ++it) {
+                        const int kb = it / S, s = it % S;  // k-block o_t, then o_{1-t}
+                        u32x4 cur[NB];
+#pragma unroll
+                        for (int n = 0; n < NB; ++n) cur[n] = nxt[n];
+                        if (it + 1 < 2 * S) {
+#pragma unroll
+                            for (int n = 0; n < NB; ++n) nxt[n] = zcol((it + 1) / S == 0 ? ot : on, (it + 1) % S, n);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                        const u32x4 a0 = kb == 0 ? pop[3][s] : lp2[s];
+                        const u32x4 a1 = kb == 0 ? lp3[s] : pop[4][s];
+#pragma unroll
+                        for (int n = 0; n < NB; ++n) {
+                            Z[0][n] = mma1<OP>(cur[n], a0, Z[0][n]);
+                            Z[1][n] = mma1<OP>(cur[n], a1, Z[1][n]);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
             }
             // the other wave's last reads of this wave's rows come before the
             // write-back reuses them
@@ -1083,7 +1198,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             }
             if constexpr (SHARED) __syncthreads();  // the row-major copy and the H slots are rewritten next step
         };
-        if constexpr (F16Shape<T, RB>::kWide) ns_steps_wide();
+        if constexpr (F16Shape<T, RB>::kSym) ns_steps_sym();
         else if constexpr (F16Shape<T, RB>::kChain) ns_steps_chain();
         else
             for (int k = 0; k < args.K; ++k) ns_step();

@@ -165,7 +165,9 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     constexpr int RM = T * RS;
     constexpr int IT = NB * S;      // k iterations of one product
 
-    __shared__ u32x4 s_slots[(SHARED && !F16Shape<T, RB>::kChain) ? TPW * MAT : 1];
+    // H slots; for the symmetric 128-tile step, 18 blocks of 32x32 fp16 (12 of H, 6 of aI + P)
+    constexpr int NSLOT = F16Shape<T, RB>::kSym ? 18 * 2048 / 16 : ((SHARED && !F16Shape<T, RB>::kChain) ? TPW * MAT : 1);
+    __shared__ u32x4 s_slots[NSLOT];
     __shared__ __attribute__((aligned(16))) uint8_t s_rm[TPW * RM];
     __shared__ float s_red[6][SHARED ? WT : 1];  // 2 tile parities x 3 reductions
 
@@ -459,46 +461,61 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             const int w = p0 / RB, wo = 1 - w;
             const int ot = 2 * wo + w;      // o_t: the other block of this wave's (r0, .) cross block
             const int on = 2 * wo + 1 - w;  // o_{1-t}: that of (r1, .)
-            uint8_t* const hb = reinterpret_cast<uint8_t*>(slots);
-            // H blocks of wave v: 0 (r0,r0)', 1 (r0,r1), 2 (r1,r1)', 3 (r0,o_t), 4 (r1,o_{1-t});
-            // P blocks: 0 (r0,r1), 1 (r0,o_t), 2 (r1,o_{1-t})
-            auto hblk = [&](int v, int e) -> uint8_t* { return hb + 2048 * (5 * v + e); };
-            auto pblk = [&](int v, int e) -> uint8_t* { return hb + 2048 * (10 + 3 * v + e); };
-            int bp_off[4];
+            // During the steps the Z copy and the blocks use a layout in which
+            // an operand slot is one aligned 16-byte pair: within each 64-byte
+            // segment, logical chunk c (columns 4c..4c+3) of row r sits at
+            // pair ((c >> 2) * 2 + (c & 1)) ^ t(r), half (c >> 1) & 1, with
+            // t(r) = ((r >> 1) ^ (r >> 2) ^ (r >> 4)) & 3. Slot s of lane
+            // (li, lh) (chunks 4s + lh and 4s + 2 + lh) is then pair
+            // (2s + lh) ^ t(li), so row pieces move with ds_read_b128 and
+            // ds_write_b128; on gfx950 these, and the transposing reads of
+            // the layout, are bank-conflict-free at row strides 320 and 64
+            // bytes (measured with the LDS bank-conflict counter). The tile's
+            // staging before and after the steps keeps the copy's own layout.
+            auto tsw = [](int r) { return ((r >> 1) ^ (r >> 2) ^ (r >> 4)) & 3; };
+            auto phys = [&](int c, int r) { return 2 * ((((c >> 2) << 1) | (c & 1)) ^ tsw(r)) + ((c >> 1) & 1); };
+            int rpB[S], bpB[S];
 #pragma unroll
-            for (int g = 0; g < 4; ++g) bp_off[g] = li * 64 + 8 * ((2 * g + lh) ^ rm_swz(li));
-            int btr_off[S][2];
+            for (int s = 0; s < S; ++s) {
+                rpB[s] = li * RS + 16 * ((2 * s + lh) ^ tsw(li));
+                bpB[s] = li * 64 + 16 * ((2 * s + lh) ^ tsw(li));
+            }
+            int trB[S][2], btrB[S][2];
 #pragma unroll
             for (int s = 0; s < S; ++s)
 #pragma unroll
                 for (int x = 0; x < 2; ++x) {
                     const int row = 16 * s + 8 * x + 4 * (grp16 >> 1) + ((lane & 15) >> 2);
                     const int chunk = 4 * (grp16 & 1) + (lane & 3);
-                    btr_off[s][x] = row * 64 + 8 * (chunk ^ rm_swz(row));
+                    trB[s][x] = row * RS + 8 * phys(chunk, row);
+                    btrB[s][x] = row * 64 + 8 * phys(chunk, row);
                 }
-            // slot s of a stored block: its rows (lane = row), or the rows of its transpose
-            auto blk_rows = [&](const uint8_t* b, int s) -> u32x4 {
-                const u32x2 lo = *reinterpret_cast<const u32x2*>(b + bp_off[2 * s]);
-                const u32x2 hi = *reinterpret_cast<const u32x2*>(b + bp_off[2 * s + 1]);
-                return u32x4{lo[0], lo[1], hi[0], hi[1]};
-            };
+            uint8_t* const hb = reinterpret_cast<uint8_t*>(slots);
+            // H blocks of wave v: 0 (r0,r0)', 1 (r0,r1), 2 (r1,r1)', 3 (r0,o_t),
+            // 4 (r1,o_{1-t}), 5 (r1,r0); P blocks: 0 (r0,r1), 1 (r0,o_t), 2 (r1,o_{1-t})
+            auto hblk = [&](int v, int e) -> uint8_t* { return hb + 2048 * (6 * v + e); };
+            auto pblk = [&](int v, int e) -> uint8_t* { return hb + 2048 * (12 + 3 * v + e); };
+            // slot s of a stored 32x32 block: its rows (lane = row), or the rows of its transpose
+            auto blk_rows = [&](const uint8_t* b, int s) -> u32x4 { return *reinterpret_cast<const u32x4*>(b + bpB[s]); };
             auto blk_tr = [&](const uint8_t* b, int s) -> u32x4 {
-                const u32x2 lo = tr_read(b + btr_off[s][0]);
-                const u32x2 hi = tr_read(b + btr_off[s][1]);
+                const u32x2 lo = tr_read(b + btrB[s][0]);
+                const u32x2 hi = tr_read(b + btrB[s][1]);
                 return u32x4{lo[0], lo[1], hi[0], hi[1]};
             };
-            // write quarter g (columns 8g + 4lh .. +3 of each row) of a block given as two slots
-            auto blk_put = [&](uint8_t* b, const u32x4 (&v)[S], int g) {
-                *reinterpret_cast<u32x2*>(b + bp_off[g]) = u32x2{v[g >> 1][(g & 1) * 2], v[g >> 1][(g & 1) * 2 + 1]};
+            auto blk_put = [&](uint8_t* b, const u32x4 (&v)[S]) {
+#pragma unroll
+                for (int s = 0; s < S; ++s) *reinterpret_cast<u32x4*>(b + bpB[s]) = v[s];
             };
-            // column pieces of Z's row block `br`, k half s, output block n
+            // column pieces of Z's row block `br`, k half s, output block n; row pieces
             auto zcol = [&](int br, int s, int n) -> u32x4 {
                 const uint8_t* const kb = rm + 32 * br * RS + 64 * n;
-                const u32x2 lo = tr_read(kb + tr_off[s][0]);
-                const u32x2 hi = tr_read(kb + tr_off[s][1]);
+                const u32x2 lo = tr_read(kb + trB[s][0]);
+                const u32x2 hi = tr_read(kb + trB[s][1]);
                 return u32x4{lo[0], lo[1], hi[0], hi[1]};
             };
-            auto zrow = [&](int br, int q, int s) -> u32x4 { return rowpiece(rm + 32 * br * RS, q, s); };
+            auto zrow = [&](int br, int q, int s) -> u32x4 {
+                return *reinterpret_cast<const u32x4*>(rm + 32 * br * RS + 64 * q + rpB[s]);
+            };
             auto shifted = [&](const f32x16& gd) -> f32x16 {
                 f32x16 r = gd;
 #pragma unroll
@@ -535,94 +552,99 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     for (int s = 0; s < S; ++s) Zop[1][q][s] = make_slot<OP>(Z[1][q], s);
                 // the other wave's reads of the previous Z copy are done
                 __syncthreads();
-                // own Z rows into the copy (32 stores), spread over the 12
-                // remaining own-block products
+                // own Z rows into the copy (16 stores), spread over 8 own-block products
 #pragma unroll
-                for (int c = 0; c < 12; ++c) {
+                for (int c = 0; c < 8; ++c) {
 #pragma unroll
-                    for (int i = c * 32 / 12; i < (c + 1) * 32 / 12; ++i) {
-                        const int rb = i / 16, N = (i / 4) % 4, gq = i % 4;
-                        *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[gq] + 64 * N) =
-                            u32x2{Zop[rb][N][gq >> 1][(gq & 1) * 2], Zop[rb][N][gq >> 1][(gq & 1) * 2 + 1]};
+                    for (int i = 2 * c; i < 2 * c + 2; ++i) {
+                        const int rb = i / 8, N = (i / 2) % 4, sz = i % 2;
+                        *reinterpret_cast<u32x4*>(rm + 32 * (p0 + rb) * RS + 64 * N + rpB[sz]) = Zop[rb][N][sz];
                     }
-                    if (c < 4) {
-                        const int q = 2 + c / 2, s = c % 2;
-                        g[1] = mma1<OP>(Zop[1][q][s], Zop[0][q][s], g[1]);
-                    } else {
-                        const int q = (c - 4) / 2, s = c % 2;
-                        g[2] = mma1<OP>(Zop[1][q][s], Zop[1][q][s], g[2]);
-                    }
+                    const int q = c < 4 ? 2 + c / 2 : (c - 4) / 2, s = c % 2;
+                    if (c < 4) g[1] = mma1<OP>(Zop[1][q][s], Zop[0][q][s], g[1]);
+                    else g[2] = mma1<OP>(Zop[1][q][s], Zop[1][q][s], g[2]);
                     __builtin_amdgcn_sched_barrier(0);
                 }
                 __syncthreads();
 
                 // ---- Gram cross blocks (r0, o_t), (r1, o_{1-t}) from the other
-                // wave's Z rows; the own blocks' conversions and stores ride along
-                u32x4 hs[5][S], qs[2][S];
-                {
-                    u32x4 nxt[2] = {zrow(ot, 0, 0), zrow(on, 0, 0)};
+                // wave's Z rows, read PD iterations ahead (the last own products
+                // cover the first reads); the own blocks' conversions and
+                // stores ride along
+                constexpr int PD = 3;
+                u32x4 rq[PD][2];
 #pragma unroll
-                    for (int it = 0; it < IT; ++it) {
-                        const int q = it / S, s = it % S;
-                        const u32x4 c0 = nxt[0], c1 = nxt[1];
-                        if (it + 1 < IT) {
-                            nxt[0] = zrow(ot, (it + 1) / S, (it + 1) % S);
-                            nxt[1] = zrow(on, (it + 1) / S, (it + 1) % S);
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
-                        g[3] = mma1<OP>(c0, Zop[0][q][s], g[3]);
-                        g[4] = mma1<OP>(c1, Zop[1][q][s], g[4]);
-                        if constexpr (CMODE != 2) {
-                            if (it == 0) {
+                for (int d = 0; d < PD; ++d) {
+                    rq[d][0] = zrow(ot, d / S, d % S);
+                    rq[d][1] = zrow(on, d / S, d % S);
+                }
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                                for (int x = 0; x < S; ++x) hs[0][x] = make_slot<OP>(g[0], x);
-                            } else if (it == 1) {
-                                const f32x16 gd = shifted(g[0]);
+                for (int q = 2; q < NB; ++q)
 #pragma unroll
-                                for (int x = 0; x < S; ++x) qs[0][x] = make_slot<OP>(gd, x);
-                            } else if (it == 2) {
+                    for (int s = 0; s < S; ++s) g[2] = mma1<OP>(Zop[1][q][s], Zop[1][q][s], g[2]);
+                __builtin_amdgcn_sched_barrier(0);
+                u32x4 hs[5][S], qs[2][S], la1[S];  // la1: H[r1, r0]
 #pragma unroll
-                                for (int x = 0; x < S; ++x) hs[1][x] = make_slot<OP>(g[1], x);
-                            } else if (it == 3) {
-#pragma unroll
-                                for (int x = 0; x < S; ++x) hs[2][x] = make_slot<OP>(g[2], x);
-                            } else if (it == 4) {
-                                const f32x16 gd = shifted(g[2]);
-#pragma unroll
-                                for (int x = 0; x < S; ++x) qs[1][x] = make_slot<OP>(gd, x);
-                            } else if (it == 5) {
-#pragma unroll
-                                for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 0), qs[0], gq);
-                            } else if (it == 6) {
-#pragma unroll
-                                for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 1), hs[1], gq);
-                            } else {
-#pragma unroll
-                                for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 2), qs[1], gq);
-                            }
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
+                for (int it = 0; it < IT; ++it) {
+                    const int q = it / S, s = it % S;
+                    const u32x4 c0 = rq[it % PD][0], c1 = rq[it % PD][1];
+                    if (it + PD < IT) {
+                        rq[it % PD][0] = zrow(ot, (it + PD) / S, (it + PD) % S);
+                        rq[it % PD][1] = zrow(on, (it + PD) / S, (it + PD) % S);
                     }
+                    __builtin_amdgcn_sched_barrier(0);
+                    g[3] = mma1<OP>(c0, Zop[0][q][s], g[3]);
+                    g[4] = mma1<OP>(c1, Zop[1][q][s], g[4]);
+                    if constexpr (CMODE != 2) {
+                        if (it == 0) {
+#pragma unroll
+                            for (int x = 0; x < S; ++x) hs[0][x] = make_slot<OP>(g[0], x);
+                        } else if (it == 1) {
+                            const f32x16 gd = shifted(g[0]);
+#pragma unroll
+                            for (int x = 0; x < S; ++x) qs[0][x] = make_slot<OP>(gd, x);
+                        } else if (it == 2) {
+#pragma unroll
+                            for (int x = 0; x < S; ++x) hs[1][x] = make_slot<OP>(g[1], x);
+                            blk_put(hblk(w, 0), qs[0]);
+                        } else if (it == 3) {
+                            blk_put(hblk(w, 1), hs[1]);
+#pragma unroll
+                            for (int x = 0; x < S; ++x) hs[2][x] = make_slot<OP>(g[2], x);
+                        } else if (it == 4) {
+                            const f32x16 gd = shifted(g[2]);
+#pragma unroll
+                            for (int x = 0; x < S; ++x) qs[1][x] = make_slot<OP>(gd, x);
+                        } else if (it == 5) {
+                            blk_put(hblk(w, 2), qs[1]);
+#pragma unroll
+                            for (int x = 0; x < S; ++x) la1[x] = blk_tr(hblk(w, 1), x);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
 
                 u32x4 pop[5][S];
+                f32x16 pa[5];
+                auto pconv = [&](int e) {
+#pragma unroll
+                    for (int x = 0; x < S; ++x) {
+                        if constexpr (CMODE == 0) pop[e][x] = make_slot<OP>(pa[e], x);
+                        else pop[e][x] = make_slot<OP>(-pa[e], x);
+                    }
+                };
                 if constexpr (CMODE != 2) {
-#pragma unroll
-                    for (int x = 0; x < S; ++x) hs[3][x] = make_slot<OP>(g[3], x);
-#pragma unroll
-                    for (int x = 0; x < S; ++x) hs[4][x] = make_slot<OP>(g[4], x);
                     // ---- P (as acc = H (H + sigma b' I) + sigma a I): block (i, j)
-                    // accumulates H'[j, k] x H[i, k] over the k-blocks
-                    f32x16 pa[5];
+                    // accumulates H'[j, k] x H[i, k] over the k-blocks. Terms on
+                    // this wave's blocks first; the cross blocks' conversions and
+                    // stores ride along.
                     pa[0] = diag_a;
                     pa[1] = f32x16{};
                     pa[2] = diag_a;
                     pa[3] = f32x16{};
                     pa[4] = f32x16{};
-                    u32x4 la1[S];  // H[r1, r0]
-#pragma unroll
-                    for (int s = 0; s < S; ++s) la1[s] = blk_tr(hblk(w, 1), s);
-                    __builtin_amdgcn_sched_barrier(0);
+                    u32x4 lb1[S], lb6[S];  // H[o_t, r0], H[o_{1-t}, r1]
 #pragma unroll
                     for (int s = 0; s < S; ++s) {
                         pa[0] = mma1<OP>(qs[0][s], hs[0][s], pa[0]);  // k = r0
@@ -631,47 +653,53 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                         pa[0] = mma1<OP>(hs[1][s], hs[1][s], pa[0]);  // k = r1
                         pa[1] = mma1<OP>(la1[s], hs[0][s], pa[1]);    // k = r0
                         pa[2] = mma1<OP>(la1[s], la1[s], pa[2]);      // k = r0
+                        if (s == 0) {
+                            blk_put(hblk(w, 5), la1);
+#pragma unroll
+                            for (int x = 0; x < S; ++x) hs[3][x] = make_slot<OP>(g[3], x);
+                            blk_put(hblk(w, 3), hs[3]);
+                        } else {
+#pragma unroll
+                            for (int x = 0; x < S; ++x) hs[4][x] = make_slot<OP>(g[4], x);
+                            blk_put(hblk(w, 4), hs[4]);
+#pragma unroll
+                            for (int x = 0; x < S; ++x) {
+                                lb1[x] = blk_tr(hblk(w, 3), x);
+                                lb6[x] = blk_tr(hblk(w, 4), x);
+                            }
+                        }
                         __builtin_amdgcn_sched_barrier(0);
                     }
-#pragma unroll
-                    for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 3), hs[3], gq);
-#pragma unroll
-                    for (int gq = 0; gq < 4; ++gq) blk_put(hblk(w, 4), hs[4], gq);
-                    u32x4 lb1[S], lb6[S];  // H[o_t, r0], H[o_{1-t}, r1]
-#pragma unroll
-                    for (int s = 0; s < S; ++s) {
-                        lb1[s] = blk_tr(hblk(w, 3), s);
-                        lb6[s] = blk_tr(hblk(w, 4), s);
-                    }
-                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int s = 0; s < S; ++s) {
                         pa[0] = mma1<OP>(hs[3][s], hs[3][s], pa[0]);  // k = o_t
                         pa[2] = mma1<OP>(hs[4][s], hs[4][s], pa[2]);  // k = o_{1-t}
-                        pa[3] = mma1<OP>(lb1[s], hs[0][s], pa[3]);    // (r0, o_t), k = r0
-                        pa[4] = mma1<OP>(lb6[s], hs[2][s], pa[4]);    // (r1, o_{1-t}), k = r1
-                        __builtin_amdgcn_sched_barrier(0);
                     }
+                    __builtin_amdgcn_sched_barrier(0);
                     __syncthreads();
-                    // the other wave's blocks
+                    // the other wave's blocks; two own terms cover their reads
                     u32x4 la2[S], la3[S], lb2[S], lb3[S], lb4[S], lb5[S], lb7[S], lb8[S];
 #pragma unroll
                     for (int s = 0; s < S; ++s) {
                         la2[s] = blk_tr(hblk(wo, 4 - w), s);     // H[r0, o_{1-t}]
                         la3[s] = blk_tr(hblk(wo, 3 + w), s);     // H[r1, o_t]
                     }
-                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int s = 0; s < S; ++s) {
                         lb2[s] = blk_rows(hblk(wo, 3 + w), s);      // H[o_t, r1]
                         lb3[s] = blk_rows(hblk(wo, 2 * w), s);      // H'[o_t, o_t]
-                        const u32x4 nrm = blk_rows(hblk(wo, 1), s); // H[o_0, o_1]
-                        const u32x4 trn = blk_tr(hblk(wo, 1), s);   // H[o_1, o_0]
-                        lb4[s] = w ? trn : nrm;                     // H[o_t, o_{1-t}]
-                        lb7[s] = w ? nrm : trn;                     // H[o_{1-t}, o_t]
+                        lb4[s] = blk_rows(hblk(wo, w ? 5 : 1), s);  // H[o_t, o_{1-t}]
+                        lb7[s] = blk_rows(hblk(wo, w ? 1 : 5), s);  // H[o_{1-t}, o_t]
                         lb5[s] = blk_rows(hblk(wo, 4 - w), s);      // H[o_{1-t}, r0]
                         lb8[s] = blk_rows(hblk(wo, 2 - 2 * w), s);  // H'[o_{1-t}, o_{1-t}]
                     }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int s = 0; s < S; ++s) {
+                        pa[3] = mma1<OP>(lb1[s], hs[0][s], pa[3]);    // (r0, o_t), k = r0
+                        pa[4] = mma1<OP>(lb6[s], hs[2][s], pa[4]);    // (r1, o_{1-t}), k = r1
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int s = 0; s < S; ++s) {
                         pa[0] = mma1<OP>(la2[s], la2[s], pa[0]);    // k = o_{1-t}
@@ -680,13 +708,6 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                         pa[1] = mma1<OP>(hs[4][s], la2[s], pa[1]);  // k = o_{1-t}
                         __builtin_amdgcn_sched_barrier(0);
                     }
-                    auto pconv = [&](int e) {
-#pragma unroll
-                        for (int x = 0; x < S; ++x) {
-                            if constexpr (CMODE == 0) pop[e][x] = make_slot<OP>(pa[e], x);
-                            else pop[e][x] = make_slot<OP>(-pa[e], x);
-                        }
-                    };
 #pragma unroll
                     for (int s = 0; s < S; ++s) {
                         pa[3] = mma1<OP>(lb2[s], hs[1][s], pa[3]);  // (r0, o_t), k = r1
@@ -700,95 +721,81 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                             pconv(1);
                         } else {
                             pconv(2);
-#pragma unroll
-                            for (int gq = 0; gq < 4; ++gq) blk_put(pblk(w, 0), pop[1], gq);
+                            blk_put(pblk(w, 0), pop[1]);
                         }
                         __builtin_amdgcn_sched_barrier(0);
                     }
-                    pconv(3);
-                    pconv(4);
                 } else {
                     // c = 0: aI + P = a I + b H, straight from the Gram blocks
 #pragma unroll
-                    for (int e = 0; e < 5; ++e) {
-                        const f32x16 pe = (e == 0 || e == 2) ? g[e] * args.bq + diag_a : g[e] * args.bq;
+                    for (int e = 0; e < 5; ++e) pa[e] = (e == 0 || e == 2) ? g[e] * args.bq + diag_a : g[e] * args.bq;
 #pragma unroll
-                        for (int x = 0; x < S; ++x) pop[e][x] = make_slot<OP>(pe, x);
-                    }
+                    for (int e = 0; e < 3; ++e)
 #pragma unroll
-                    for (int gq = 0; gq < 4; ++gq) blk_put(pblk(w, 0), pop[1], gq);
+                        for (int x = 0; x < S; ++x) pop[e][x] = make_slot<OP>(pa[e], x);
+                    blk_put(pblk(w, 0), pop[1]);
                 }
-#pragma unroll
-                for (int gq = 0; gq < 4; ++gq) blk_put(pblk(w, 1), pop[3], gq);
-#pragma unroll
-                for (int gq = 0; gq < 4; ++gq) blk_put(pblk(w, 2), pop[4], gq);
 
-                // ---- Z <- (a I + P) Z. k-blocks r0 and r1 need only this
+                // ---- Z <- (a I + P) Z over the k-blocks r0, r1, o_t, o_{1-t}
+                // (two k halves each). The first three iterations need only this
                 // wave's blocks ((aI + P)[r1, r0] is the transpose of its own
-                // (r0, r1) block); o_t and o_{1-t} follow the barrier.
+                // (r0, r1) block) and finish the cross blocks' conversions and
+                // stores; the fourth, after the barrier, covers the reads of the
+                // other wave's blocks.
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
                     for (int n = 0; n < NB; ++n) Z[rb][n] = f32x16{};
-                u32x4 lp1[S];  // (aI + P)[r1, r0]
+                u32x4 lp[3][S];  // (aI + P)[r1, r0], [r0, o_{1-t}], [r1, o_t]
 #pragma unroll
-                for (int s = 0; s < S; ++s) lp1[s] = blk_tr(pblk(w, 0), s);
-                {
-                    u32x4 nxt[NB];
+                for (int s = 0; s < S; ++s) lp[0][s] = blk_tr(pblk(w, 0), s);
+                auto kblk = [&](int it) -> int { return it < 2 ? p0 : (it < 4 ? p0 + 1 : (it < 6 ? ot : on)); };
+                u32x4 nxt[NB];
 #pragma unroll
-                    for (int n = 0; n < NB; ++n) nxt[n] = zcol(p0, 0, n);
+                for (int n = 0; n < NB; ++n) nxt[n] = zcol(p0, 0, n);
 #pragma unroll
-                    for (int it = 0; it < 2 * S; ++it) {
-                        const int kb = it / S, s = it % S;  // k-block r0 + kb
-                        u32x4 cur[NB];
+                for (int it = 0; it < 4 * S; ++it) {
+                    const int s = it % S;
+                    if (it == 3) {
+                        __syncthreads();
 #pragma unroll
-                        for (int n = 0; n < NB; ++n) cur[n] = nxt[n];
-                        if (it + 1 < 2 * S) {
-#pragma unroll
-                            for (int n = 0; n < NB; ++n) nxt[n] = zcol(p0 + (it + 1) / S, (it + 1) % S, n);
+                        for (int x = 0; x < S; ++x) {
+                            lp[1][x] = blk_tr(pblk(wo, 2 - w), x);
+                            lp[2][x] = blk_tr(pblk(wo, 1 + w), x);
                         }
-                        __builtin_amdgcn_sched_barrier(0);
-                        const u32x4 a0 = kb == 0 ? pop[0][s] : pop[1][s];
-                        const u32x4 a1 = kb == 0 ? lp1[s] : pop[2][s];
-#pragma unroll
-                        for (int n = 0; n < NB; ++n) {
-                            Z[0][n] = mma1<OP>(cur[n], a0, Z[0][n]);
-                            Z[1][n] = mma1<OP>(cur[n], a1, Z[1][n]);
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
                     }
-                }
-                __syncthreads();
-                {
-                    u32x4 lp2[S], lp3[S];  // (aI + P)[r0, o_{1-t}], (aI + P)[r1, o_t]
+                    u32x4 cur[NB];
 #pragma unroll
-                    for (int s = 0; s < S; ++s) {
-                        lp2[s] = blk_tr(pblk(wo, 2 - w), s);
-                        lp3[s] = blk_tr(pblk(wo, 1 + w), s);
+                    for (int n = 0; n < NB; ++n) cur[n] = nxt[n];
+                    if (it + 1 < 4 * S) {
+#pragma unroll
+                        for (int n = 0; n < NB; ++n) nxt[n] = zcol(kblk(it + 1), (it + 1) % S, n);
                     }
-                    u32x4 nxt[NB];
+                    __builtin_amdgcn_sched_barrier(0);
+                    const u32x4 a0 = it < 2 ? pop[0][s] : (it < 4 ? pop[1][s] : (it < 6 ? pop[3][s] : lp[1][s]));
+                    const u32x4 a1 = it < 2 ? lp[0][s] : (it < 4 ? pop[2][s] : (it < 6 ? lp[2][s] : pop[4][s]));
 #pragma unroll
-                    for (int n = 0; n < NB; ++n) nxt[n] = zcol(ot, 0, n);
-#pragma unroll
-                    for (int it = 0; it < 2 * S; ++it) {
-                        const int kb = it / S, s = it % S;  // k-block o_t, then o_{1-t}
-                        u32x4 cur[NB];
-#pragma unroll
-                        for (int n = 0; n < NB; ++n) cur[n] = nxt[n];
-                        if (it + 1 < 2 * S) {
-#pragma unroll
-                            for (int n = 0; n < NB; ++n) nxt[n] = zcol((it + 1) / S == 0 ? ot : on, (it + 1) % S, n);
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
-                        const u32x4 a0 = kb == 0 ? pop[3][s] : lp2[s];
-                        const u32x4 a1 = kb == 0 ? lp3[s] : pop[4][s];
-#pragma unroll
-                        for (int n = 0; n < NB; ++n) {
-                            Z[0][n] = mma1<OP>(cur[n], a0, Z[0][n]);
-                            Z[1][n] = mma1<OP>(cur[n], a1, Z[1][n]);
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
+                    for (int n = 0; n < NB; ++n) {
+                        Z[0][n] = mma1<OP>(cur[n], a0, Z[0][n]);
+                        Z[1][n] = mma1<OP>(cur[n], a1, Z[1][n]);
                     }
+                    if (it == 0) {
+                        if constexpr (CMODE != 2) pconv(3);
+                        else {
+#pragma unroll
+                            for (int x = 0; x < S; ++x) pop[3][x] = make_slot<OP>(pa[3], x);
+                        }
+                    } else if (it == 1) {
+                        if constexpr (CMODE != 2) pconv(4);
+                        else {
+#pragma unroll
+                            for (int x = 0; x < S; ++x) pop[4][x] = make_slot<OP>(pa[4], x);
+                        }
+                        blk_put(pblk(w, 1), pop[3]);
+                    } else if (it == 2) {
+                        blk_put(pblk(w, 2), pop[4]);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
             // the other wave's last reads of this wave's rows come before the

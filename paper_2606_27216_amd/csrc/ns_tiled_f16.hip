@@ -525,46 +525,29 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 
             for (int k = 0; k < args.K; ++k) {
                 // ---- Gram. The operands of the current Z are made here, each
-                // right before its first product.
+                // right before its first product, and stored as this wave's rows
+                // of the Z copy (no wave reads the copy after the previous
+                // step's last barrier, see below).
                 u32x4 Zop[RB][NB][S];
                 f32x16 g[5];
 #pragma unroll
                 for (int e = 0; e < 5; ++e) g[e] = f32x16{};
 #pragma unroll
-                for (int q = 0; q < NB; ++q)
+                for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-                    for (int s = 0; s < S; ++s) {
-                        Zop[0][q][s] = make_slot<OP>(Z[0][q], s);
-                        g[0] = mma1<OP>(Zop[0][q][s], Zop[0][q][s], g[0]);
-                        __builtin_amdgcn_sched_barrier(0);
-                    }
+                    for (int q = 0; q < NB; ++q)
+#pragma unroll
+                        for (int s = 0; s < S; ++s) {
+                            Zop[rb][q][s] = make_slot<OP>(Z[rb][q], s);
+                            if (rb == 0) g[0] = mma1<OP>(Zop[0][q][s], Zop[0][q][s], g[0]);
+                            else g[1] = mma1<OP>(Zop[1][q][s], Zop[0][q][s], g[1]);
+                            *reinterpret_cast<u32x4*>(rm + 32 * (p0 + rb) * RS + 64 * q + rpB[s]) = Zop[rb][q][s];
+                            __builtin_amdgcn_sched_barrier(0);
+                        }
 #pragma unroll
                 for (int q = 0; q < 2; ++q)
 #pragma unroll
-                    for (int s = 0; s < S; ++s) {
-                        Zop[1][q][s] = make_slot<OP>(Z[1][q], s);
-                        g[1] = mma1<OP>(Zop[1][q][s], Zop[0][q][s], g[1]);
-                        __builtin_amdgcn_sched_barrier(0);
-                    }
-#pragma unroll
-                for (int q = 2; q < NB; ++q)
-#pragma unroll
-                    for (int s = 0; s < S; ++s) Zop[1][q][s] = make_slot<OP>(Z[1][q], s);
-                // the other wave's reads of the previous Z copy are done
-                __syncthreads();
-                // own Z rows into the copy (16 stores), spread over 8 own-block products
-#pragma unroll
-                for (int c = 0; c < 8; ++c) {
-#pragma unroll
-                    for (int i = 2 * c; i < 2 * c + 2; ++i) {
-                        const int rb = i / 8, N = (i / 2) % 4, sz = i % 2;
-                        *reinterpret_cast<u32x4*>(rm + 32 * (p0 + rb) * RS + 64 * N + rpB[sz]) = Zop[rb][N][sz];
-                    }
-                    const int q = c < 4 ? 2 + c / 2 : (c - 4) / 2, s = c % 2;
-                    if (c < 4) g[1] = mma1<OP>(Zop[1][q][s], Zop[0][q][s], g[1]);
-                    else g[2] = mma1<OP>(Zop[1][q][s], Zop[1][q][s], g[2]);
-                    __builtin_amdgcn_sched_barrier(0);
-                }
+                    for (int s = 0; s < S; ++s) g[2] = mma1<OP>(Zop[1][q][s], Zop[1][q][s], g[2]);
                 __syncthreads();
 
                 // ---- Gram cross blocks (r0, o_t), (r1, o_{1-t}) from the other
@@ -737,11 +720,13 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                 }
 
                 // ---- Z <- (a I + P) Z over the k-blocks r0, r1, o_t, o_{1-t}
-                // (two k halves each). The first three iterations need only this
-                // wave's blocks ((aI + P)[r1, r0] is the transpose of its own
-                // (r0, r1) block) and finish the cross blocks' conversions and
-                // stores; the fourth, after the barrier, covers the reads of the
-                // other wave's blocks.
+                // (two k halves each). Before the barrier: every product on this
+                // wave's blocks of aI + P ((aI + P)[r1, r0] is the transpose of its
+                // own (r0, r1) block) but one k half, with the cross blocks'
+                // conversions and stores riding along; the column pieces of the
+                // other wave's rows stay in registers for the two products on
+                // the other wave's blocks after it. So no wave reads the Z copy
+                // after the barrier, and the next step stores its rows at once.
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -749,14 +734,18 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                 u32x4 lp[3][S];  // (aI + P)[r1, r0], [r0, o_{1-t}], [r1, o_t]
 #pragma unroll
                 for (int s = 0; s < S; ++s) lp[0][s] = blk_tr(pblk(w, 0), s);
-                auto kblk = [&](int it) -> int { return it < 2 ? p0 : (it < 4 ? p0 + 1 : (it < 6 ? ot : on)); };
+                // (k-block, half) read order; pieces of o_t and o_{1-t} are kept
+                constexpr int NPZ = 8;
+                auto pz_blk = [&](int it) -> int { return it < 2 ? p0 : (it == 2 ? p0 + 1 : (it < 5 ? ot : (it < 7 ? on : p0 + 1))); };
+                auto pz_half = [&](int it) -> int { return it < 2 ? it : (it == 2 ? 0 : (it < 5 ? it - 3 : (it < 7 ? it - 5 : 1))); };
+                u32x4 kept[2][S][NB];  // column pieces of o_t, o_{1-t}
                 u32x4 nxt[NB];
 #pragma unroll
-                for (int n = 0; n < NB; ++n) nxt[n] = zcol(p0, 0, n);
+                for (int n = 0; n < NB; ++n) nxt[n] = zcol(pz_blk(0), pz_half(0), n);
 #pragma unroll
-                for (int it = 0; it < 4 * S; ++it) {
-                    const int s = it % S;
-                    if (it == 3) {
+                for (int it = 0; it < NPZ; ++it) {
+                    const int s = pz_half(it);
+                    if (it == 7) {
                         __syncthreads();
 #pragma unroll
                         for (int x = 0; x < S; ++x) {
@@ -767,17 +756,31 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     u32x4 cur[NB];
 #pragma unroll
                     for (int n = 0; n < NB; ++n) cur[n] = nxt[n];
-                    if (it + 1 < 4 * S) {
+                    if (it + 1 < NPZ) {
 #pragma unroll
-                        for (int n = 0; n < NB; ++n) nxt[n] = zcol(kblk(it + 1), (it + 1) % S, n);
+                        for (int n = 0; n < NB; ++n) nxt[n] = zcol(pz_blk(it + 1), pz_half(it + 1), n);
                     }
                     __builtin_amdgcn_sched_barrier(0);
-                    const u32x4 a0 = it < 2 ? pop[0][s] : (it < 4 ? pop[1][s] : (it < 6 ? pop[3][s] : lp[1][s]));
-                    const u32x4 a1 = it < 2 ? lp[0][s] : (it < 4 ? pop[2][s] : (it < 6 ? lp[2][s] : pop[4][s]));
+                    if (it < 3 || it == 7) {  // own k-blocks, both rows
+                        const u32x4 a0 = it < 2 ? pop[0][s] : pop[1][s];
+                        const u32x4 a1 = it < 2 ? lp[0][s] : pop[2][s];
 #pragma unroll
-                    for (int n = 0; n < NB; ++n) {
-                        Z[0][n] = mma1<OP>(cur[n], a0, Z[0][n]);
-                        Z[1][n] = mma1<OP>(cur[n], a1, Z[1][n]);
+                        for (int n = 0; n < NB; ++n) {
+                            Z[0][n] = mma1<OP>(cur[n], a0, Z[0][n]);
+                            Z[1][n] = mma1<OP>(cur[n], a1, Z[1][n]);
+                        }
+                    } else if (it < 5) {  // o_t: row r0 on this wave's (r0, o_t) block
+#pragma unroll
+                        for (int n = 0; n < NB; ++n) {
+                            kept[0][s][n] = cur[n];
+                            Z[0][n] = mma1<OP>(cur[n], pop[3][s], Z[0][n]);
+                        }
+                    } else {  // o_{1-t}: row r1 on this wave's (r1, o_{1-t}) block
+#pragma unroll
+                        for (int n = 0; n < NB; ++n) {
+                            kept[1][s][n] = cur[n];
+                            Z[1][n] = mma1<OP>(cur[n], pop[4][s], Z[1][n]);
+                        }
                     }
                     if (it == 0) {
                         if constexpr (CMODE != 2) pconv(3);
@@ -794,6 +797,16 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                         blk_put(pblk(w, 1), pop[3]);
                     } else if (it == 2) {
                         blk_put(pblk(w, 2), pop[4]);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                // the other wave's blocks: (aI + P)[r1, o_t] and [r0, o_{1-t}]
+#pragma unroll
+                for (int s = 0; s < S; ++s) {
+#pragma unroll
+                    for (int n = 0; n < NB; ++n) {
+                        Z[1][n] = mma1<OP>(kept[0][s][n], lp[2][s], Z[1][n]);
+                        Z[0][n] = mma1<OP>(kept[1][s][n], lp[1][s], Z[0][n]);
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }

@@ -66,12 +66,21 @@ HM_DEV uint32_t wave_max_u32(uint32_t v)
 }
 
 // Matrix owning `tile`, searching from `hint` (the tiles one wave visits only
-// grow, so the owner of an earlier tile is a lower bound).
+// grow, so the owner of an earlier tile is a lower bound). The first tiles of
+// the next four matrices are loaded together (independent scalar loads), which
+// settles the usual case in one round trip; a binary search covers the rest.
 HM_DEV int find_matrix_from(const KernelArgs& args, int64_t tile, int hint)
 {
     const ConstDesc* const descs = desc_table(args);
-    if (hint + 1 >= args.n_mats || descs[hint + 1].tile_begin > tile) return hint;
-    int lo = hint + 1, hi = args.n_mats - 1;
+    constexpr int kAhead = 4;
+    int passed = 0;
+#pragma unroll
+    for (int j = 1; j <= kAhead; ++j) {
+        const int idx = min(hint + j, args.n_mats - 1);
+        passed += (hint + j < args.n_mats && descs[idx].tile_begin <= tile) ? 1 : 0;
+    }
+    if (passed < kAhead) return hint + passed;
+    int lo = hint + kAhead, hi = args.n_mats - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
         if (descs[mid].tile_begin <= tile) lo = mid;
@@ -288,6 +297,21 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     auto io_swap = [&](const u32x4& v, int row) -> u32x4 {
         return (rm_swz(row) & 1) ? u32x4{v[2], v[3], v[0], v[1]} : v;
     };
+    // The symmetric 128-tile step keeps its Z copy in a layout of aligned
+    // 16-byte operand pairs (described at ns_steps_sym); its tiles are
+    // staged in that layout too: a 16-byte row chunk goes in as two 8-byte
+    // halves, and row pieces move as whole pairs.
+    constexpr bool PAIRS = F16Shape<T, RB>::kSym;
+    auto tsw = [](int r) { return ((r >> 1) ^ (r >> 2) ^ (r >> 4)) & 3; };
+    int rpB[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) rpB[s] = li * RS + 16 * ((2 * s + lh) ^ tsw(li));
+    // byte offset of half h (columns 8 io_cc + 4h .. +3) of staging chunk io_cc of
+    // `row` (the pair swizzle is a function of the row within its 32-row block)
+    auto io_half = [&](int row, int h) -> int {
+        const int jj = io_cc & 3;
+        return row * RS + 64 * (io_cc >> 2) + 16 * ((2 * (jj >> 1) + h) ^ tsw(row & 31)) + 8 * (jj & 1);
+    };
 
     // Whole row segments of the own rows to HBM (16-byte chunks read back from
     // the row-major copy into `outv`).
@@ -362,7 +386,12 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int row = 32 * p0 + RPI * i + io_row;
-            *reinterpret_cast<u32x4*>(rm + io_lds(row)) = io_swap(raw[i], row);
+            if constexpr (PAIRS) {
+                *reinterpret_cast<u32x2*>(rm + io_half(row, 0)) = u32x2{raw[i][0], raw[i][1]};
+                *reinterpret_cast<u32x2*>(rm + io_half(row, 1)) = u32x2{raw[i][2], raw[i][3]};
+            } else {
+                *reinterpret_cast<u32x4*>(rm + io_lds(row)) = io_swap(raw[i], row);
+            }
         }
         if (pending) store_rows(prv, outv);
         if constexpr (EARLY) {
@@ -375,9 +404,17 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             for (int q = 0; q < NB; ++q)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
-                    const u32x2 w = *reinterpret_cast<const u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q);
-                    W[rb][q][2 * g] = w[0];
-                    W[rb][q][2 * g + 1] = w[1];
+                    if constexpr (PAIRS) {
+                        if (g % 2 == 0) {
+                            const u32x4 w = *reinterpret_cast<const u32x4*>(rm + 32 * (p0 + rb) * RS + 64 * q + rpB[g / 2]);
+#pragma unroll
+                            for (int x = 0; x < 4; ++x) W[rb][q][2 * g + x] = w[x];
+                        }
+                    } else {
+                        const u32x2 w = *reinterpret_cast<const u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q);
+                        W[rb][q][2 * g] = w[0];
+                        W[rb][q][2 * g + 1] = w[1];
+                    }
                 }
 
         // Z_0 = |c|^(1/4) S / ||S||_F (Phi_K(0) = 0). The fp32 sum of squares
@@ -470,16 +507,12 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             // (2s + lh) ^ t(li), so row pieces move with ds_read_b128 and
             // ds_write_b128; on gfx950 these, and the transposing reads of
             // the layout, are bank-conflict-free at row strides 320 and 64
-            // bytes (measured with the LDS bank-conflict counter). The tile's
-            // staging before and after the steps keeps the copy's own layout.
-            auto tsw = [](int r) { return ((r >> 1) ^ (r >> 2) ^ (r >> 4)) & 3; };
+            // bytes (measured with the LDS bank-conflict counter). The tile is
+            // staged in the same layout (tsw, rpB and io_half above).
             auto phys = [&](int c, int r) { return 2 * ((((c >> 2) << 1) | (c & 1)) ^ tsw(r)) + ((c >> 1) & 1); };
-            int rpB[S], bpB[S];
+            int bpB[S];
 #pragma unroll
-            for (int s = 0; s < S; ++s) {
-                rpB[s] = li * RS + 16 * ((2 * s + lh) ^ tsw(li));
-                bpB[s] = li * 64 + 16 * ((2 * s + lh) ^ tsw(li));
-            }
+            for (int s = 0; s < S; ++s) bpB[s] = li * 64 + 16 * ((2 * s + lh) ^ tsw(li));
             int trB[S][2], btrB[S][2];
 #pragma unroll
             for (int s = 0; s < S; ++s)
@@ -1236,13 +1269,26 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
             for (int q = 0; q < NB; ++q)
 #pragma unroll
-                for (int g = 0; g < 4; ++g)
-                    *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q) =
-                        u32x2{OB[rb][q][2 * g], OB[rb][q][2 * g + 1]};
+                for (int g = 0; g < 4; ++g) {
+                    if constexpr (PAIRS) {
+                        if (g % 2 == 0)
+                            *reinterpret_cast<u32x4*>(rm + 32 * (p0 + rb) * RS + 64 * q + rpB[g / 2]) =
+                                u32x4{OB[rb][q][2 * g], OB[rb][q][2 * g + 1], OB[rb][q][2 * g + 2], OB[rb][q][2 * g + 3]};
+                    } else {
+                        *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q) =
+                            u32x2{OB[rb][q][2 * g], OB[rb][q][2 * g + 1]};
+                    }
+                }
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int row = 32 * p0 + RPI * i + io_row;
-            outv[i] = io_swap(*reinterpret_cast<const u32x4*>(rm + io_lds(row)), row);
+            if constexpr (PAIRS) {
+                const u32x2 lo = *reinterpret_cast<const u32x2*>(rm + io_half(row, 0));
+                const u32x2 hi = *reinterpret_cast<const u32x2*>(rm + io_half(row, 1));
+                outv[i] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+            } else {
+                outv[i] = io_swap(*reinterpret_cast<const u32x4*>(rm + io_lds(row)), row);
+            }
         }
         prv = cur;
         pending = true;

@@ -14,7 +14,10 @@ step). Rank 0 prints one JSON line on stdout; progress goes to stderr.
 The JSON also carries:
   roofline      the fused kernel's algorithmic flops per launch over its mean
                 launch duration (HIP events on the launch stream), against the
-                published dense fp16/bf16 MFMA peak (2.5 PFLOP/s); `traffic` is
+                published dense fp16/bf16 MFMA peak (2.5 PFLOP/s); the MFMA
+                work actually issued (less than 6T^3 per tile-step where a
+                kernel exploits the symmetry of H and aI + P) is reported
+                beside it as mfma_issued_*; `traffic` is
                 the HBM bytes per launch from rocprofv3 FETCH_SIZE/WRITE_SIZE
                 counters (profiles/ns_tiled_traffic.json) when they were taken
                 on the current kernel source, else null;
@@ -85,6 +88,16 @@ def traffic_for_launch(T, K, dtype, compute, tiles_per_launch):
     if not ent:
         return None
     return ent["fetch_bytes"] + ent["write_bytes"]
+
+
+def issued_fraction(T, op_name, c):
+    """MFMA work a launch issues, as a fraction of the 6T^3 per tile-step the
+    metric counts. The fp16 128-tile kernel evaluates only the ten upper
+    32x32 blocks of the symmetric H and aI + P (of 16 each) plus the full PZ
+    product; with c = 0 there is no P product (aI + P = aI + bH)."""
+    if op_name == "f16" and T == 128:
+        return (10 + (10 if c != 0 else 0) + 16) / 48.0
+    return 1.0 if c != 0 else 2.0 / 3.0
 
 
 def cpu_baseline(mats, T, K, coeffs, budget_s, seed=0):
@@ -206,6 +219,7 @@ def main():
     flops_launch = flops_step / launches
     achieved = flops_launch / (launch_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[op_name]
+    issued = issued_fraction(args.T, op_name, coeffs[2])
     tiles_launch = total // launches
     traffic = traffic_for_launch(args.T, args.K, args.dtype, op_name, tiles_launch)
 
@@ -232,7 +246,12 @@ def main():
             "bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4), "traffic": traffic,
             "flops_per_launch": flops_launch, "mean_launch_ms": round(launch_ms, 4),
+            "mfma_issued_fraction": round(issued, 4),
+            "mfma_issued_tflops": round(achieved * issued, 3),
+            "mfma_issued_frac": round(achieved * issued / peak, 4),
         },
+        "step_ms": {"median": round(float(np.median(step_ms)), 4),
+                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4)},
     }
     if args.cpu_seconds > 0:
         log(f"cpu baseline: oracle on sampled tiles for ~{args.cpu_seconds:.0f} s")

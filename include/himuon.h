@@ -69,9 +69,9 @@ typedef enum himuon_status {
                                     leave the fp16 range for these a, b, c, K      */
 } himuon_status_t;
 
-/* Device workspace bytes a call over n_mats matrices needs: the per-matrix
- * descriptor table the kernels read (64 bytes per matrix, rounded up to
- * 256). Host-only; returns 0 for n_mats < 1. */
+/* Device workspace bytes a himuon_ns_tiled call over n_mats matrices needs:
+ * the per-matrix descriptor table the kernels read (64 bytes per matrix,
+ * rounded up to 256). Host-only; returns 0 for n_mats < 1. */
 size_t himuon_ns_tiled_workspace_size(int64_t n_mats);
 
 /*
@@ -117,6 +117,53 @@ int himuon_ns_tiled(int64_t n_mats,
                     void* workspace, size_t workspace_bytes,
                     size_t chunk_budget_bytes,
                     void* stream);
+
+/*
+ * Phi_K through library GEMMs: the full-matrix branch and large tiles.
+ *
+ * T = 0: Phi_K of every whole matrix (the full-matrix branch, Sec. 4.4.3).
+ *        A matrix with more rows than columns is worked on transposed,
+ *        Phi_K(S) = Phi_K(S^T)^T, so the Gram matrix is min(H, W) square.
+ * T >= 1: Phi_{K,T}, eq. (tiled_ns), with each T x T tile a problem of its
+ *        own; meant for tiles too large to stay on one compute unit
+ *        (T = 512 is the multi-kernel tile of Sec. 4.4.1), but any T works.
+ * Problems of equal shape are batched; each step of eq. (ns_iteration) is
+ * three batched GEMMs (A = X X^T, B = bA + cA^2, X <- aX + BX) with fp32
+ * accumulation. Operands are fp32 for fp32 storage; for bf16 storage fp16
+ * (a rescaled iterate, himuon_select_compute's range argument applied to
+ * the largest Gram size of the call) unless `compute` asks for bf16. The
+ * norm of each problem is summed in fp64 in a fixed order, so a result does
+ * not depend on the batch or chunk a problem lands in.
+ *
+ * Arguments are those of himuon_ns_tiled, except:
+ * T                   0 or any positive tile size.
+ * workspace           device memory of at least himuon_ns_gemm_workspace_size
+ *                     (same arguments) bytes, owned by the caller: the
+ *                     problem table, the iterate buffers of one chunk and
+ *                     the GEMM library's scratch (64 MiB).
+ * chunk_budget_bytes  bound on a chunk's iterate buffers (2 m n + 2 m^2
+ *                     operand elements per problem); 0 = every problem of a
+ *                     shape in one chunk (at most 65535).
+ *
+ * The first call on a device creates the GEMM library's handle there (its
+ * own host and device resources, once per process); calls after that
+ * allocate nothing. Errors as himuon_ns_tiled, plus HIMUON_ERR_UNSUPPORTED
+ * when the GEMM library has no kernel for a shape or a Gram size exceeds
+ * 32768.
+ */
+size_t himuon_ns_gemm_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T,
+                                     int dtype, int compute, int K, float a, float b, float c,
+                                     size_t chunk_budget_bytes);
+
+int himuon_ns_gemm(int64_t n_mats,
+                   const void* const* in_ptrs, void* const* out_ptrs,
+                   const int64_t* rows, const int64_t* cols,
+                   const int64_t* ld_in, const int64_t* ld_out,
+                   int T, int K, float a, float b, float c,
+                   int dtype, int compute,
+                   void* workspace, size_t workspace_bytes,
+                   size_t chunk_budget_bytes,
+                   void* stream);
 
 /*
  * Host-only planner (no HIP call): the tiles and chunks himuon_ns_tiled

@@ -53,6 +53,12 @@ def lib():
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                       ctypes.c_int, ctypes.c_int, vp, sz, sz, vp]
         L.himuon_ns_tiled.restype = ctypes.c_int
+        L.himuon_ns_gemm_workspace_size.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                    ctypes.c_int, ctypes.c_float, ctypes.c_float,
+                                                    ctypes.c_float, sz]
+        L.himuon_ns_gemm_workspace_size.restype = sz
+        L.himuon_ns_gemm.argtypes = L.himuon_ns_tiled.argtypes
+        L.himuon_ns_gemm.restype = ctypes.c_int
         L.himuon_plan_chunks.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, sz, vp, vp, vp, i64]
         L.himuon_plan_chunks.restype = ctypes.c_int
         L.himuon_select_compute.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -90,6 +96,24 @@ def himuon_ns_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, 
     arrays (``ld_in``/``ld_out`` may be None), integers for device pointers
     and the stream handle. Returns the status code."""
     return int(lib().himuon_ns_tiled(
+        int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
+        None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
+        int(T), int(K), float(a), float(b), float(c), int(dtype), int(compute),
+        int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes),
+        int(stream) if stream else None))
+
+
+def himuon_ns_gemm_workspace_size(rows, cols, T, dtype, compute, K, a, b, c, chunk_budget_bytes=0) -> int:
+    """Workspace bytes of a himuon_ns_gemm call over matrices of these shapes (0 on an invalid plan)."""
+    return int(lib().himuon_ns_gemm_workspace_size(
+        len(rows), _i64_array(rows), _i64_array(cols), int(T), int(dtype), int(compute), int(K),
+        float(a), float(b), float(c), int(chunk_budget_bytes)))
+
+
+def himuon_ns_gemm(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c,
+                   dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream) -> int:
+    """Same arguments as the C function (see himuon_ns_tiled). Returns the status code."""
+    return int(lib().himuon_ns_gemm(
         int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
         None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
         int(T), int(K), float(a), float(b), float(c), int(dtype), int(compute),
@@ -182,4 +206,48 @@ def ns_tiled(inputs, outputs=None, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_D
         chunk_budget_bytes, stream.cuda_stream)
     if st != OK:
         raise HimuonError(st, "himuon_ns_tiled")
+    return outputs
+
+
+def ns_gemm(inputs, outputs=None, T=0, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT,
+            chunk_budget_bytes=0, workspace=None, stream=None):
+    """Phi_K of every whole matrix (T = 0) or Phi_{K,T} with T x T tiles
+    (T >= 1, e.g. 512) through library GEMMs, in one call. Arguments and
+    return value as ``ns_tiled``; ``workspace`` (if given) must hold
+    ``himuon_ns_gemm_workspace_size`` bytes for these shapes."""
+    import torch
+    inputs = list(inputs)
+    if not inputs:
+        raise ValueError("no matrices")
+    code = _dtype_code(inputs[0])
+    dev = inputs[0].device
+    for x in inputs:
+        if x.dim() != 2 or not x.is_cuda or x.device != dev or _dtype_code(x) != code or x.stride(1) != 1:
+            raise ValueError("inputs must be 2-D row-major CUDA tensors of one dtype on one device")
+    if outputs is None:
+        outputs = [torch.empty_like(x, memory_format=torch.contiguous_format) for x in inputs]
+    outputs = list(outputs)
+    if len(outputs) != len(inputs):
+        raise ValueError("inputs and outputs differ in length")
+    for x, y in zip(inputs, outputs):
+        if y.shape != x.shape or y.dtype != x.dtype or y.device != dev or y.stride(1) != 1:
+            raise ValueError("each output must match its input's shape, dtype and device")
+    n = len(inputs)
+    a, b, c = coeffs
+    rows = [x.shape[0] for x in inputs]
+    cols = [x.shape[1] for x in inputs]
+    need = himuon_ns_gemm_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
+    if need == 0:
+        raise HimuonError(ERR_INVALID_ARG, "himuon_ns_gemm_workspace_size")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    st = himuon_ns_gemm(
+        n, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs], rows, cols,
+        [x.stride(0) for x in inputs], [y.stride(0) for y in outputs],
+        T, K, a, b, c, code, compute, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+        chunk_budget_bytes, stream.cuda_stream)
+    if st != OK:
+        raise HimuonError(st, "himuon_ns_gemm")
     return outputs

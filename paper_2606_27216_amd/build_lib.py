@@ -32,8 +32,12 @@ COMMON = [
 SOURCES = [
     ("ns_tiled_kernels.hip", []),
     ("ns_tiled_f16.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form"]),
+    ("ns_gemm_kernels.hip", []),
     ("himuon_api.cpp", []),
+    ("ns_gemm_path.cpp", []),
 ]
+# The whole-matrix and large-tile path runs its Newton-Schulz GEMMs on hipBLASLt.
+LINK_LIBS = ["-lhipblaslt"]
 
 
 def hipcc() -> str:
@@ -63,7 +67,7 @@ def build(verbose: bool = False) -> str:
         _run([hipcc()] + COMMON + extra + ["-c", os.path.join(CSRC, src), "-o", obj], verbose)
         objs.append(obj)
     tmp = LIBRARY + ".tmp"
-    _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC"] + objs + ["-o", tmp], verbose)
+    _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC"] + objs + LINK_LIBS + ["-o", tmp], verbose)
     os.replace(tmp, LIBRARY)
     return LIBRARY
 

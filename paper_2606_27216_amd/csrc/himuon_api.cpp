@@ -21,13 +21,7 @@ using himuon::MatDesc;
 
 constexpr int kVersion = 100;  // 0.1.0
 
-thread_local int g_last_hip_error = 0;
-
-int hip_fail(hipError_t e)
-{
-    g_last_hip_error = (int)e;
-    return HIMUON_ERR_HIP;
-}
+int hip_fail(hipError_t e) { return himuon::set_hip_error(e); }
 
 size_t elem_size(int dtype) { return dtype == HIMUON_BF16 ? 2 : 4; }
 
@@ -73,6 +67,46 @@ int64_t chunk_bound(int64_t i, int64_t total, int64_t n_chunks)
 
 bool finite3(float a, float b, float c) { return isfinite(a) && isfinite(b) && isfinite(c); }
 
+int resolve_compute(int dtype, int compute, int K, float a, float b, float c)
+{
+    if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
+    if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
+    if (!finite3(a, b, c) || K < 0) return HIMUON_ERR_INVALID_ARG;
+    if (dtype == HIMUON_F32) {
+        if (compute == HIMUON_COMPUTE_DEFAULT || compute == HIMUON_COMPUTE_F32) return HIMUON_COMPUTE_F32;
+        return HIMUON_ERR_UNSUPPORTED;
+    }
+    if (compute == HIMUON_COMPUTE_F32) return HIMUON_ERR_UNSUPPORTED;
+    if (compute == HIMUON_COMPUTE_BF16) return HIMUON_COMPUTE_BF16;
+    // fp16 operands (kernel state Z = X |c|^(1/4), H = Z Z^T): Z, H,
+    // H + sigma b' I, the step operator a I + sigma H (H + sigma b' I), and
+    // the 256-tile chain operand Y = sigma (H + sigma b' I) Z must stay far
+    // below 65504, and so must the bf16-operand path's A = X X^T and
+    // B = bA + cA^2. Entries are bounded by spectral norms.
+    const double M = 4.0 * himuon::iterate_bound(K, a, b, c);
+    const double zs = c != 0.f ? pow(fabs((double)c), 0.25) : 1.0;
+    const double bp = c != 0.f ? fabs((double)b) / sqrt(fabs((double)c)) : fabs((double)b);
+    const double Mz = M * zs, MH = Mz * Mz;
+    const double M2 = M * M;
+    const double fp16_ops = fmax(fmax(Mz, MH + bp), fmax(fabs((double)a) + bp * MH + MH * MH, (MH + bp) * Mz));
+    const double bound = fmax(fp16_ops, fmax(M2, fabs((double)b) * M2 + fabs((double)c) * M2 * M2));
+    const bool safe = bound < 16384.0;
+    if (compute == HIMUON_COMPUTE_F16) return safe ? HIMUON_COMPUTE_F16 : HIMUON_ERR_RANGE;
+    return safe ? HIMUON_COMPUTE_F16 : HIMUON_COMPUTE_BF16;
+}
+
+}  // namespace
+
+namespace himuon {
+
+thread_local int g_last_hip_error = 0;
+
+int set_hip_error(hipError_t e)
+{
+    g_last_hip_error = (int)e;
+    return HIMUON_ERR_HIP;
+}
+
 // Largest |p^k(s)| over s in [0, 1] and k < K, for p(s) = a s + b s^3 + c s^5:
 // each singular value of the normalised tile starts in [0, 1] and follows p
 // exactly, so this bounds every entry of the operand X at every step. The
@@ -96,34 +130,6 @@ double iterate_bound(int K, double a, double b, double c)
     return m;
 }
 
-int resolve_compute(int dtype, int compute, int K, float a, float b, float c)
-{
-    if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
-    if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
-    if (!finite3(a, b, c) || K < 0) return HIMUON_ERR_INVALID_ARG;
-    if (dtype == HIMUON_F32) {
-        if (compute == HIMUON_COMPUTE_DEFAULT || compute == HIMUON_COMPUTE_F32) return HIMUON_COMPUTE_F32;
-        return HIMUON_ERR_UNSUPPORTED;
-    }
-    if (compute == HIMUON_COMPUTE_F32) return HIMUON_ERR_UNSUPPORTED;
-    if (compute == HIMUON_COMPUTE_BF16) return HIMUON_COMPUTE_BF16;
-    // fp16 operands (kernel state Z = X |c|^(1/4), H = Z Z^T): Z, H,
-    // H + sigma b' I, the step operator a I + sigma H (H + sigma b' I), and
-    // the 256-tile chain operand Y = sigma (H + sigma b' I) Z must stay far
-    // below 65504, and so must the bf16-operand path's A = X X^T and
-    // B = bA + cA^2. Entries are bounded by spectral norms.
-    const double M = 4.0 * iterate_bound(K, a, b, c);
-    const double zs = c != 0.f ? pow(fabs((double)c), 0.25) : 1.0;
-    const double bp = c != 0.f ? fabs((double)b) / sqrt(fabs((double)c)) : fabs((double)b);
-    const double Mz = M * zs, MH = Mz * Mz;
-    const double M2 = M * M;
-    const double fp16_ops = fmax(fmax(Mz, MH + bp), fmax(fabs((double)a) + bp * MH + MH * MH, (MH + bp) * Mz));
-    const double bound = fmax(fp16_ops, fmax(M2, fabs((double)b) * M2 + fabs((double)c) * M2 * M2));
-    const bool safe = bound < 16384.0;
-    if (compute == HIMUON_COMPUTE_F16) return safe ? HIMUON_COMPUTE_F16 : HIMUON_ERR_RANGE;
-    return safe ? HIMUON_COMPUTE_F16 : HIMUON_COMPUTE_BF16;
-}
-
 // Pinned host staging for the descriptor table. A ring of slots lets the
 // host run several calls ahead of the GPU; a slot is reused only after the
 // copy that read it has completed (its event).
@@ -140,47 +146,46 @@ std::mutex g_staging_mu;
 StagingSlot g_slots[kSlots];
 unsigned g_next_slot = 0;
 
-int upload_descs(const std::vector<MatDesc>& descs, void* workspace, hipStream_t stream, int dev)
+int upload_table(const void* data, size_t bytes, void* workspace, hipStream_t stream, int dev)
 {
-    const size_t bytes = descs.size() * sizeof(MatDesc);
     std::lock_guard<std::mutex> lock(g_staging_mu);
     StagingSlot& sl = g_slots[g_next_slot++ % kSlots];
     hipError_t e;
     if (sl.pending) {
         e = hipEventSynchronize(sl.ev);
-        if (e != hipSuccess) return hip_fail(e);
+        if (e != hipSuccess) return set_hip_error(e);
         sl.pending = false;
     }
     if (sl.cap < bytes) {
         if (sl.host) {
             e = hipHostFree(sl.host);
-            if (e != hipSuccess) return hip_fail(e);
+            if (e != hipSuccess) return set_hip_error(e);
             sl.host = nullptr;
             sl.cap = 0;
         }
         size_t cap = 4096;
         while (cap < bytes) cap *= 2;
         e = hipHostMalloc(&sl.host, cap, hipHostMallocDefault);
-        if (e != hipSuccess) return hip_fail(e);
+        if (e != hipSuccess) return set_hip_error(e);
         sl.cap = cap;
     }
     if (sl.dev != dev) {
         if (sl.ev) (void)hipEventDestroy(sl.ev);
         sl.ev = nullptr;
         e = hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
-        if (e != hipSuccess) return hip_fail(e);
+        if (e != hipSuccess) return set_hip_error(e);
         sl.dev = dev;
     }
-    memcpy(sl.host, descs.data(), bytes);
+    memcpy(sl.host, data, bytes);
     e = hipMemcpyAsync(workspace, sl.host, bytes, hipMemcpyHostToDevice, stream);
-    if (e != hipSuccess) return hip_fail(e);
+    if (e != hipSuccess) return set_hip_error(e);
     e = hipEventRecord(sl.ev, stream);
-    if (e != hipSuccess) return hip_fail(e);
+    if (e != hipSuccess) return set_hip_error(e);
     sl.pending = true;
     return HIMUON_OK;
 }
 
-}  // namespace
+}  // namespace himuon
 
 extern "C" {
 
@@ -279,7 +284,7 @@ int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out
     }
     if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e);
 
-    int status = upload_descs(descs, workspace, hs, dev);
+    int status = himuon::upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
     if (status == HIMUON_OK) {
         himuon::KernelArgs ka;
         ka.descs = static_cast<const MatDesc*>(workspace);
@@ -325,7 +330,7 @@ const char* himuon_status_string(int status)
     }
 }
 
-int himuon_last_hip_error(void) { return g_last_hip_error; }
+int himuon_last_hip_error(void) { return himuon::g_last_hip_error; }
 
 int himuon_version(void) { return kVersion; }
 

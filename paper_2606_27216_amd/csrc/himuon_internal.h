@@ -53,7 +53,18 @@ hipError_t launch_ns_tiled(int T, Storage st, Operand op, const KernelArgs& args
 // True when a kernel exists for the triple (no HIP call).
 bool has_kernel(int T, Storage st, Operand op);
 
-// The fp16-operand kernel family (bf16 storage), T in {32, 64, 128}.
+// The fp16-operand kernel family (bf16 storage), T in {32, 64, 128, 256}.
 hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream);
+
+// Host helpers shared by the entry points (himuon_api.cpp).
+extern thread_local int g_last_hip_error;
+// Records `e` as the calling thread's last HIP error; returns HIMUON_ERR_HIP.
+int set_hip_error(hipError_t e);
+// Copies `bytes` of host data to device memory `dst` on `stream` through a
+// ring of pinned staging slots (asynchronous; a slot is reused once its
+// copy has completed). Returns a himuon status.
+int upload_table(const void* data, size_t bytes, void* dst, hipStream_t stream, int dev);
+// Largest |p^k(s)| over s in [0, 1], k < K, p(s) = a s + b s^3 + c s^5.
+double iterate_bound(int K, double a, double b, double c);
 
 }  // namespace himuon

@@ -1,0 +1,219 @@
+// Gather, normalisation and scatter kernels of the library-GEMM path
+// (whole matrices and large tiles). The Newton-Schulz steps themselves are
+// three library GEMMs per step (see ns_gemm_path.cpp); these kernels move a
+// problem's block between the caller's matrix and the iterate buffer:
+//   - B_T (Sec. 2.1, eq. tiling_operator): the block at the top left of an
+//     m x n iterate, zero elsewhere; a whole matrix with more rows than
+//     columns is taken transposed (Phi_K(S^T) = Phi_K(S)^T), so the Gram
+//     matrix is the smaller one;
+//   - the normalisation X0 = S / ||S||_F of Phi_K (Sec. 2.2, eq. phi_k_def;
+//     Phi_K(0) = 0), with the norm summed in fp64 in a fixed order, so a
+//     result never depends on how problems are grouped into launches;
+//   - B_T^{-1}: the block part of the final iterate back to the matrix.
+#include "ns_gemm_path.h"
+
+#include <hip/hip_bf16.h>
+#include <hip/hip_fp16.h>
+#include <math.h>
+
+namespace himuon {
+namespace {
+
+constexpr int kThreads = 256;  // 32 x 8: a 32 x 32 iterate tile, four rows per thread
+
+template <GemmStore ST>
+__device__ __forceinline__ double load_elem(const void* base, int64_t idx)
+{
+    if constexpr (ST == GemmStore::BF16) {
+        const uint16_t u = static_cast<const uint16_t*>(base)[idx];
+        return (double)__uint_as_float((uint32_t)u << 16);
+    } else {
+        return (double)static_cast<const float*>(base)[idx];
+    }
+}
+
+template <GemmStore ST>
+__device__ __forceinline__ void store_elem(void* base, int64_t idx, float v)
+{
+    if constexpr (ST == GemmStore::BF16) {
+        const __bf16 h = (__bf16)v;  // round to nearest even
+        static_cast<__bf16*>(base)[idx] = h;
+    } else {
+        static_cast<float*>(base)[idx] = v;
+    }
+}
+
+template <GemmOperand OP> struct OpType;
+template <> struct OpType<GemmOperand::F32> { typedef float T; };
+template <> struct OpType<GemmOperand::F16> { typedef _Float16 T; };
+template <> struct OpType<GemmOperand::BF16> { typedef __bf16 T; };
+
+// Part j of problem p sums the squares of rows [j*rpp, (j+1)*rpp) of its
+// block, each thread over a fixed set of columns, then a fixed-order tree.
+template <GemmStore ST>
+__global__ void __launch_bounds__(kThreads) gemm_norm_partials(const GemmProb* probs, int nparts, double* partial)
+{
+    const GemmProb P = probs[blockIdx.y];
+    const int rpp = (P.h + nparts - 1) / nparts;
+    const int r0 = (int)blockIdx.x * rpp;
+    const int r1 = min(P.h, r0 + rpp);
+    double acc = 0.0;
+    for (int r = r0; r < r1; ++r) {
+        const int64_t rowoff = (P.row0 + r) * P.ld_in + P.col0;
+        for (int c = threadIdx.x; c < P.w; c += kThreads) {
+            const double v = load_elem<ST>(P.in, rowoff + c);
+            acc += v * v;
+        }
+    }
+    __shared__ double red[kThreads];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+#pragma unroll
+    for (int s = kThreads / 2; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partial[(int64_t)blockIdx.y * nparts + blockIdx.x] = red[0];
+}
+
+// The problem's scale factor, scale / ||B||_F (0 for a zero block), written
+// over its first partial.
+__global__ void gemm_norm_finalize(int nprob, int nparts, double scale, double* partial)
+{
+    const int p = blockIdx.x * blockDim.x + threadIdx.x;
+    if (p >= nprob) return;
+    double ss = 0.0;
+    for (int j = 0; j < nparts; ++j) ss += partial[(int64_t)p * nparts + j];
+    partial[(int64_t)p * nparts] = ss > 0.0 ? scale / sqrt(ss) : 0.0;
+}
+
+template <GemmStore ST, GemmOperand OP>
+__global__ void __launch_bounds__(kThreads) gemm_gather(const GemmProb* probs, int m, int n, int nparts,
+                                                        const double* partial, void* xv)
+{
+    typedef typename OpType<OP>::T OT;
+    const int p = blockIdx.y;
+    const GemmProb P = probs[p];
+    const double s = partial[(int64_t)p * nparts];
+    const int tiles_n = (n + 31) / 32;
+    const int i0 = (int)(blockIdx.x / tiles_n) * 32, j0 = (int)(blockIdx.x % tiles_n) * 32;
+    OT* x = static_cast<OT*>(xv) + (int64_t)p * m * n;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    if (!P.trans) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int i = i0 + ty + 8 * k, j = j0 + tx;
+            if (i < m && j < n) {
+                double v = 0.0;
+                if (i < P.h && j < P.w) v = load_elem<ST>(P.in, (P.row0 + i) * P.ld_in + P.col0 + j) * s;
+                x[(int64_t)i * n + j] = (OT)(float)v;
+            }
+        }
+    } else {
+        // iterate (i, j) = block (j, i): block rows j0.., columns i0.. through LDS
+        __shared__ float t[32][33];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int r = j0 + ty + 8 * k, c = i0 + tx;
+            double v = 0.0;
+            if (r < P.h && c < P.w) v = load_elem<ST>(P.in, (P.row0 + r) * P.ld_in + P.col0 + c) * s;
+            t[ty + 8 * k][tx] = (float)v;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int i = i0 + ty + 8 * k, j = j0 + tx;
+            if (i < m && j < n) x[(int64_t)i * n + j] = (OT)t[tx][ty + 8 * k];
+        }
+    }
+}
+
+template <GemmStore ST, GemmOperand OP>
+__global__ void __launch_bounds__(kThreads) gemm_scatter(const GemmProb* probs, int m, int n, float inv_scale,
+                                                         const void* xv)
+{
+    typedef typename OpType<OP>::T OT;
+    const int p = blockIdx.y;
+    const GemmProb P = probs[p];
+    const int tiles_n = (n + 31) / 32;
+    const int i0 = (int)(blockIdx.x / tiles_n) * 32, j0 = (int)(blockIdx.x % tiles_n) * 32;
+    const OT* x = static_cast<const OT*>(xv) + (int64_t)p * m * n;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    if (!P.trans) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int i = i0 + ty + 8 * k, j = j0 + tx;
+            if (i < P.h && j < P.w)
+                store_elem<ST>(P.out, (P.row0 + i) * P.ld_out + P.col0 + j, (float)x[(int64_t)i * n + j] * inv_scale);
+        }
+    } else {
+        __shared__ float t[32][33];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int i = i0 + ty + 8 * k, j = j0 + tx;
+            t[ty + 8 * k][tx] = (i < m && j < n) ? (float)x[(int64_t)i * n + j] * inv_scale : 0.f;
+        }
+        __syncthreads();
+        // block (r, c) = iterate (c, r): block rows j0.., columns i0..
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int r = j0 + ty + 8 * k, c = i0 + tx;
+            if (r < P.h && c < P.w) store_elem<ST>(P.out, (P.row0 + r) * P.ld_out + P.col0 + c, t[tx][ty + 8 * k]);
+        }
+    }
+}
+
+dim3 tile_grid(int m, int n, int nprob)
+{
+    return dim3((unsigned)(((m + 31) / 32) * ((n + 31) / 32)), (unsigned)nprob, 1);
+}
+
+}  // namespace
+
+hipError_t launch_gemm_norm_partials(GemmStore st, const GemmProb* probs, int nprob, int nparts, double* partial,
+                                     hipStream_t stream)
+{
+    if (nprob <= 0) return hipSuccess;
+    const dim3 grid((unsigned)nparts, (unsigned)nprob, 1);
+    if (st == GemmStore::BF16)
+        hipLaunchKernelGGL(gemm_norm_partials<GemmStore::BF16>, grid, dim3(kThreads), 0, stream, probs, nparts, partial);
+    else
+        hipLaunchKernelGGL(gemm_norm_partials<GemmStore::F32>, grid, dim3(kThreads), 0, stream, probs, nparts, partial);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_gather(GemmStore st, GemmOperand op, const GemmProb* probs, int nprob, int m, int n,
+                              int nparts, const double* partial, double scale, void* x, hipStream_t stream)
+{
+    if (nprob <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gemm_norm_finalize, dim3((unsigned)((nprob + 255) / 256)), dim3(256), 0, stream, nprob, nparts,
+                       scale, const_cast<double*>(partial));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid = tile_grid(m, n, nprob);
+#define HM_GATHER(S, O) \
+    hipLaunchKernelGGL((gemm_gather<S, O>), grid, dim3(kThreads), 0, stream, probs, m, n, nparts, partial, x)
+    if (st == GemmStore::F32 && op == GemmOperand::F32) HM_GATHER(GemmStore::F32, GemmOperand::F32);
+    else if (st == GemmStore::BF16 && op == GemmOperand::F16) HM_GATHER(GemmStore::BF16, GemmOperand::F16);
+    else if (st == GemmStore::BF16 && op == GemmOperand::BF16) HM_GATHER(GemmStore::BF16, GemmOperand::BF16);
+    else return hipErrorInvalidValue;
+#undef HM_GATHER
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_scatter(GemmStore st, GemmOperand op, const GemmProb* probs, int nprob, int m, int n,
+                               float inv_scale, const void* x, hipStream_t stream)
+{
+    if (nprob <= 0) return hipSuccess;
+    const dim3 grid = tile_grid(m, n, nprob);
+#define HM_SCATTER(S, O) \
+    hipLaunchKernelGGL((gemm_scatter<S, O>), grid, dim3(kThreads), 0, stream, probs, m, n, inv_scale, x)
+    if (st == GemmStore::F32 && op == GemmOperand::F32) HM_SCATTER(GemmStore::F32, GemmOperand::F32);
+    else if (st == GemmStore::BF16 && op == GemmOperand::F16) HM_SCATTER(GemmStore::BF16, GemmOperand::F16);
+    else if (st == GemmStore::BF16 && op == GemmOperand::BF16) HM_SCATTER(GemmStore::BF16, GemmOperand::BF16);
+    else return hipErrorInvalidValue;
+#undef HM_SCATTER
+    return hipGetLastError();
+}
+
+}  // namespace himuon

@@ -150,3 +150,53 @@ def test_planner_errors():
         hm.himuon_plan_chunks([10], [10], 32, hm.BF16, 1000)  # budget below one tile
     with pytest.raises(hm.HimuonError):
         hm.himuon_plan_chunks([0], [10], 32, hm.BF16, 0)
+
+
+# ---- the library-GEMM path (himuon_ns_gemm): sizing and validation, no HIP call
+
+def test_gemm_workspace_size():
+    a, b, c = hm.QUINTIC
+    ws = lambda rows, cols, T, dtype=hm.BF16, budget=0, compute=hm.COMPUTE_DEFAULT, K=5: \
+        hm.himuon_ns_gemm_workspace_size(rows, cols, T, dtype, compute, K, a, b, c, budget)
+    lt = 64 << 20
+    # one 7B layer as whole matrices: the 4096 x 4096 group (4 problems of X, X', A, B in fp16) dominates
+    layer_r, layer_c = [4096] * 4 + [11008, 11008, 4096], [4096] * 4 + [4096, 4096, 11008]
+    assert ws(layer_r, layer_c, 0) >= 4 * 4 * 4096 * 4096 * 2 + lt
+    # fp32 storage doubles the iterate bytes
+    assert ws([512], [512], 0, hm.F32) - lt > ws([512], [512], 0) - lt
+    # a chunk budget bounds the buffers; below one problem there is no plan
+    one = 2 * (2 * 512 * 512 + 2 * 512 * 512)
+    assert ws([4096], [4096], 512, budget=2 * one) < ws([4096], [4096], 512)
+    assert ws([4096], [4096], 512, budget=one - 1) == 0
+    assert ws([0], [64], 0) == 0
+    assert ws([64], [64], -1) == 0
+    assert ws([64], [64], 0, dtype=7) == 0
+    assert ws([64], [64], 0, dtype=hm.F32, compute=hm.COMPUTE_F16) == 0
+    assert ws([40000], [40000], 0) == 0  # Gram size above 32768
+
+
+def _gcall(**kw):
+    args = dict(n_mats=1, in_ptrs=[FAKE], out_ptrs=[FAKE], rows=[64], cols=[64], ld_in=None, ld_out=None,
+                T=0, K=5, a=3.4445, b=-4.775, c=2.0315, dtype=hm.BF16, compute=hm.COMPUTE_DEFAULT,
+                workspace=FAKE, workspace_bytes=256, chunk_budget_bytes=0, stream=None)
+    args.update(kw)
+    return hm.himuon_ns_gemm(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(in_ptrs=[0]), hm.ERR_INVALID_ARG),
+    (dict(rows=[0]), hm.ERR_INVALID_ARG),
+    (dict(ld_in=[63]), hm.ERR_INVALID_ARG),
+    (dict(T=-1), hm.ERR_INVALID_ARG),
+    (dict(K=-1), hm.ERR_INVALID_ARG),
+    (dict(b=float("nan")), hm.ERR_INVALID_ARG),
+    (dict(dtype=7), hm.ERR_INVALID_ARG),
+    (dict(dtype=hm.F32, compute=hm.COMPUTE_BF16), hm.ERR_UNSUPPORTED),
+    (dict(rows=[40000], cols=[40000]), hm.ERR_UNSUPPORTED),
+    (dict(compute=hm.COMPUTE_F16, a=50.0, b=0.0, c=0.0), hm.ERR_RANGE),
+    (dict(workspace=0), hm.ERR_WORKSPACE),
+    (dict(workspace_bytes=1 << 20), hm.ERR_WORKSPACE),
+    (dict(T=512, chunk_budget_bytes=100), hm.ERR_WORKSPACE),
+])
+def test_gemm_validation_rejects_before_any_hip_call(kw, status):
+    assert _gcall(**kw) == status

@@ -1,0 +1,110 @@
+"""The library-GEMM path (himuon_ns_gemm) against the fp64 oracle.
+
+T = 0 is Phi_K of the whole matrix (the full-matrix branch, Sec. 4.4.3):
+checked against the oracle's phi_k, with the relative Frobenius error of the
+whole matrix. T >= 1 is the tiled map with each tile a GEMM problem
+(T = 512, the multi-kernel tile of Sec. 4.4.1): checked tile by tile against
+the oracle's ns_tiled. Bars as for the fused kernels: 1e-5 (fp32 storage),
+2e-2 (bf16 storage).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_27216_amd as hm
+from parity import COEF32, TOL, tile_errors, to_f64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def announce(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def rand(shape, dtype, seed, scale=1.0):
+    g = np.random.default_rng(seed)
+    x = g.standard_normal(shape) * scale
+    return torch.tensor(x, dtype=torch.float32).to(dtype).to(DEV)
+
+
+def rel(y, r):
+    nr = np.linalg.norm(r)
+    return (0.0 if not np.any(y) else np.inf) if nr == 0 else np.linalg.norm(y - r) / nr
+
+
+def gemm(mats, T, K=5, coeffs=COEF32, compute=hm.COMPUTE_DEFAULT, budget=0):
+    out = hm.ns_gemm(mats, T=T, K=K, coeffs=coeffs, compute=compute, chunk_budget_bytes=budget)
+    torch.cuda.synchronize()
+    return out
+
+
+SHAPES = [(384, 640), (640, 384), (512, 512), (1, 700), (333, 1), (257, 1000)]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_full_matrix(dtype):
+    announce(f"gemm T=0 dtype={dtype} shapes={SHAPES}")
+    mats = [rand(s, dtype, 100 + i) for i, s in enumerate(SHAPES)]
+    out = gemm(mats, T=0)
+    for x, y in zip(mats, out):
+        e = rel(to_f64(y), oracle.phi_k(to_f64(x), 5, *COEF32))
+        assert e <= TOL[dtype], f"{tuple(x.shape)}: error {e:.3e}"
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_tiles_512(dtype):
+    announce(f"gemm T=512 dtype={dtype} (ragged 2x2 tile grid)")
+    x = rand((700, 900), dtype, 7)
+    y = gemm([x], T=512)[0]
+    R = oracle.ns_tiled(to_f64(x), 512, 5, *COEF32)
+    e = tile_errors(to_f64(y), R, 512)
+    assert e.max() <= TOL[dtype], f"max per-tile error {e.max():.3e}"
+
+
+def test_tiles_128_agree_with_fused_kernel():
+    announce("gemm T=128 vs oracle and vs the fused kernel, bf16")
+    x = rand((384, 520), torch.bfloat16, 11)
+    y = gemm([x], T=128)[0]
+    z = hm.ns_tiled([x], T=128, K=5, coeffs=COEF32)[0]
+    torch.cuda.synchronize()
+    R = oracle.ns_tiled(to_f64(x), 128, 5, *COEF32)
+    assert tile_errors(to_f64(y), R, 128).max() <= 2e-2
+    assert tile_errors(to_f64(y), to_f64(z), 128).max() <= 2e-2
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_zero_and_k0(dtype):
+    announce(f"gemm zero matrix and K=0, dtype={dtype}")
+    z = torch.zeros((200, 300), dtype=dtype, device=DEV)
+    assert not torch.any(gemm([z], T=0)[0])
+    x = rand((200, 300), dtype, 3, scale=1e3)
+    y0 = gemm([x], T=0, K=0)[0]
+    S = to_f64(x)
+    assert rel(to_f64(y0), S / np.linalg.norm(S)) <= TOL[dtype]
+
+
+def test_chunked_matches_one_chunk():
+    announce("gemm T=512 with several chunks vs one chunk, bf16")
+    mats = [rand((1024, 1024), torch.bfloat16, 40 + i) for i in range(2)]
+    one = gemm(mats, T=512)
+    ws1 = hm.himuon_ns_gemm_workspace_size([1024, 1024], [1024, 1024], 512, hm.BF16, 0, 5, *COEF32)
+    per = 2 * (2 * 512 * 512 + 2 * 512 * 512)  # fp16 iterate buffers of one problem
+    many = gemm(mats, T=512, budget=3 * per)
+    ws3 = hm.himuon_ns_gemm_workspace_size([1024, 1024], [1024, 1024], 512, hm.BF16, 0, 5, *COEF32, 3 * per)
+    assert ws3 < ws1
+    for a, b, x in zip(one, many, mats):
+        R = oracle.ns_tiled(to_f64(x), 512, 5, *COEF32)
+        assert tile_errors(to_f64(a), R, 512).max() <= 2e-2
+        assert tile_errors(to_f64(b), R, 512).max() <= 2e-2
+        assert tile_errors(to_f64(a), to_f64(b), 512).max() <= 1e-3
+
+
+def test_transpose_equivariance():
+    announce("gemm T=0: Phi(S^T) = Phi(S)^T, fp32")
+    x = rand((300, 500), torch.float32, 5)
+    y = gemm([x], T=0)[0]
+    yt = gemm([x.t().contiguous()], T=0)[0]
+    assert rel(to_f64(yt).T, to_f64(y)) <= 2e-6

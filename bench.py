@@ -129,6 +129,61 @@ def cpu_baseline(mats, T, K, coeffs, budget_s, seed=0):
             "sample": f"{done} random {T}x{T} tiles of the same workload (fp64 oracle, {elapsed:.1f} s)"}
 
 
+def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, stream):
+    """The library-GEMM path: whole matrices (T = 0, the full-matrix branch)
+    or large tiles (T >= 1). Work counted: for T >= 1 the tiled metric
+    6*H*W*T*K; for T = 0 the three products of each step on the m x n
+    iterate (m = min(H, W)): (2 m^2 n + 2 m^3 + 2 m^2 n) K. Both are what
+    the GEMMs issue (no symmetry is exploited on this path)."""
+    rows = [x.shape[0] for x in mats]
+    cols = [x.shape[1] for x in mats]
+    if args.T == 0:
+        flops_step = sum((4.0 * min(h, w) ** 2 * max(h, w) + 2.0 * min(h, w) ** 3) * args.K for h, w in zip(rows, cols))
+        metric = "full-matrix NS TFLOP/s ((4m^2n + 2m^3)K, m = min(H,W)), 7B layer stack K=%d" % args.K
+    else:
+        flops_step = sum(6.0 * h * w * args.T * args.K for h, w in zip(rows, cols))
+        metric = "tiled-NS TFLOP/s (6*H*W*T*K) + %% bf16 MFMA peak, 7B layer stack T=%d K=%d (library GEMMs)" % (args.T, args.K)
+    need = hm.himuon_ns_gemm_workspace_size(rows, cols, args.T, code, compute, args.K, *coeffs, int(args.budget))
+    if need == 0:
+        raise SystemExit("no plan for this call (budget below one problem?)")
+    log(f"gemm path workspace {need / 2**30:.2f} GiB")
+    ws = torch.empty(need, dtype=torch.uint8, device=mats[0].device)
+
+    def step():
+        hm.ns_gemm(mats, outputs=outs, T=args.T, K=args.K, coeffs=coeffs, compute=compute,
+                   chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    op_name = "f32" if code == hm.F32 else ("bf16" if compute == hm.COMPUTE_BF16 else "f16")
+    peak = PEAK_TFLOPS[op_name]
+    achieved = flops_step / (float(np.mean(step_ms)) * 1e-3) / 1e12
+    rec = {
+        "metric": metric, "value": round(flops_step / (wall / args.steps) / 1e12, 3), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": op_name, "data": "synthetic",
+        "config": {"workload": desc, "path": "gemm", "T": args.T, "K": args.K, "matrices": len(mats),
+                   "storage": args.dtype, "mfma_operands": op_name, "accumulate": "f32",
+                   "chunk_budget_bytes": int(args.budget), "workspace_bytes": need},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None, "flops_per_step": flops_step,
+                     "mean_step_ms": round(float(np.mean(step_ms)), 4)},
+        "step_ms": {"median": round(float(np.median(step_ms)), 4),
+                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4)},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,6 +196,9 @@ def main():
     ap.add_argument("--compute", default="default", choices=["default", "f16", "bf16", "f32"])
     ap.add_argument("--budget", type=float, default=16e9, help="chunk budget in bytes (0: one chunk)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
+    ap.add_argument("--path", default="tiled", choices=["tiled", "gemm"],
+                    help="tiled: the fused per-tile kernels (T <= 256); gemm: himuon_ns_gemm, whole matrices "
+                         "(--T 0) or large tiles (e.g. --T 512) through batched library GEMMs")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB per launch (counter calibration)")
     args = ap.parse_args()
@@ -182,6 +240,9 @@ def main():
     rows = [x.shape[0] for x in mats]
     cols = [x.shape[1] for x in mats]
     code = hm.BF16 if args.dtype == "bf16" else hm.F32
+    stream = torch.cuda.current_stream(dev)
+    if args.path == "gemm":
+        return bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, stream)
     total, bounds = hm.himuon_plan_chunks(rows, cols, args.T, code, int(args.budget))
     launches = len(bounds) - 1
     flops_step = sum(6.0 * h * w * args.T * args.K for h, w in zip(rows, cols))
@@ -189,7 +250,6 @@ def main():
     bytes_step = sum(2.0 * h * w * elem for h, w in zip(rows, cols))
 
     ws = torch.empty(hm.himuon_ns_tiled_workspace_size(len(mats)), dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream(dev)
 
     def step():
         hm.ns_tiled(mats, outputs=outs, T=args.T, K=args.K, coeffs=coeffs, compute=compute,

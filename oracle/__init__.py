@@ -16,6 +16,9 @@ taken as given, so callers that want the GPU's fp32 coefficients pass
 * ``ns_tiled(A, T, K, a, b, c)``    Φ_{K,T}(A), eq. (tiled_ns).
 * ``ns_tiles(A, T, K, a, b, c, ids)`` selected tiles of Φ_{K,T}, each T×T.
 * ``tile_count(H, W, T)``           R·C of the tiling operator B_T.
+* ``himuon_step(W, M, G, T, K, a, b, c, lr, beta, wd, nesterov, scale_c)``
+                                    one optimizer step of Alg. 1 (T = 0: the
+                                    full-matrix branch); returns (W', M', U).
 """
 from __future__ import annotations
 
@@ -58,6 +61,9 @@ def _bind(lib):
     lib.oracle_ns_tiled.restype = ctypes.c_int
     lib.oracle_ns_tiles.argtypes = [p, i64, i64, i64, i64, ctypes.c_int, d, d, d, i64, p, p]
     lib.oracle_ns_tiles.restype = ctypes.c_int
+    lib.oracle_himuon_step.argtypes = [p, p, p, i64, i64, i64, ctypes.c_int, d, d, d, d, d, d, ctypes.c_int,
+                                       d, p]
+    lib.oracle_himuon_step.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     return lib
@@ -123,6 +129,22 @@ def ns_tiles(A, T, K, a, b, c, tile_ids, lib=None):
 def tile_count(H, W, T, lib=None):
     lib = lib or load()
     return int(lib.oracle_tile_count(int(H), int(W), int(T)))
+
+
+def himuon_step(W, M, G, T, K, a, b, c, lr, beta, weight_decay, nesterov, scale_c, lib=None):
+    """Alg. 1 for one matrix: returns new copies (W', M', U); inputs untouched."""
+    lib = lib or load()
+    W1 = _f64(W).copy()
+    M1 = _f64(M).copy()
+    G = _f64(G)
+    if W1.shape != M1.shape or W1.shape != G.shape:
+        raise ValueError("W, M and G must have one shape")
+    H, Wd = W1.shape
+    U = np.empty_like(W1)
+    _check(lib.oracle_himuon_step(W1.ctypes.data, M1.ctypes.data, G.ctypes.data, H, Wd, int(T), int(K),
+                                  float(a), float(b), float(c), float(lr), float(beta), float(weight_decay),
+                                  int(bool(nesterov)), float(scale_c), U.ctypes.data), "himuon_step")
+    return W1, M1, U
 
 
 def num_threads(lib=None):

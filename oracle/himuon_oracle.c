@@ -206,6 +206,53 @@ int oracle_ns_tiles(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_
     return status;
 }
 
+/*
+ * One HiMuon optimizer step of one matrix (Sec. 3.4's Muon update with the
+ * tiled map substituted, Alg. 1, Sec. 4.3 eq. (scaled_update)), in place on
+ * the H x W weights Wt and momentum Mt (both contiguous), given the gradient
+ * G (contiguous):
+ *   M   <- beta M + G                                   eq. (muon_momentum)
+ *   Ghat = G + beta M  (Nesterov, eq. (muon_lookahead)), else Ghat = M
+ *   if T == 0 (the branch T = infinity) or T >= max(H, W):
+ *       U = Phi_K(Ghat),         tau = scale_c * sqrt(max(H, W))
+ *   else
+ *       U = Phi_{K,T}(Ghat),     tau = scale_c * sqrt(T)
+ *   W   <- (1 - lr * lambda) W - lr * tau * U
+ * The update direction U is also written to U_out when it is non-null.
+ */
+int oracle_himuon_step(double* Wt, double* Mt, const double* G, int64_t H, int64_t W, int64_t T, int K,
+                       double a, double b, double c, double lr, double beta, double lambda, int nesterov,
+                       double scale_c, double* U_out)
+{
+    if (!Wt || !Mt || !G || H < 1 || W < 1 || T < 0 || K < 0) return ORACLE_BAD_ARG;
+    int64_t n = H * W;
+    double* Ghat = (double*)malloc(sizeof(double) * n);
+    double* U = (double*)malloc(sizeof(double) * n);
+    if (!Ghat || !U) {
+        free(Ghat);
+        free(U);
+        return ORACLE_NO_MEM;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        Mt[i] = beta * Mt[i] + G[i];
+        Ghat[i] = nesterov ? G[i] + beta * Mt[i] : Mt[i];
+    }
+    int64_t big = H > W ? H : W;
+    int full = T == 0 || T >= big;
+    int st = full ? oracle_phi_k(Ghat, H, W, W, K, a, b, c, U, W)
+                  : oracle_ns_tiled(Ghat, H, W, W, T, K, a, b, c, U, W);
+    if (st == ORACLE_OK) {
+        double tau = scale_c * sqrt((double)(full ? big : T));
+        for (int64_t i = 0; i < n; ++i) {
+            Wt[i] = (1.0 - lr * lambda) * Wt[i] - lr * tau * U[i];
+            if (U_out) U_out[i] = U[i];
+        }
+    }
+    free(Ghat);
+    free(U);
+    return st;
+}
+
 /* Threads an OpenMP parallel region of this library uses (0 without OpenMP). */
 int oracle_num_threads(void)
 {

@@ -16,7 +16,12 @@ relative error it saw. The routes:
 * invariances that any correct implementation obeys: transposition,
   orthogonal equivariance, odd homogeneity of degree 0, tile permutation;
 * the textbook special case: cubic Newton–Schulz (1.5, −0.5, 0) converges to
-  the polar factor (``scipy.linalg.polar``) for well-conditioned input.
+  the polar factor (``scipy.linalg.polar``) for well-conditioned input;
+* for the optimizer step of Alg. 1: geometric sums over repeated steps with a
+  constant gradient (the momentum buffer and the decayed weights have closed
+  forms, and Φ_K is blind to positive scaling), the sign of the second
+  update under a gradient that reverses, and the branch rule of eq.
+  (scaled_update) on shapes where tiling and the full map give different τ.
 
 ``run_all`` is used by the mutation test in a subprocess, so a mutant that
 crashes or misbehaves anywhere is reported as caught.
@@ -264,10 +269,89 @@ def pin_tile_count(lib=None):
     return float(bad)
 
 
+STEP = dict(a=QUINTIC[0], b=QUINTIC[1], c=QUINTIC[2], K=5)
+
+
+def _tilewise_closed_form(S, T, K):
+    """Φ_{K,T} by numpy slicing of the zero-padded matrix, each tile by SVD."""
+    H, W = S.shape
+    R, C = -(-H // T), -(-W // T)
+    P = np.zeros((R * T, C * T))
+    P[:H, :W] = S
+    Y = np.zeros_like(P)
+    for r in range(R):
+        for q in range(C):
+            Y[r * T:(r + 1) * T, q * T:(q + 1) * T] = svd_closed_form(P[r * T:(r + 1) * T, q * T:(q + 1) * T], K)
+    return Y[:H, :W]
+
+
+def pin_step_constant_gradient(lib=None):
+    """t steps from M = 0 with one gradient G: M_t = G (1 - β^t)/(1 - β); the
+    direction Ĝ is a positive multiple of G (either flag), so U = Φ_{K,T}(G)
+    every step and W_t = d^t W_0 - lr τ U (1 - d^t)/(1 - d), d = 1 - lr λ."""
+    g = np.random.default_rng(21)
+    worst = 0.0
+    lr, beta, lam, sc, steps = 0.05, 0.9, 0.3, 0.2, 4
+    for (H, W, T, nesterov) in [(48, 100, 32, True), (48, 100, 64, False), (90, 60, 0, True), (33, 33, 128, False)]:
+        G = g.standard_normal((H, W))
+        W0 = g.standard_normal((H, W))
+        Wt, Mt = W0.copy(), np.zeros((H, W))
+        for _ in range(steps):
+            Wt, Mt, _U = oracle.himuon_step(Wt, Mt, G, T, lr=lr, beta=beta, weight_decay=lam, nesterov=nesterov,
+                                            scale_c=sc, lib=lib, **STEP)
+        big = max(H, W)
+        full = T == 0 or T >= big
+        U = svd_closed_form(G, STEP["K"]) if full else _tilewise_closed_form(G, T, STEP["K"])
+        tau = sc * np.sqrt(big if full else T)
+        d = 1.0 - lr * lam
+        W_ref = d ** steps * W0 - lr * tau * U * (1.0 - d ** steps) / (1.0 - d)
+        M_ref = G * (1.0 - beta ** steps) / (1.0 - beta)
+        worst = max(worst, rel(Wt, W_ref), rel(Mt, M_ref))
+    return worst
+
+
+def pin_step_nesterov_sign(lib=None):
+    """Gradients G then -0.85 G with β = 0.9 from M = 0: the second direction
+    is G (-0.85 + β² - 0.85 β) = -0.805 G with Nesterov (U = -Φ_K(G)) and the
+    new buffer (β - 0.85) G = 0.05 G without it (U = +Φ_K(G))."""
+    g = np.random.default_rng(22)
+    G = g.standard_normal((40, 72))
+    U_ref = svd_closed_form(G, STEP["K"])
+    worst = 0.0
+    for nesterov, sign in [(True, -1.0), (False, 1.0)]:
+        Wt, Mt = np.zeros_like(G), np.zeros_like(G)
+        Wt, Mt, U1 = oracle.himuon_step(Wt, Mt, G, 0, lr=0.1, beta=0.9, weight_decay=0.0, nesterov=nesterov,
+                                        scale_c=0.2, lib=lib, **STEP)
+        Wt, Mt, U2 = oracle.himuon_step(Wt, Mt, -0.85 * G, 0, lr=0.1, beta=0.9, weight_decay=0.0,
+                                        nesterov=nesterov, scale_c=0.2, lib=lib, **STEP)
+        tau = 0.2 * np.sqrt(72)
+        worst = max(worst, rel(U1, U_ref), rel(U2, sign * U_ref), rel(Mt, 0.05 * G),
+                    rel(Wt, -0.1 * tau * (1.0 + sign) * U_ref) if sign > 0 else rel(Wt, np.zeros_like(G)))
+    return worst
+
+
+def pin_step_scale_branch(lib=None):
+    """Eq. (scaled_update): with W = 0, β = 0, λ = 0 one step leaves
+    W = -lr τ U. T >= max(H, W) is the full map with τ = c sqrt(max(H, W));
+    T < max(H, W) tiles with τ = c sqrt(T), also when T exceeds min(H, W)."""
+    g = np.random.default_rng(23)
+    worst = 0.0
+    for (H, W, T) in [(48, 100, 64), (100, 48, 64), (48, 100, 100), (48, 100, 256), (100, 48, 0)]:
+        G = g.standard_normal((H, W))
+        Wt, _M, U = oracle.himuon_step(np.zeros((H, W)), np.zeros((H, W)), G, T, lr=0.5, beta=0.0,
+                                       weight_decay=0.0, nesterov=False, scale_c=0.2, lib=lib, **STEP)
+        full = T == 0 or T >= max(H, W)
+        U_ref = svd_closed_form(G, STEP["K"]) if full else _tilewise_closed_form(G, T, STEP["K"])
+        tau = 0.2 * np.sqrt(max(H, W) if full else T)
+        worst = max(worst, rel(U, U_ref), rel(Wt, -0.5 * tau * U_ref))
+    return worst
+
+
 PINS = [
     pin_svd_closed_form, pin_tiled_blocks, pin_sampled_tiles, pin_rank_one, pin_scaled_orthogonal,
     pin_diagonal, pin_zero, pin_special_coefficients, pin_cubic_polar, pin_invariances,
     pin_tile_permutation, pin_single_tile_is_full_map, pin_tile_count,
+    pin_step_constant_gradient, pin_step_nesterov_sign, pin_step_scale_branch,
 ]
 
 

@@ -29,6 +29,15 @@ MUTATIONS = [
     ("floor_tile_count", "    int64_t R = (H + T - 1) / T, C = (W + T - 1) / T;\n    int status",
      "    int64_t R = H / T, C = W / T;\n    int status"),
     ("zero_tile_not_zero", "if (nrm == 0.0) {", "if (nrm < 0.0) {"),
+    ("step_momentum_no_beta", "Mt[i] = beta * Mt[i] + G[i];", "Mt[i] = Mt[i] + G[i];"),
+    ("step_nesterov_old_buffer",
+     "Mt[i] = beta * Mt[i] + G[i];\n        Ghat[i] = nesterov ? G[i] + beta * Mt[i] : Mt[i];",
+     "Ghat[i] = nesterov ? G[i] + beta * Mt[i] : beta * Mt[i] + G[i];\n        Mt[i] = beta * Mt[i] + G[i];"),
+    ("step_nesterov_flag_flipped", "nesterov ? G[i] + beta * Mt[i] : Mt[i]", "nesterov ? Mt[i] : G[i] + beta * Mt[i]"),
+    ("step_tau_no_sqrt", "sqrt((double)(full ? big : T))", "(double)(full ? big : T)"),
+    ("step_branch_on_min", "int64_t big = H > W ? H : W;", "int64_t big = H < W ? H : W;"),
+    ("step_decay_sign", "(1.0 - lr * lambda) * Wt[i]", "(1.0 + lr * lambda) * Wt[i]"),
+    ("step_update_sign", "Wt[i] - lr * tau * U[i]", "Wt[i] + lr * tau * U[i]"),
 ]
 
 

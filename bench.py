@@ -184,6 +184,80 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
     print(json.dumps(rec), flush=True)
 
 
+def bench_optstep(args, hm, torch, np, dev):
+    """The optimizer-step benchmark of Sec. 5 (cross-layer batching): 8
+    stacked bias-free Linear(H, H) layers in bf16, fresh Gaussian gradients
+    before every step (outside the timed region), HiMuon with T = 512, K = 5
+    against full-matrix Muon (T = 0: the same Alg. 1 step with Phi_K of the
+    whole matrix), each as one call per layer and as one batched call over
+    all layers. Per-step time is the median of the HIP-event times of
+    `--steps` steps after `--warmup` (the paper: 50 after 20); peak memory
+    is torch's peak allocation over the variant's run, workspace included."""
+    coeffs = tuple(float(np.float32(v)) for v in hm.QUINTIC)
+    hs = [int(h) for h in args.hidden.split(",")]
+    stream = torch.cuda.current_stream(dev)
+    out = {}
+    for H in hs:
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(H)
+        Ws = [(torch.randn(H, H, device=dev, generator=gen) * 0.02).to(torch.bfloat16) for _ in range(8)]
+        Gs = [torch.empty(H, H, dtype=torch.bfloat16, device=dev) for _ in range(8)]
+        res = {}
+        for name, T, batched in [("muon_full_per_layer", 0, False), ("muon_full_batched", 0, True),
+                                 ("himuon_T512_per_layer", 512, False), ("himuon_T512_batched", 512, True)]:
+            Ms = [torch.zeros_like(w) for w in Ws]
+            torch.cuda.synchronize()
+            torch.cuda.reset_peak_memory_stats(dev)
+            groups = [list(range(8))] if batched else [[i] for i in range(8)]
+            opts = [hm.HiMuon([Ws[i] for i in g], T=T, K=5, coeffs=coeffs, lr=0.02, momentum=0.95,
+                              weight_decay=0.0, nesterov=True, scale_c=0.2) for g in groups]
+            for o, g in zip(opts, groups):
+                o.moms = [Ms[i] for i in g]
+            ws_bytes = sum(o._workspace.numel() for o in opts)
+
+            def one_step():
+                for o, g in zip(opts, groups):
+                    o.step([Gs[i] for i in g], stream=stream)
+
+            times = []
+            for it in range(args.warmup + args.steps):
+                for g in Gs:
+                    g.normal_(generator=gen)
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                one_step()
+                b.record(stream)
+                if it >= args.warmup:
+                    times.append((a, b))
+            torch.cuda.synchronize()
+            ms = np.array([a.elapsed_time(b) for a, b in times])
+            flops = 8 * (6.0 * H * H * 512 * 5 if T else 6.0 * H ** 3 * 5)
+            res[name] = {"median_ms": round(float(np.median(ms)), 4),
+                         "iqr_ms": round(float(np.percentile(ms, 75) - np.percentile(ms, 25)), 4),
+                         "ns_tflops": round(flops / (float(np.median(ms)) * 1e-3) / 1e12, 2),
+                         "peak_mem_MiB": round(torch.cuda.max_memory_allocated(dev) / 2 ** 20, 1),
+                         "workspace_MiB": round(ws_bytes / 2 ** 20, 1)}
+            log(f"H={H} {name}: {res[name]}")
+            del opts
+        base = res["muon_full_per_layer"]["median_ms"]
+        for name in res:
+            res[name]["speedup_vs_full_per_layer"] = round(base / res[name]["median_ms"], 3)
+        out[str(H)] = res
+        del Ws, Gs
+        torch.cuda.empty_cache()
+    h_last = str(hs[-1])
+    rec = {
+        "metric": "optimizer-step time, 8 x Linear(H,H) bf16, HiMuon T=512 K=5 (batched) [ms]",
+        "value": out[h_last]["himuon_T512_batched"]["median_ms"], "unit": "ms", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"8 x Linear({h_last},{h_last}) bf16, fresh N(0,1) gradients each step",
+                   "T": 512, "K": 5, "momentum": 0.95, "nesterov": True, "scale_c": 0.2},
+        "results": out,
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,6 +273,9 @@ def main():
     ap.add_argument("--path", default="tiled", choices=["tiled", "gemm"],
                     help="tiled: the fused per-tile kernels (T <= 256); gemm: himuon_ns_gemm, whole matrices "
                          "(--T 0) or large tiles (e.g. --T 512) through batched library GEMMs")
+    ap.add_argument("--optstep", action="store_true",
+                    help="run the optimizer-step benchmark (8 x Linear(H,H), HiMuon T=512 vs full Muon) instead")
+    ap.add_argument("--hidden", default="1024,2048,4096", help="H values of --optstep")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB per launch (counter calibration)")
     args = ap.parse_args()
@@ -224,6 +301,9 @@ def main():
         torch.cuda.synchronize()
         log(f"copied {args.calib_copy_mib} MiB x {args.warmup + args.steps}")
         return
+
+    if args.optstep:
+        return bench_optstep(args, hm, torch, np, dev)
 
     coeffs = tuple(float(np.float32(v)) for v in hm.QUINTIC)
     compute = {"default": hm.COMPUTE_DEFAULT, "f16": hm.COMPUTE_F16, "bf16": hm.COMPUTE_BF16,

@@ -127,6 +127,8 @@ int himuon_ns_tiled(int64_t n_mats,
  * T >= 1: Phi_{K,T}, eq. (tiled_ns), with each T x T tile a problem of its
  *        own; meant for tiles too large to stay on one compute unit
  *        (T = 512 is the multi-kernel tile of Sec. 4.4.1), but any T works.
+ *        A matrix with T >= max(H, W) is one whole problem as for T = 0
+ *        (its single padded tile has the same Phi_K, Sec. 4.4.3).
  * Problems of equal shape are batched; each step of eq. (ns_iteration) is
  * three batched GEMMs (A = X X^T, B = bA + cA^2, X <- aX + BX) with fp32
  * accumulation. Operands are fp32 for fp32 storage; for bf16 storage fp16
@@ -164,6 +166,56 @@ int himuon_ns_gemm(int64_t n_mats,
                    void* workspace, size_t workspace_bytes,
                    size_t chunk_budget_bytes,
                    void* stream);
+
+/*
+ * One HiMuon optimizer step (Alg. 1) on n_mats parameter matrices, in place:
+ *
+ *   M_l <- beta M_l + G_l                            eq. (muon_momentum)
+ *   Ghat = G_l + beta M_l  (nesterov != 0, eq. muon_lookahead), else M_l
+ *   U    = Phi_K(Ghat)      if T = 0 (T = infinity) or T >= max(H_l, W_l),
+ *          Phi_{K,T}(Ghat)  otherwise                 eq. (tiled_ns)
+ *   W_l <- (1 - lr weight_decay) W_l - lr tau_l U     eq. (scaled_update)
+ *   tau_l = scale_c sqrt(max(H_l, W_l)) on the full branch, scale_c sqrt(T)
+ *           when tiled (Sec. 4.3; the paper's runs use scale_c = 0.2).
+ *
+ * weights[l], grads[l], moms[l]  device pointers, storage `dtype`, one
+ *                          row-major layout (leading dimension ld[l]; ld may
+ *                          be NULL for contiguous rows). W and M are updated in
+ *                          place; G is only read. The three must not overlap
+ *                          (equal pointers are rejected). The new M is stored
+ *                          rounded to `dtype`, and the lookahead is formed from
+ *                          the stored value.
+ * T, K, a, b, c            as himuon_ns_gemm: T = 0 or any positive tile size.
+ *                          T in {32, 64, 128, 256} runs the fused tile kernels
+ *                          (an element-wise prologue and epilogue around the
+ *                          tiled map, with the lookahead held in `dtype` in the
+ *                          workspace); any other T runs the library-GEMM path
+ *                          with the momentum fused into its gather and the
+ *                          update into its scatter.
+ * lr, momentum, weight_decay, nesterov, scale_c   the step's scalars (finite).
+ * workspace                device memory of at least himuon_step_workspace_size
+ *                          (same arguments) bytes, owned by the caller.
+ * chunk_budget_bytes       fused tile sizes: bound on the lookahead buffers of
+ *                          one group of consecutive matrices (0: one group);
+ *                          other T: as himuon_ns_gemm.
+ *
+ * Errors as himuon_ns_gemm; nothing is enqueued when one is returned.
+ * Matrices with non-finite gradients or momenta give non-finite weights
+ * only within their own problems (tiles or whole matrix).
+ */
+size_t himuon_step_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T,
+                                  int dtype, int compute, int K, float a, float b, float c,
+                                  size_t chunk_budget_bytes);
+
+int himuon_step(int64_t n_mats,
+                void* const* weights, const void* const* grads, void* const* moms,
+                const int64_t* rows, const int64_t* cols, const int64_t* ld,
+                int T, int K, float a, float b, float c,
+                float lr, float momentum, float weight_decay, int nesterov, float scale_c,
+                int dtype, int compute,
+                void* workspace, size_t workspace_bytes,
+                size_t chunk_budget_bytes,
+                void* stream);
 
 /*
  * Host-only planner (no HIP call): the tiles and chunks himuon_ns_tiled

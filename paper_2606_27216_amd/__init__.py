@@ -59,6 +59,12 @@ def lib():
         L.himuon_ns_gemm_workspace_size.restype = sz
         L.himuon_ns_gemm.argtypes = L.himuon_ns_tiled.argtypes
         L.himuon_ns_gemm.restype = ctypes.c_int
+        L.himuon_step_workspace_size.argtypes = L.himuon_ns_gemm_workspace_size.argtypes
+        L.himuon_step_workspace_size.restype = sz
+        f = ctypes.c_float
+        L.himuon_step.argtypes = [i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, f, f, f,
+                                  f, f, f, ctypes.c_int, f, ctypes.c_int, ctypes.c_int, vp, sz, sz, vp]
+        L.himuon_step.restype = ctypes.c_int
         L.himuon_plan_chunks.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, sz, vp, vp, vp, i64]
         L.himuon_plan_chunks.restype = ctypes.c_int
         L.himuon_select_compute.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -119,6 +125,24 @@ def himuon_ns_gemm(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a
         int(T), int(K), float(a), float(b), float(c), int(dtype), int(compute),
         int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes),
         int(stream) if stream else None))
+
+
+def himuon_step_workspace_size(rows, cols, T, dtype, compute, K, a, b, c, chunk_budget_bytes=0) -> int:
+    """Workspace bytes of a himuon_step call over matrices of these shapes (0 on an invalid plan)."""
+    return int(lib().himuon_step_workspace_size(
+        len(rows), _i64_array(rows), _i64_array(cols), int(T), int(dtype), int(compute), int(K),
+        float(a), float(b), float(c), int(chunk_budget_bytes)))
+
+
+def himuon_step(n_mats, weights, grads, moms, rows, cols, ld, T, K, a, b, c, lr, momentum, weight_decay,
+                nesterov, scale_c, dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream) -> int:
+    """Same arguments as the C function (``ld`` may be None). Returns the status code."""
+    return int(lib().himuon_step(
+        int(n_mats), _ptr_array(weights), _ptr_array(grads), _ptr_array(moms), _i64_array(rows),
+        _i64_array(cols), None if ld is None else _i64_array(ld), int(T), int(K), float(a), float(b),
+        float(c), float(lr), float(momentum), float(weight_decay), int(bool(nesterov)), float(scale_c),
+        int(dtype), int(compute), int(workspace) if workspace else None, int(workspace_bytes),
+        int(chunk_budget_bytes), int(stream) if stream else None))
 
 
 def himuon_plan_chunks(rows, cols, T, dtype=BF16, chunk_budget_bytes=0):
@@ -251,3 +275,87 @@ def ns_gemm(inputs, outputs=None, T=0, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFA
     if st != OK:
         raise HimuonError(st, "himuon_ns_gemm")
     return outputs
+
+
+def step(weights, grads, moms, T=512, K=5, coeffs=QUINTIC, lr=0.02, momentum=0.95, weight_decay=0.0,
+         nesterov=True, scale_c=0.2, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0, workspace=None, stream=None):
+    """One HiMuon optimizer step (Alg. 1) on every matrix, in one library
+    call: ``weights`` and ``moms`` are updated in place from ``grads``. All
+    three are lists of 2-D CUDA tensors of one dtype, matrix l sharing one
+    shape and row stride across the three lists. T = 0 is the full-matrix
+    branch. Returns ``weights``."""
+    import torch
+    weights, grads, moms = list(weights), list(grads), list(moms)
+    if not weights or len(grads) != len(weights) or len(moms) != len(weights):
+        raise ValueError("weights, grads and moms must be equally long, non-empty lists")
+    code = _dtype_code(weights[0])
+    dev = weights[0].device
+    for w, g, m in zip(weights, grads, moms):
+        for x in (w, g, m):
+            if x.dim() != 2 or not x.is_cuda or x.device != dev or _dtype_code(x) != code or x.stride(1) != 1:
+                raise ValueError("matrices must be 2-D row-major CUDA tensors of one dtype on one device")
+        if g.shape != w.shape or m.shape != w.shape or g.stride(0) != w.stride(0) or m.stride(0) != w.stride(0):
+            raise ValueError("W, G and M of a matrix must share shape and row stride")
+    a, b, c = coeffs
+    rows = [w.shape[0] for w in weights]
+    cols = [w.shape[1] for w in weights]
+    need = himuon_step_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
+    if need == 0:
+        raise HimuonError(ERR_INVALID_ARG, "himuon_step_workspace_size")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    st = himuon_step(
+        len(weights), [w.data_ptr() for w in weights], [g.data_ptr() for g in grads], [m.data_ptr() for m in moms],
+        rows, cols, [w.stride(0) for w in weights], T, K, a, b, c, lr, momentum, weight_decay, nesterov, scale_c,
+        code, compute, workspace.data_ptr(), workspace.numel() * workspace.element_size(), chunk_budget_bytes,
+        stream.cuda_stream)
+    if st != OK:
+        raise HimuonError(st, "himuon_step")
+    return weights
+
+
+class HiMuon:
+    """Optimizer state around ``himuon_step`` (Alg. 1): one momentum buffer per
+    matrix (zero at the start, independent of T) and a device workspace
+    cached across steps. ``reconfigure(T)`` changes the tile size at run time
+    (Sec. 4.4.4) and keeps the momentum; T = 0 is the full-matrix branch.
+    Every step is one library call over all matrices (cross-layer batching,
+    Sec. 4.4.2)."""
+
+    def __init__(self, params, T=512, K=5, coeffs=QUINTIC, lr=0.02, momentum=0.95, weight_decay=0.0,
+                 nesterov=True, scale_c=0.2, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0):
+        import torch
+        self.params = list(params)
+        if not self.params:
+            raise ValueError("no parameters")
+        self.moms = [torch.zeros_like(p, memory_format=torch.contiguous_format) for p in self.params]
+        for p, m in zip(self.params, self.moms):
+            if p.dim() != 2 or p.stride(1) != 1 or p.stride(0) != m.stride(0):
+                raise ValueError("parameters must be contiguous 2-D matrices")
+        self.K, self.coeffs, self.lr, self.momentum = K, coeffs, lr, momentum
+        self.weight_decay, self.nesterov, self.scale_c = weight_decay, nesterov, scale_c
+        self.compute, self.chunk_budget_bytes = compute, chunk_budget_bytes
+        self._workspace = None
+        self.reconfigure(T)
+
+    def reconfigure(self, T):
+        """Set the tile size for the following steps; the plan's workspace is
+        sized once here and reused by every step."""
+        import torch
+        a, b, c = self.coeffs
+        code = _dtype_code(self.params[0])
+        need = himuon_step_workspace_size([p.shape[0] for p in self.params], [p.shape[1] for p in self.params],
+                                          T, code, self.compute, self.K, a, b, c, self.chunk_budget_bytes)
+        if need == 0:
+            raise HimuonError(ERR_INVALID_ARG, "himuon_step_workspace_size")
+        if self._workspace is None or self._workspace.numel() < need:
+            self._workspace = torch.empty(need, dtype=torch.uint8, device=self.params[0].device)
+        self.T = T
+
+    def step(self, grads, stream=None):
+        return step(self.params, grads, self.moms, T=self.T, K=self.K, coeffs=self.coeffs, lr=self.lr,
+                    momentum=self.momentum, weight_decay=self.weight_decay, nesterov=self.nesterov,
+                    scale_c=self.scale_c, compute=self.compute, chunk_budget_bytes=self.chunk_budget_bytes,
+                    workspace=self._workspace, stream=stream)

@@ -33,8 +33,10 @@ SOURCES = [
     ("ns_tiled_kernels.hip", []),
     ("ns_tiled_f16.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form"]),
     ("ns_gemm_kernels.hip", []),
+    ("optim_kernels.hip", []),
     ("himuon_api.cpp", []),
     ("ns_gemm_path.cpp", []),
+    ("himuon_step.cpp", []),
 ]
 # The whole-matrix and large-tile path runs its Newton-Schulz GEMMs on hipBLASLt.
 LINK_LIBS = ["-lhipblaslt"]

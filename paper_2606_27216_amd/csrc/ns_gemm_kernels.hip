@@ -10,6 +10,10 @@
 //     Phi_K(0) = 0), with the norm summed in fp64 in a fixed order, so a
 //     result never depends on how problems are grouped into launches;
 //   - B_T^{-1}: the block part of the final iterate back to the matrix.
+// With the optimizer step of Alg. 1 fused in (OPT), the problem's input is
+// the lookahead gradient formed on the fly from G and the momentum M (the
+// norm pass also stores the new M), and the scatter applies the decoupled
+// weight decay and the tau-scaled update to W (eq. scaled_update).
 #include "ns_gemm_path.h"
 
 #include <hip/hip_bf16.h>
@@ -43,6 +47,53 @@ __device__ __forceinline__ void store_elem(void* base, int64_t idx, float v)
     }
 }
 
+template <GemmStore ST>
+__device__ __forceinline__ float load_f32(const void* base, int64_t idx)
+{
+    if constexpr (ST == GemmStore::BF16) {
+        const uint16_t u = static_cast<const uint16_t*>(base)[idx];
+        return __uint_as_float((uint32_t)u << 16);
+    } else {
+        return static_cast<const float*>(base)[idx];
+    }
+}
+
+// The value a store of v leaves in memory, as fp32.
+template <GemmStore ST>
+__device__ __forceinline__ float stored_value(float v)
+{
+    if constexpr (ST == GemmStore::BF16) return (float)(__bf16)v;
+    else return v;
+}
+
+// Eq. (muon_lookahead) or the plain buffer, from G and the stored new M.
+__device__ __forceinline__ float lookahead(float g, float m_new, const OptArgs& o)
+{
+    return o.nesterov ? g + o.beta * m_new : m_new;
+}
+
+// Element `idx` of the problem's input: the matrix itself, or (OPT) the
+// lookahead gradient from G (`in`) and the already updated momentum.
+template <GemmStore ST, bool OPT>
+__device__ __forceinline__ float input_elem(const GemmProb& P, int64_t idx, const OptArgs& o)
+{
+    if constexpr (OPT) return lookahead(load_f32<ST>(P.in, idx), load_f32<ST>(P.mom, idx), o);
+    else return load_f32<ST>(P.in, idx);
+}
+
+// Writes the result u of element `idx`: the plain output, or (OPT) the
+// weight update W <- (1 - lr lambda) W - lr tau u.
+template <GemmStore ST, bool OPT>
+__device__ __forceinline__ void output_elem(const GemmProb& P, int64_t idx, float u, const OptArgs& o)
+{
+    if constexpr (OPT) {
+        const float w = load_f32<ST>(P.out, idx);
+        store_elem<ST>(P.out, idx, o.decay * w - (o.lr * P.tau) * u);
+    } else {
+        store_elem<ST>(P.out, idx, u);
+    }
+}
+
 template <GemmOperand OP> struct OpType;
 template <> struct OpType<GemmOperand::F32> { typedef float T; };
 template <> struct OpType<GemmOperand::F16> { typedef _Float16 T; };
@@ -50,8 +101,12 @@ template <> struct OpType<GemmOperand::BF16> { typedef __bf16 T; };
 
 // Part j of problem p sums the squares of rows [j*rpp, (j+1)*rpp) of its
 // block, each thread over a fixed set of columns, then a fixed-order tree.
-template <GemmStore ST>
-__global__ void __launch_bounds__(kThreads) gemm_norm_partials(const GemmProb* probs, int nparts, double* partial)
+// (OPT: the momentum update M <- beta M + G of every element happens here,
+// once, and the sum is over the lookahead gradient formed from its stored
+// value, exactly as the gather forms it.)
+template <GemmStore ST, bool OPT>
+__global__ void __launch_bounds__(kThreads) gemm_norm_partials(const GemmProb* probs, int nparts, double* partial,
+                                                               const OptArgs o)
 {
     const GemmProb P = probs[blockIdx.y];
     const int rpp = (P.h + nparts - 1) / nparts;
@@ -61,7 +116,15 @@ __global__ void __launch_bounds__(kThreads) gemm_norm_partials(const GemmProb* p
     for (int r = r0; r < r1; ++r) {
         const int64_t rowoff = (P.row0 + r) * P.ld_in + P.col0;
         for (int c = threadIdx.x; c < P.w; c += kThreads) {
-            const double v = load_elem<ST>(P.in, rowoff + c);
+            double v;
+            if constexpr (OPT) {
+                const float g = load_f32<ST>(P.in, rowoff + c);
+                const float m = stored_value<ST>(o.beta * load_f32<ST>(P.mom, rowoff + c) + g);
+                store_elem<ST>(P.mom, rowoff + c, m);
+                v = (double)lookahead(g, m, o);
+            } else {
+                v = load_elem<ST>(P.in, rowoff + c);
+            }
             acc += v * v;
         }
     }
@@ -87,9 +150,9 @@ __global__ void gemm_norm_finalize(int nprob, int nparts, double scale, double* 
     partial[(int64_t)p * nparts] = ss > 0.0 ? scale / sqrt(ss) : 0.0;
 }
 
-template <GemmStore ST, GemmOperand OP>
+template <GemmStore ST, GemmOperand OP, bool OPT>
 __global__ void __launch_bounds__(kThreads) gemm_gather(const GemmProb* probs, int m, int n, int nparts,
-                                                        const double* partial, void* xv)
+                                                        const double* partial, void* xv, const OptArgs o)
 {
     typedef typename OpType<OP>::T OT;
     const int p = blockIdx.y;
@@ -105,7 +168,7 @@ __global__ void __launch_bounds__(kThreads) gemm_gather(const GemmProb* probs, i
             const int i = i0 + ty + 8 * k, j = j0 + tx;
             if (i < m && j < n) {
                 double v = 0.0;
-                if (i < P.h && j < P.w) v = load_elem<ST>(P.in, (P.row0 + i) * P.ld_in + P.col0 + j) * s;
+                if (i < P.h && j < P.w) v = (double)input_elem<ST, OPT>(P, (P.row0 + i) * P.ld_in + P.col0 + j, o) * s;
                 x[(int64_t)i * n + j] = (OT)(float)v;
             }
         }
@@ -116,7 +179,7 @@ __global__ void __launch_bounds__(kThreads) gemm_gather(const GemmProb* probs, i
         for (int k = 0; k < 4; ++k) {
             const int r = j0 + ty + 8 * k, c = i0 + tx;
             double v = 0.0;
-            if (r < P.h && c < P.w) v = load_elem<ST>(P.in, (P.row0 + r) * P.ld_in + P.col0 + c) * s;
+            if (r < P.h && c < P.w) v = (double)input_elem<ST, OPT>(P, (P.row0 + r) * P.ld_in + P.col0 + c, o) * s;
             t[ty + 8 * k][tx] = (float)v;
         }
         __syncthreads();
@@ -128,9 +191,9 @@ __global__ void __launch_bounds__(kThreads) gemm_gather(const GemmProb* probs, i
     }
 }
 
-template <GemmStore ST, GemmOperand OP>
+template <GemmStore ST, GemmOperand OP, bool OPT>
 __global__ void __launch_bounds__(kThreads) gemm_scatter(const GemmProb* probs, int m, int n, float inv_scale,
-                                                         const void* xv)
+                                                         const void* xv, const OptArgs o)
 {
     typedef typename OpType<OP>::T OT;
     const int p = blockIdx.y;
@@ -144,7 +207,7 @@ __global__ void __launch_bounds__(kThreads) gemm_scatter(const GemmProb* probs, 
         for (int k = 0; k < 4; ++k) {
             const int i = i0 + ty + 8 * k, j = j0 + tx;
             if (i < P.h && j < P.w)
-                store_elem<ST>(P.out, (P.row0 + i) * P.ld_out + P.col0 + j, (float)x[(int64_t)i * n + j] * inv_scale);
+                output_elem<ST, OPT>(P, (P.row0 + i) * P.ld_out + P.col0 + j, (float)x[(int64_t)i * n + j] * inv_scale, o);
         }
     } else {
         __shared__ float t[32][33];
@@ -158,7 +221,7 @@ __global__ void __launch_bounds__(kThreads) gemm_scatter(const GemmProb* probs, 
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int r = j0 + ty + 8 * k, c = i0 + tx;
-            if (r < P.h && c < P.w) store_elem<ST>(P.out, (P.row0 + r) * P.ld_out + P.col0 + c, t[tx][ty + 8 * k]);
+            if (r < P.h && c < P.w) output_elem<ST, OPT>(P, (P.row0 + r) * P.ld_out + P.col0 + c, t[tx][ty + 8 * k], o);
         }
     }
 }
@@ -171,19 +234,27 @@ dim3 tile_grid(int m, int n, int nprob)
 }  // namespace
 
 hipError_t launch_gemm_norm_partials(GemmStore st, const GemmProb* probs, int nprob, int nparts, double* partial,
-                                     hipStream_t stream)
+                                     const OptArgs* opt, hipStream_t stream)
 {
     if (nprob <= 0) return hipSuccess;
     const dim3 grid((unsigned)nparts, (unsigned)nprob, 1);
-    if (st == GemmStore::BF16)
-        hipLaunchKernelGGL(gemm_norm_partials<GemmStore::BF16>, grid, dim3(kThreads), 0, stream, probs, nparts, partial);
-    else
-        hipLaunchKernelGGL(gemm_norm_partials<GemmStore::F32>, grid, dim3(kThreads), 0, stream, probs, nparts, partial);
+    const OptArgs o = opt ? *opt : OptArgs{};
+#define HM_NORM(S, F) \
+    hipLaunchKernelGGL((gemm_norm_partials<S, F>), grid, dim3(kThreads), 0, stream, probs, nparts, partial, o)
+    if (st == GemmStore::BF16) {
+        if (opt) HM_NORM(GemmStore::BF16, true);
+        else HM_NORM(GemmStore::BF16, false);
+    } else {
+        if (opt) HM_NORM(GemmStore::F32, true);
+        else HM_NORM(GemmStore::F32, false);
+    }
+#undef HM_NORM
     return hipGetLastError();
 }
 
 hipError_t launch_gemm_gather(GemmStore st, GemmOperand op, const GemmProb* probs, int nprob, int m, int n,
-                              int nparts, const double* partial, double scale, void* x, hipStream_t stream)
+                              int nparts, const double* partial, double scale, void* x, const OptArgs* opt,
+                              hipStream_t stream)
 {
     if (nprob <= 0) return hipSuccess;
     hipLaunchKernelGGL(gemm_norm_finalize, dim3((unsigned)((nprob + 255) / 256)), dim3(256), 0, stream, nprob, nparts,
@@ -191,8 +262,16 @@ hipError_t launch_gemm_gather(GemmStore st, GemmOperand op, const GemmProb* prob
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const dim3 grid = tile_grid(m, n, nprob);
-#define HM_GATHER(S, O) \
-    hipLaunchKernelGGL((gemm_gather<S, O>), grid, dim3(kThreads), 0, stream, probs, m, n, nparts, partial, x)
+    const OptArgs o = opt ? *opt : OptArgs{};
+#define HM_GATHER(S, O)                                                                                              \
+    do {                                                                                                             \
+        if (opt)                                                                                                     \
+            hipLaunchKernelGGL((gemm_gather<S, O, true>), grid, dim3(kThreads), 0, stream, probs, m, n, nparts,      \
+                               partial, x, o);                                                                       \
+        else                                                                                                         \
+            hipLaunchKernelGGL((gemm_gather<S, O, false>), grid, dim3(kThreads), 0, stream, probs, m, n, nparts,     \
+                               partial, x, o);                                                                       \
+    } while (0)
     if (st == GemmStore::F32 && op == GemmOperand::F32) HM_GATHER(GemmStore::F32, GemmOperand::F32);
     else if (st == GemmStore::BF16 && op == GemmOperand::F16) HM_GATHER(GemmStore::BF16, GemmOperand::F16);
     else if (st == GemmStore::BF16 && op == GemmOperand::BF16) HM_GATHER(GemmStore::BF16, GemmOperand::BF16);
@@ -202,12 +281,20 @@ hipError_t launch_gemm_gather(GemmStore st, GemmOperand op, const GemmProb* prob
 }
 
 hipError_t launch_gemm_scatter(GemmStore st, GemmOperand op, const GemmProb* probs, int nprob, int m, int n,
-                               float inv_scale, const void* x, hipStream_t stream)
+                               float inv_scale, const void* x, const OptArgs* opt, hipStream_t stream)
 {
     if (nprob <= 0) return hipSuccess;
     const dim3 grid = tile_grid(m, n, nprob);
-#define HM_SCATTER(S, O) \
-    hipLaunchKernelGGL((gemm_scatter<S, O>), grid, dim3(kThreads), 0, stream, probs, m, n, inv_scale, x)
+    const OptArgs o = opt ? *opt : OptArgs{};
+#define HM_SCATTER(S, O)                                                                                             \
+    do {                                                                                                             \
+        if (opt)                                                                                                     \
+            hipLaunchKernelGGL((gemm_scatter<S, O, true>), grid, dim3(kThreads), 0, stream, probs, m, n, inv_scale,  \
+                               x, o);                                                                                \
+        else                                                                                                         \
+            hipLaunchKernelGGL((gemm_scatter<S, O, false>), grid, dim3(kThreads), 0, stream, probs, m, n, inv_scale, \
+                               x, o);                                                                                \
+    } while (0)
     if (st == GemmStore::F32 && op == GemmOperand::F32) HM_SCATTER(GemmStore::F32, GemmOperand::F32);
     else if (st == GemmStore::BF16 && op == GemmOperand::F16) HM_SCATTER(GemmStore::BF16, GemmOperand::F16);
     else if (st == GemmStore::BF16 && op == GemmOperand::BF16) HM_SCATTER(GemmStore::BF16, GemmOperand::BF16);

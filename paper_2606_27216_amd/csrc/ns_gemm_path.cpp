@@ -63,9 +63,15 @@ struct Group {
 
 int group_nparts(int n) { return (int)std::min<int64_t>(256, std::max<int64_t>(1, ceil_div(n, 64))); }
 
+// A matrix is one whole problem when T = 0 (the branch T = infinity) or
+// T >= max(H, W): the tiling operator then gives a single padded tile, and
+// Phi_K of a zero-padded matrix is the padded Phi_K of the matrix (Sec.
+// 4.4.3), so the smaller unpadded problem is worked on instead.
+bool whole_matrix(int64_t rows, int64_t cols, int T) { return T == 0 || T >= std::max(rows, cols); }
+
 // Groups (in order of first appearance) and, when `probs` is given, the
-// problem list in group order. T = 0: one problem per matrix; T >= 1: the
-// R x C tiles of every matrix, row-major.
+// problem list in group order. Whole matrices: one problem each; otherwise
+// the R x C tiles of the matrix, row-major.
 int plan_groups(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, std::vector<Group>& groups,
                 std::vector<std::vector<int64_t>>* members)
 {
@@ -76,7 +82,7 @@ int plan_groups(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T,
     for (int64_t l = 0; l < n_mats; ++l) {
         if (rows[l] < 1 || cols[l] < 1) return HIMUON_ERR_INVALID_ARG;
         int64_t m, n, cnt;
-        if (T == 0) {
+        if (whole_matrix(rows[l], cols[l], T)) {
             m = std::min(rows[l], cols[l]);
             n = std::max(rows[l], cols[l]);
             cnt = 1;
@@ -261,27 +267,13 @@ int run_gemm(hipblasLtHandle_t h, const Gemm& g, float alpha, const void* A, con
 
 }  // namespace
 
-extern "C" {
+namespace himuon {
 
-size_t himuon_ns_gemm_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
-                                     int compute, int K, float a, float b, float c, size_t chunk_budget_bytes)
-{
-    std::vector<Group> groups;
-    if (plan_groups(n_mats, rows, cols, T, groups, nullptr) != HIMUON_OK) return 0;
-    int m_max = 0;
-    for (const Group& g : groups) m_max = std::max(m_max, g.m);
-    GemmOperand op;
-    if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return 0;
-    if (resolve_operand(dtype, compute, K, a, b, c, m_max, &op) != HIMUON_OK) return 0;
-    size_t ws = 0;
-    if (plan_chunks(groups, op, chunk_budget_bytes, &ws) != HIMUON_OK) return 0;
-    return ws;
-}
-
-int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
-                   const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
-                   float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
-                   size_t chunk_budget_bytes, void* stream)
+int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, void* const* mom_ptrs,
+                  const float* tau, const int64_t* rows, const int64_t* cols, const int64_t* ld_in,
+                  const int64_t* ld_out, int T, int K, float a, float b, float c, int dtype, int compute,
+                  void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes, void* stream,
+                  const OptArgs* opt)
 {
     // ---- validation and plan: nothing is enqueued unless every check passes
     if (n_mats < 1 || n_mats > INT32_MAX || !in_ptrs || !out_ptrs || !rows || !cols) return HIMUON_ERR_INVALID_ARG;
@@ -290,6 +282,7 @@ int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_
     if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
     for (int64_t l = 0; l < n_mats; ++l) {
         if (!in_ptrs[l] || !out_ptrs[l] || rows[l] < 1 || cols[l] < 1) return HIMUON_ERR_INVALID_ARG;
+        if (opt && (!mom_ptrs || !mom_ptrs[l] || !tau || !isfinite(tau[l]))) return HIMUON_ERR_INVALID_ARG;
         const int64_t li = ld_in ? ld_in[l] : cols[l];
         const int64_t lo = ld_out ? ld_out[l] : cols[l];
         if (li < cols[l] || lo < cols[l]) return HIMUON_ERR_INVALID_ARG;
@@ -323,7 +316,9 @@ int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_
             p.out = out_ptrs[l];
             p.ld_in = ld_in ? ld_in[l] : cols[l];
             p.ld_out = ld_out ? ld_out[l] : cols[l];
-            if (T == 0) {
+            p.mom = opt ? mom_ptrs[l] : nullptr;
+            p.tau = opt ? tau[l] : 0.f;
+            if (whole_matrix(rows[l], cols[l], T)) {
                 p.row0 = p.col0 = 0;
                 p.h = (int32_t)rows[l];
                 p.w = (int32_t)cols[l];
@@ -331,13 +326,13 @@ int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_
                 probs.push_back(p);
             } else {
                 const int64_t R = ceil_div(rows[l], T), C = ceil_div(cols[l], T);
+                p.trans = 0;
                 for (int64_t r = 0; r < R; ++r)
                     for (int64_t q = 0; q < C; ++q) {
                         p.row0 = r * T;
                         p.col0 = q * T;
                         p.h = (int32_t)std::min<int64_t>(T, rows[l] - r * T);
                         p.w = (int32_t)std::min<int64_t>(T, cols[l] - q * T);
-                        p.trans = 0;
                         probs.push_back(p);
                     }
             }
@@ -398,8 +393,9 @@ int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_
             const Plan* pl = nullptr;
             status = get_plan(dev, g.m, g.n, np, op, &lt, &pl);
             if (status != HIMUON_OK) break;
-            if ((e = himuon::launch_gemm_norm_partials(sto, tp, np, g.nparts, partial, hs)) != hipSuccess ||
-                (e = himuon::launch_gemm_gather(sto, op, tp, np, g.m, g.n, g.nparts, partial, s, X[0], hs)) != hipSuccess) {
+            if ((e = himuon::launch_gemm_norm_partials(sto, tp, np, g.nparts, partial, opt, hs)) != hipSuccess ||
+                (e = himuon::launch_gemm_gather(sto, op, tp, np, g.m, g.n, g.nparts, partial, s, X[0], opt, hs)) !=
+                    hipSuccess) {
                 status = himuon::set_hip_error(e);
                 break;
             }
@@ -413,12 +409,47 @@ int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_
                 cur_x ^= 1;
             }
             if (status == HIMUON_OK &&
-                (e = himuon::launch_gemm_scatter(sto, op, tp, np, g.m, g.n, (float)(1.0 / s), X[cur_x], hs)) != hipSuccess)
+                (e = himuon::launch_gemm_scatter(sto, op, tp, np, g.m, g.n, (float)(1.0 / s), X[cur_x], opt, hs)) !=
+                    hipSuccess)
                 status = himuon::set_hip_error(e);
         }
     }
     if (dev != cur) (void)hipSetDevice(cur);
     return status;
+}
+
+size_t gemm_path_workspace(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype, int compute,
+                           int K, float a, float b, float c, size_t chunk_budget_bytes)
+{
+    std::vector<Group> groups;
+    if (plan_groups(n_mats, rows, cols, T, groups, nullptr) != HIMUON_OK) return 0;
+    int m_max = 0;
+    for (const Group& g : groups) m_max = std::max(m_max, g.m);
+    GemmOperand op;
+    if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return 0;
+    if (resolve_operand(dtype, compute, K, a, b, c, m_max, &op) != HIMUON_OK) return 0;
+    size_t ws = 0;
+    if (plan_chunks(groups, op, chunk_budget_bytes, &ws) != HIMUON_OK) return 0;
+    return ws;
+}
+
+}  // namespace himuon
+
+extern "C" {
+
+size_t himuon_ns_gemm_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
+                                     int compute, int K, float a, float b, float c, size_t chunk_budget_bytes)
+{
+    return himuon::gemm_path_workspace(n_mats, rows, cols, T, dtype, compute, K, a, b, c, chunk_budget_bytes);
+}
+
+int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+                   const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
+                   float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
+                   size_t chunk_budget_bytes, void* stream)
+{
+    return himuon::run_gemm_path(n_mats, in_ptrs, out_ptrs, nullptr, nullptr, rows, cols, ld_in, ld_out, T, K, a, b, c,
+                                 dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream, nullptr);
 }
 
 }  // extern "C"

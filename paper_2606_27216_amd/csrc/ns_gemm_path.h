@@ -21,9 +21,23 @@ struct alignas(64) GemmProb {
     int64_t row0, col0;  // origin of the block in the matrix
     int32_t h, w;        // block rows, columns (in the matrix's orientation)
     int32_t trans;
-    int32_t pad_;
+    float tau;           // optimizer step: the update scale tau of the block's matrix
+    void* mom;           // optimizer step: the momentum buffer (layout of `in`)
+    int64_t pad_[7];
 };
-static_assert(sizeof(GemmProb) == 64, "problem descriptor layout");
+static_assert(sizeof(GemmProb) == 128, "problem descriptor layout");
+
+// The optimizer step of Alg. 1 fused into the gather and scatter kernels:
+// `in` holds the gradient G, `mom` the momentum M and `out` the weights W.
+// The gather stores M <- beta M + G (rounded to the storage type) and takes
+// the problem's input as G + beta M (Nesterov) or M; the scatter stores
+// W <- (1 - lr lambda) W - lr tau U, eq. (scaled_update).
+struct OptArgs {
+    float beta;
+    float decay;  // 1 - lr * lambda
+    float lr;
+    int32_t nesterov;
+};
 
 // Element types: storage (what the caller's matrices hold) and the GEMM
 // operand type of the iterate.
@@ -33,16 +47,28 @@ enum class GemmOperand : int { F32 = 1, F16 = 2, BF16 = 3 };
 // Partial sums of squares, fp64: part j of problem p covers a fixed slice
 // of its h x w block; result at partial[p * nparts + j].
 hipError_t launch_gemm_norm_partials(GemmStore st, const GemmProb* probs, int nprob, int nparts,
-                                     double* partial, hipStream_t stream);
+                                     double* partial, const OptArgs* opt, hipStream_t stream);
 
 // X0 = scale * B / ||B||_F (zero when the block is zero) as the m x n
 // row-major iterate of each problem, stride m * n elements.
 hipError_t launch_gemm_gather(GemmStore st, GemmOperand op, const GemmProb* probs, int nprob, int m, int n,
-                              int nparts, const double* partial, double scale, void* x, hipStream_t stream);
+                              int nparts, const double* partial, double scale, void* x, const OptArgs* opt,
+                              hipStream_t stream);
 
 // Output block = inv_scale * (the block's part of the iterate), rounded to
 // the storage type (nearest even for bf16).
 hipError_t launch_gemm_scatter(GemmStore st, GemmOperand op, const GemmProb* probs, int nprob, int m, int n,
-                               float inv_scale, const void* x, hipStream_t stream);
+                               float inv_scale, const void* x, const OptArgs* opt, hipStream_t stream);
+
+// Core of himuon_ns_gemm and of the optimizer step on the GEMM path (`opt`
+// null: Phi of `in` into `out`). Returns a himuon status.
+int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, void* const* mom_ptrs,
+                  const float* tau, const int64_t* rows, const int64_t* cols, const int64_t* ld_in,
+                  const int64_t* ld_out, int T, int K, float a, float b, float c, int dtype, int compute,
+                  void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes, void* stream,
+                  const OptArgs* opt);
+// Workspace of run_gemm_path (0 when the call has no plan).
+size_t gemm_path_workspace(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype, int compute,
+                           int K, float a, float b, float c, size_t chunk_budget_bytes);
 
 }  // namespace himuon

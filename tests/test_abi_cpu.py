@@ -200,3 +200,56 @@ def _gcall(**kw):
 ])
 def test_gemm_validation_rejects_before_any_hip_call(kw, status):
     assert _gcall(**kw) == status
+
+
+# ---- the optimizer step (himuon_step): sizing and validation, no HIP call
+
+def test_step_workspace_size():
+    a, b, c = hm.QUINTIC
+    ws = lambda rows, cols, T, dtype=hm.BF16, budget=0: \
+        hm.himuon_step_workspace_size(rows, cols, T, dtype, hm.COMPUTE_DEFAULT, 5, a, b, c, budget)
+    gemm = lambda rows, cols, T, dtype=hm.BF16, budget=0: \
+        hm.himuon_ns_gemm_workspace_size(rows, cols, T, dtype, hm.COMPUTE_DEFAULT, 5, a, b, c, budget)
+    # T = 512 and T = 0 run the library-GEMM path: the same plan as himuon_ns_gemm
+    assert ws([1024] * 8, [1024] * 8, 512) == gemm([1024] * 8, [1024] * 8, 512)
+    assert ws([300], [500], 0, hm.F32) == gemm([300], [500], 0, hm.F32)
+    # fused tile sizes: the lookahead buffers of all matrices plus two descriptor tables
+    need = ws([1024] * 8, [1024] * 8, 128)
+    assert need >= 8 * 1024 * 1024 * 2 and need < 8 * 1024 * 1024 * 2 + 4096
+    # a budget groups matrices; one matrix above it has no plan
+    assert ws([1024] * 8, [1024] * 8, 128, budget=2 * 1024 * 1024 * 2) < need
+    assert ws([1024] * 8, [1024] * 8, 128, budget=1024 * 1024 * 2 - 1) == 0
+    assert ws([0], [64], 128) == 0
+    assert ws([64], [64], -1) == 0
+
+
+def _scall(**kw):
+    args = dict(n_mats=1, weights=[FAKE], grads=[FAKE + 4096], moms=[FAKE + 8192], rows=[64], cols=[64], ld=None,
+                T=128, K=5, a=3.4445, b=-4.775, c=2.0315, lr=0.02, momentum=0.95, weight_decay=0.0, nesterov=True,
+                scale_c=0.2, dtype=hm.BF16, compute=hm.COMPUTE_DEFAULT, workspace=FAKE, workspace_bytes=256,
+                chunk_budget_bytes=0, stream=None)
+    args.update(kw)
+    return hm.himuon_step(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(weights=[0]), hm.ERR_INVALID_ARG),
+    (dict(moms=[0]), hm.ERR_INVALID_ARG),
+    (dict(grads=[FAKE]), hm.ERR_INVALID_ARG),       # G aliases W
+    (dict(moms=[FAKE + 4096]), hm.ERR_INVALID_ARG),  # M aliases G
+    (dict(rows=[0]), hm.ERR_INVALID_ARG),
+    (dict(ld=[63]), hm.ERR_INVALID_ARG),
+    (dict(T=-1), hm.ERR_INVALID_ARG),
+    (dict(K=-1), hm.ERR_INVALID_ARG),
+    (dict(lr=float("inf")), hm.ERR_INVALID_ARG),
+    (dict(momentum=float("nan")), hm.ERR_INVALID_ARG),
+    (dict(scale_c=float("nan")), hm.ERR_INVALID_ARG),
+    (dict(dtype=7), hm.ERR_INVALID_ARG),
+    (dict(T=0, dtype=hm.F32, compute=hm.COMPUTE_BF16), hm.ERR_UNSUPPORTED),
+    (dict(T=0, compute=hm.COMPUTE_F16, a=50.0, b=0.0, c=0.0), hm.ERR_RANGE),
+    (dict(workspace=0), hm.ERR_WORKSPACE),              # fused route: buffers do not fit
+    (dict(T=512, workspace_bytes=1 << 20), hm.ERR_WORKSPACE),  # GEMM route
+    (dict(chunk_budget_bytes=100), hm.ERR_WORKSPACE),
+])
+def test_step_validation_rejects_before_any_hip_call(kw, status):
+    assert _scall(**kw) == status

@@ -1,0 +1,206 @@
+"""The optimizer step (himuon_step, Alg. 1) against the fp64 oracle's step.
+
+Both routes are covered: the library-GEMM path (T = 0, the full-matrix
+branch, and T = 512) with the momentum fused into its gather and the update
+into its scatter, and the fused tile kernels (T = 128, 32) with element-wise
+prologue and epilogue. Bars:
+  - momentum M: each element within one unit in the last place of the
+    storage type of the oracle's value (the GPU rounds beta M + G once to
+    storage; the oracle keeps fp64);
+  - weights W: per tile, ||W_gpu - W_ref|| <= tol * ||lr tau U_ref|| +
+    u * ||W_ref||, with tol the tiled map's bar (1e-5 fp32, 2e-2 bf16) on the
+    direction and u the storage type's unit roundoff (2^-24, 2^-8) for the
+    final rounding of W;
+  - the direction itself, read back as (W_gpu - (1 - lr lambda) W) / (-lr tau)
+    with W = 0, per tile within the tiled map's bar.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_27216_amd as hm
+from parity import COEF32, TOL, tile_errors, to_f64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+UNIT = {torch.float32: 2.0 ** -24, torch.bfloat16: 2.0 ** -8}
+ULP = {torch.float32: 2.0 ** -23, torch.bfloat16: 2.0 ** -7}
+
+
+def announce(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def rand(shape, dtype, seed, scale=1.0):
+    g = np.random.default_rng(seed)
+    x = g.standard_normal(shape) * scale
+    return torch.tensor(x, dtype=torch.float32).to(dtype).to(DEV)
+
+
+def f32(v):
+    return float(np.float32(v))
+
+
+def tau_of(H, W, T, sc):
+    full = T == 0 or T >= max(H, W)
+    return f32(sc) * np.sqrt(max(H, W) if full else T)
+
+
+def check_step(W0, G, M0, W1, M1, T, dtype, lr, beta, wd, nesterov, sc, K=5, tile=None):
+    """W0, G, M0: the inputs (device); W1, M1: the GPU's results."""
+    Wr, Mr, Ur = oracle.himuon_step(to_f64(W0), to_f64(M0), to_f64(G), T, K, *COEF32, f32(lr), f32(beta), f32(wd),
+                                    nesterov, f32(sc))
+    m = to_f64(M1)
+    # one rounding to storage, after fp32 arithmetic on beta M and G
+    slack = 2.0 ** -22 * (f32(beta) * np.abs(to_f64(M0)) + np.abs(to_f64(G)))
+    assert np.all(np.abs(m - Mr) <= ULP[dtype] * np.abs(Mr) + slack), \
+        f"momentum off by more than one ulp: {np.max(np.abs(m - Mr) / (np.abs(Mr) + 1e-30)):.3e}"
+    H, Wd = Wr.shape
+    t = tile or (max(H, Wd) if T == 0 or T >= max(H, Wd) else T)
+    upd = f32(lr) * tau_of(H, Wd, T, sc) * Ur
+    w = to_f64(W1)
+    worst = 0.0
+    for r0 in range(0, H, t):
+        for c0 in range(0, Wd, t):
+            sl = np.s_[r0:r0 + t, c0:c0 + t]
+            bound = TOL[dtype] * np.linalg.norm(upd[sl]) + UNIT[dtype] * np.linalg.norm(Wr[sl])
+            err = np.linalg.norm(w[sl] - Wr[sl])
+            assert err <= bound, f"tile ({r0},{c0}): |dW| {err:.3e} > {bound:.3e}"
+            worst = max(worst, err / max(bound, 1e-300))
+    return worst
+
+
+def run_step(Ws, Gs, Ms, T, dtype, lr=0.02, beta=0.95, wd=0.1, nesterov=True, sc=0.2, budget=0):
+    hm.step(Ws, Gs, Ms, T=T, K=5, coeffs=COEF32, lr=lr, momentum=beta, weight_decay=wd, nesterov=nesterov,
+            scale_c=sc, chunk_budget_bytes=budget)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("T", [512, 0])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_gemm_route(T, dtype):
+    shapes = [(700, 900), (520, 384), (64, 96)] if T else [(300, 500), (500, 300), (1, 257)]
+    announce(f"step gemm route T={T} dtype={dtype} shapes={shapes}")
+    W0 = [rand(s, dtype, 10 + i) for i, s in enumerate(shapes)]
+    G = [rand(s, dtype, 20 + i, 1e-2) for i, s in enumerate(shapes)]
+    M0 = [rand(s, dtype, 30 + i, 1e-2) for i, s in enumerate(shapes)]
+    W1 = [w.clone() for w in W0]
+    M1 = [m.clone() for m in M0]
+    run_step(W1, G, M1, T, dtype)
+    for i in range(len(shapes)):
+        check_step(W0[i], G[i], M0[i], W1[i], M1[i], T, dtype, 0.02, 0.95, 0.1, True, 0.2)
+
+
+@pytest.mark.parametrize("T", [128, 32])
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_fused_route_bf16(T, nesterov):
+    shapes = [(384, 520), (100, 60), (257, 131)]
+    announce(f"step fused route T={T} nesterov={nesterov} bf16 shapes={shapes}")
+    W0 = [rand(s, torch.bfloat16, 40 + i) for i, s in enumerate(shapes)]
+    G = [rand(s, torch.bfloat16, 50 + i, 1e-2) for i, s in enumerate(shapes)]
+    M0 = [rand(s, torch.bfloat16, 60 + i, 1e-2) for i, s in enumerate(shapes)]
+    W1 = [w.clone() for w in W0]
+    M1 = [m.clone() for m in M0]
+    run_step(W1, G, M1, T, torch.bfloat16, nesterov=nesterov)
+    for i in range(len(shapes)):
+        check_step(W0[i], G[i], M0[i], W1[i], M1[i], T, torch.bfloat16, 0.02, 0.95, 0.1, nesterov, 0.2)
+
+
+def test_direction_per_tile():
+    """W = 0, lambda = 0: the step leaves -lr tau U; U per tile within the map's bar."""
+    announce("step direction readback, T=512 and T=128, bf16")
+    for T in (512, 128):
+        x = rand((700, 900), torch.bfloat16, 70, 1e-2)
+        W = torch.zeros_like(x)
+        M = torch.zeros_like(x)
+        run_step([W], [x], [M], T, torch.bfloat16, lr=0.5, beta=0.9, wd=0.0)
+        _, _, Ur = oracle.himuon_step(np.zeros((700, 900)), np.zeros((700, 900)), to_f64(x), T, 5, *COEF32,
+                                      f32(0.5), f32(0.9), 0.0, True, f32(0.2))
+        U = to_f64(W) / (-f32(0.5) * tau_of(700, 900, T, 0.2))
+        e = tile_errors(U, Ur, T)
+        assert e.max() <= TOL[torch.bfloat16], f"T={T}: max per-tile error {e.max():.3e}"
+
+
+@pytest.mark.parametrize("T", [512, 128])
+def test_three_steps_fp32_with_reconfigure_keeping_momentum(T):
+    """Three steps of the HiMuon state object (fp32), the second after a
+    reconfigure to T = 0 and back: momentum carries across tile sizes."""
+    announce(f"step x3 fp32 with reconfigure, T={T}")
+    shape = (520, 700)
+    p = rand(shape, torch.float32, 80)
+    opt = hm.HiMuon([p], T=T, K=5, coeffs=COEF32, lr=0.05, momentum=0.9, weight_decay=0.05, nesterov=True,
+                    scale_c=0.2)
+    Wr, Mr = to_f64(p), np.zeros(shape)
+    for t, Tt in enumerate([T, 0, T]):
+        opt.reconfigure(Tt)
+        g = rand(shape, torch.float32, 90 + t, 1e-2)
+        W_before, M_before = p.clone(), opt.moms[0].clone()
+        opt.step([g])
+        torch.cuda.synchronize()
+        check_step(W_before, g, M_before, p, opt.moms[0], Tt, torch.float32, 0.05, 0.9, 0.05, True, 0.2)
+        Wr, Mr, _ = oracle.himuon_step(Wr, Mr, to_f64(g), Tt, 5, *COEF32, f32(0.05), f32(0.9), f32(0.05), True,
+                                       f32(0.2))
+    # the trajectory as a whole: three updates of size lr tau ~ 0.05 * 0.2 * sqrt(T)
+    assert np.linalg.norm(to_f64(p) - Wr) <= 1e-5 * np.linalg.norm(Wr)
+    assert np.linalg.norm(to_f64(opt.moms[0]) - Mr) <= 1e-6 * np.linalg.norm(Mr)
+
+
+@pytest.mark.parametrize("T", [512, 128])
+def test_chunked_equals_unchunked(T):
+    announce(f"step chunked vs one chunk, T={T}, bf16")
+    shapes = [(1024, 1024), (512, 768), (640, 512)]
+    W0 = [rand(s, torch.bfloat16, 100 + i) for i, s in enumerate(shapes)]
+    G = [rand(s, torch.bfloat16, 110 + i, 1e-2) for i, s in enumerate(shapes)]
+    M0 = [rand(s, torch.bfloat16, 120 + i, 1e-2) for i, s in enumerate(shapes)]
+    outs = []
+    budget = 1024 * 1024 * 2 if T == 128 else 2 * (2 * 512 * 512 + 2 * 512 * 512) * 3
+    for bud in (0, budget):
+        W1 = [w.clone() for w in W0]
+        M1 = [m.clone() for m in M0]
+        run_step(W1, G, M1, T, torch.bfloat16, budget=bud)
+        outs.append((W1, M1))
+    # the momentum is element-wise either way
+    for a, b in zip(outs[0][1], outs[1][1]):
+        assert torch.equal(a, b)
+    if T == 128:
+        # fused route: groups of whole matrices, each tile's result is independent of its launch
+        for a, b in zip(outs[0][0], outs[1][0]):
+            assert torch.equal(a, b)
+    else:
+        # GEMM route: the GEMM library may pick another kernel for another batch count
+        for i in range(len(shapes)):
+            for W1 in (outs[0][0][i], outs[1][0][i]):
+                check_step(W0[i], G[i], M0[i], W1, outs[0][1][i], T, torch.bfloat16, 0.02, 0.95, 0.1, True, 0.2)
+
+
+def test_non_contiguous_rows_and_untouched_gradient():
+    """A row stride above the width (a column slice of a wider buffer); the
+    gradient is read only, and the columns outside the slice stay as they were."""
+    announce("step strided rows, T=128 and T=512, bf16")
+    for T in (128, 512):
+        big_w = rand((300, 720), torch.bfloat16, 130)
+        big_g = rand((300, 720), torch.bfloat16, 131, 1e-2)
+        big_m = rand((300, 720), torch.bfloat16, 132, 1e-2)
+        W, G, M = big_w[:, :600], big_g[:, :600], big_m[:, :600]
+        W0, G0, M0 = W.clone(), G.clone(), M.clone()
+        w_rest, g_all, m_rest = big_w[:, 600:].clone(), big_g.clone(), big_m[:, 600:].clone()
+        run_step([W], [G], [M], T, torch.bfloat16)
+        check_step(W0, G0, M0, W, M, T, torch.bfloat16, 0.02, 0.95, 0.1, True, 0.2)
+        assert torch.equal(big_g, g_all)
+        assert torch.equal(big_w[:, 600:], w_rest) and torch.equal(big_m[:, 600:], m_rest)
+
+
+def test_zero_gradient_and_momentum():
+    """G = M = 0: Phi_K(0) = 0, so the step is pure weight decay."""
+    announce("step with zero gradient and momentum, T=512 and T=128, fp32")
+    for T in (512, 128, 0):
+        W = rand((300, 400), torch.float32, 140)
+        W0 = W.clone()
+        G = torch.zeros_like(W)
+        M = torch.zeros_like(W)
+        run_step([W], [G], [M], T, torch.float32, lr=0.1, wd=0.5)
+        assert not torch.any(M)
+        d = np.float32(1.0) - np.float32(0.1) * np.float32(0.5)
+        assert np.allclose(to_f64(W), d * to_f64(W0), rtol=2 ** -23, atol=0)

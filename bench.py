@@ -148,6 +148,11 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
         raise SystemExit("no plan for this call (budget below one problem?)")
     log(f"gemm path workspace {need / 2**30:.2f} GiB")
     ws = torch.empty(need, dtype=torch.uint8, device=mats[0].device)
+    if args.tune:
+        t0 = time.perf_counter()
+        hm.gemm_tune(list(zip(rows, cols)), args.T, code, K=args.K, coeffs=coeffs, compute=compute,
+                     chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
+        log(f"GEMM candidates timed in {time.perf_counter() - t0:.1f} s")
 
     def step():
         hm.ns_gemm(mats, outputs=outs, T=args.T, K=args.K, coeffs=coeffs, compute=compute,
@@ -174,7 +179,7 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": op_name, "data": "synthetic",
         "config": {"workload": desc, "path": "gemm", "T": args.T, "K": args.K, "matrices": len(mats),
                    "storage": args.dtype, "mfma_operands": op_name, "accumulate": "f32",
-                   "chunk_budget_bytes": int(args.budget), "workspace_bytes": need},
+                   "chunk_budget_bytes": int(args.budget), "workspace_bytes": need, "gemm_tuned": bool(args.tune)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": None, "flops_per_step": flops_step,
                      "mean_step_ms": round(float(np.mean(step_ms)), 4)},
@@ -203,14 +208,18 @@ def bench_optstep(args, hm, torch, np, dev):
         Ws = [(torch.randn(H, H, device=dev, generator=gen) * 0.02).to(torch.bfloat16) for _ in range(8)]
         Gs = [torch.empty(H, H, dtype=torch.bfloat16, device=dev) for _ in range(8)]
         res = {}
-        for name, T, batched in [("muon_full_per_layer", 0, False), ("muon_full_batched", 0, True),
-                                 ("himuon_T512_per_layer", 512, False), ("himuon_T512_batched", 512, True)]:
+        variants = [("muon_full_per_layer", 0, False), ("muon_full_batched", 0, True),
+                    ("himuon_T512_per_layer", 512, False), ("himuon_T512_batched", 512, True)]
+        if args.variants != "all":
+            keep = args.variants.split(",")
+            variants = [v for v in variants if v[0] in keep]
+        for name, T, batched in variants:
             Ms = [torch.zeros_like(w) for w in Ws]
             torch.cuda.synchronize()
             torch.cuda.reset_peak_memory_stats(dev)
             groups = [list(range(8))] if batched else [[i] for i in range(8)]
             opts = [hm.HiMuon([Ws[i] for i in g], T=T, K=5, coeffs=coeffs, lr=0.02, momentum=0.95,
-                              weight_decay=0.0, nesterov=True, scale_c=0.2) for g in groups]
+                              weight_decay=0.0, nesterov=True, scale_c=0.2, tune=args.tune) for g in groups]
             for o, g in zip(opts, groups):
                 o.moms = [Ms[i] for i in g]
             ws_bytes = sum(o._workspace.numel() for o in opts)
@@ -239,20 +248,23 @@ def bench_optstep(args, hm, torch, np, dev):
                          "workspace_MiB": round(ws_bytes / 2 ** 20, 1)}
             log(f"H={H} {name}: {res[name]}")
             del opts
-        base = res["muon_full_per_layer"]["median_ms"]
-        for name in res:
-            res[name]["speedup_vs_full_per_layer"] = round(base / res[name]["median_ms"], 3)
+        if "muon_full_per_layer" in res:
+            base = res["muon_full_per_layer"]["median_ms"]
+            for name in res:
+                res[name]["speedup_vs_full_per_layer"] = round(base / res[name]["median_ms"], 3)
         out[str(H)] = res
         del Ws, Gs
         torch.cuda.empty_cache()
     h_last = str(hs[-1])
     rec = {
         "metric": "optimizer-step time, 8 x Linear(H,H) bf16, HiMuon T=512 K=5 (batched) [ms]",
-        "value": out[h_last]["himuon_T512_batched"]["median_ms"], "unit": "ms", "n_gpus": 1,
+        "value": out[h_last].get("himuon_T512_batched", next(iter(out[h_last].values())))["median_ms"],
+        "unit": "ms", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "higher_is_better": False, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"8 x Linear({h_last},{h_last}) bf16, fresh N(0,1) gradients each step",
-                   "T": 512, "K": 5, "momentum": 0.95, "nesterov": True, "scale_c": 0.2},
+                   "T": 512, "K": 5, "momentum": 0.95, "nesterov": True, "scale_c": 0.2,
+                   "gemm_tuned": bool(args.tune)},
         "results": out,
     }
     print(json.dumps(rec), flush=True)
@@ -275,7 +287,11 @@ def main():
                          "(--T 0) or large tiles (e.g. --T 512) through batched library GEMMs")
     ap.add_argument("--optstep", action="store_true",
                     help="run the optimizer-step benchmark (8 x Linear(H,H), HiMuon T=512 vs full Muon) instead")
+    ap.add_argument("--tune", type=int, default=1,
+                    help="time the GEMM library's candidates for the GEMM path before the run (1) or not (0)")
     ap.add_argument("--hidden", default="1024,2048,4096", help="H values of --optstep")
+    ap.add_argument("--variants", default="all",
+                    help="--optstep variants to run (comma-separated names, or all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB per launch (counter calibration)")
     args = ap.parse_args()

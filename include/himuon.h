@@ -168,6 +168,25 @@ int himuon_ns_gemm(int64_t n_mats,
                    void* stream);
 
 /*
+ * Picks, for every GEMM that a himuon_ns_gemm (or GEMM-route himuon_step)
+ * call with these shapes and arguments would run, the fastest of the GEMM
+ * library's leading heuristic candidates (up to 8), by timing each on the
+ * workspace's buffers on `stream`; later calls on this device use the
+ * choice. Results never depend on it beyond the rounding of the GEMMs.
+ *
+ * Arguments as himuon_ns_gemm_workspace_size, plus workspace (at least that
+ * many bytes; its contents are overwritten) and stream. Unlike the compute
+ * entry points this call synchronises with `stream` (it waits on timing
+ * events) and must not run concurrently with other calls on the device.
+ * A shape set that was tuned before returns at once. Errors as
+ * himuon_ns_gemm.
+ */
+int himuon_gemm_tune(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T,
+                     int dtype, int compute, int K, float a, float b, float c,
+                     void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
+                     void* stream);
+
+/*
  * One HiMuon optimizer step (Alg. 1) on n_mats parameter matrices, in place:
  *
  *   M_l <- beta M_l + G_l                            eq. (muon_momentum)

@@ -65,6 +65,9 @@ def lib():
         L.himuon_step.argtypes = [i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, f, f, f,
                                   f, f, f, ctypes.c_int, f, ctypes.c_int, ctypes.c_int, vp, sz, sz, vp]
         L.himuon_step.restype = ctypes.c_int
+        L.himuon_gemm_tune.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       f, f, f, vp, sz, sz, vp]
+        L.himuon_gemm_tune.restype = ctypes.c_int
         L.himuon_plan_chunks.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, sz, vp, vp, vp, i64]
         L.himuon_plan_chunks.restype = ctypes.c_int
         L.himuon_select_compute.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -143,6 +146,37 @@ def himuon_step(n_mats, weights, grads, moms, rows, cols, ld, T, K, a, b, c, lr,
         float(c), float(lr), float(momentum), float(weight_decay), int(bool(nesterov)), float(scale_c),
         int(dtype), int(compute), int(workspace) if workspace else None, int(workspace_bytes),
         int(chunk_budget_bytes), int(stream) if stream else None))
+
+
+def himuon_gemm_tune(rows, cols, T, dtype, compute, K, a, b, c, workspace, workspace_bytes,
+                     chunk_budget_bytes=0, stream=None) -> int:
+    """Same arguments as the C function (``workspace`` a device pointer). Returns the status code."""
+    return int(lib().himuon_gemm_tune(
+        len(rows), _i64_array(rows), _i64_array(cols), int(T), int(dtype), int(compute), int(K),
+        float(a), float(b), float(c), int(workspace) if workspace else None, int(workspace_bytes),
+        int(chunk_budget_bytes), int(stream) if stream else None))
+
+
+def gemm_tune(shapes, T, dtype, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0,
+              workspace=None, stream=None, device="cuda"):
+    """Time the GEMM library's candidates for the GEMM-path calls over matrices
+    of these ``(rows, cols)`` shapes (T = 0 or large tiles) and keep the
+    fastest; synchronises. ``dtype`` is F32 or BF16."""
+    import torch
+    a, b, c = coeffs
+    rows = [int(h) for h, _ in shapes]
+    cols = [int(w) for _, w in shapes]
+    need = himuon_ns_gemm_workspace_size(rows, cols, T, dtype, compute, K, a, b, c, chunk_budget_bytes)
+    if need == 0:
+        raise HimuonError(ERR_INVALID_ARG, "himuon_ns_gemm_workspace_size")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    if stream is None:
+        stream = torch.cuda.current_stream(workspace.device)
+    st = himuon_gemm_tune(rows, cols, T, dtype, compute, K, a, b, c, workspace.data_ptr(),
+                          workspace.numel() * workspace.element_size(), chunk_budget_bytes, stream.cuda_stream)
+    if st != OK:
+        raise HimuonError(st, "himuon_gemm_tune")
 
 
 def himuon_plan_chunks(rows, cols, T, dtype=BF16, chunk_budget_bytes=0):
@@ -322,10 +356,11 @@ class HiMuon:
     cached across steps. ``reconfigure(T)`` changes the tile size at run time
     (Sec. 4.4.4) and keeps the momentum; T = 0 is the full-matrix branch.
     Every step is one library call over all matrices (cross-layer batching,
-    Sec. 4.4.2)."""
+    Sec. 4.4.2). With ``tune`` (default), a tile size served by the library
+    GEMMs has its GEMM kernels chosen by timing at (re)configuration."""
 
     def __init__(self, params, T=512, K=5, coeffs=QUINTIC, lr=0.02, momentum=0.95, weight_decay=0.0,
-                 nesterov=True, scale_c=0.2, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0):
+                 nesterov=True, scale_c=0.2, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0, tune=True):
         import torch
         self.params = list(params)
         if not self.params:
@@ -337,6 +372,7 @@ class HiMuon:
         self.K, self.coeffs, self.lr, self.momentum = K, coeffs, lr, momentum
         self.weight_decay, self.nesterov, self.scale_c = weight_decay, nesterov, scale_c
         self.compute, self.chunk_budget_bytes = compute, chunk_budget_bytes
+        self.tune = tune
         self._workspace = None
         self.reconfigure(T)
 
@@ -352,6 +388,9 @@ class HiMuon:
             raise HimuonError(ERR_INVALID_ARG, "himuon_step_workspace_size")
         if self._workspace is None or self._workspace.numel() < need:
             self._workspace = torch.empty(need, dtype=torch.uint8, device=self.params[0].device)
+        if self.tune and T not in (32, 64, 128, 256):
+            gemm_tune([tuple(p.shape) for p in self.params], T, code, K=self.K, coeffs=self.coeffs,
+                      compute=self.compute, chunk_budget_bytes=self.chunk_budget_bytes, workspace=self._workspace)
         self.T = T
 
     def step(self, grads, stream=None):

@@ -15,6 +15,7 @@
 // norm pass also stores the new M), and the scatter applies the decoupled
 // weight decay and the tau-scaled update to W (eq. scaled_update).
 #include "ns_gemm_path.h"
+#include "elementwise8.h"
 
 #include <hip/hip_bf16.h>
 #include <hip/hip_fp16.h>
@@ -23,18 +24,12 @@
 namespace himuon {
 namespace {
 
-constexpr int kThreads = 256;  // 32 x 8: a 32 x 32 iterate tile, four rows per thread
-
-template <GemmStore ST>
-__device__ __forceinline__ double load_elem(const void* base, int64_t idx)
-{
-    if constexpr (ST == GemmStore::BF16) {
-        const uint16_t u = static_cast<const uint16_t*>(base)[idx];
-        return (double)__uint_as_float((uint32_t)u << 16);
-    } else {
-        return (double)static_cast<const float*>(base)[idx];
-    }
-}
+constexpr int kThreads = 256;
+// A block of the gather and scatter covers 32 rows x 64 columns of the
+// iterate: in the row-major orientation a thread moves one 8-column chunk;
+// a transposed block goes through LDS as two 32 x 32 tiles, four rows per
+// thread.
+constexpr int kBlkRows = 32, kBlkCols = 64;
 
 template <GemmStore ST>
 __device__ __forceinline__ void store_elem(void* base, int64_t idx, float v)
@@ -56,14 +51,6 @@ __device__ __forceinline__ float load_f32(const void* base, int64_t idx)
     } else {
         return static_cast<const float*>(base)[idx];
     }
-}
-
-// The value a store of v leaves in memory, as fp32.
-template <GemmStore ST>
-__device__ __forceinline__ float stored_value(float v)
-{
-    if constexpr (ST == GemmStore::BF16) return (float)(__bf16)v;
-    else return v;
 }
 
 // Eq. (muon_lookahead) or the plain buffer, from G and the stored new M.
@@ -115,17 +102,22 @@ __global__ void __launch_bounds__(kThreads) gemm_norm_partials(const GemmProb* p
     double acc = 0.0;
     for (int r = r0; r < r1; ++r) {
         const int64_t rowoff = (P.row0 + r) * P.ld_in + P.col0;
-        for (int c = threadIdx.x; c < P.w; c += kThreads) {
-            double v;
+        for (int c = 8 * (int)threadIdx.x; c < P.w; c += 8 * kThreads) {
+            const int nv = min(8, P.w - c);
+            const bool vec = (P.vec & GEMM_VEC_IN) && nv == 8;
+            float g[8];
+            load8<ST>(P.in, rowoff + c, nv, vec, g);
             if constexpr (OPT) {
-                const float g = load_f32<ST>(P.in, rowoff + c);
-                const float m = stored_value<ST>(o.beta * load_f32<ST>(P.mom, rowoff + c) + g);
-                store_elem<ST>(P.mom, rowoff + c, m);
-                v = (double)lookahead(g, m, o);
-            } else {
-                v = load_elem<ST>(P.in, rowoff + c);
+                float m[8];
+                load8<ST>(P.mom, rowoff + c, nv, vec, m);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) m[e] = o.beta * m[e] + g[e];
+                store8<ST>(P.mom, rowoff + c, nv, vec, m);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) g[e] = lookahead(g[e], m[e], o);
             }
-            acc += v * v;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc += (double)g[e] * (double)g[e];
         }
     }
     __shared__ double red[kThreads];
@@ -150,6 +142,60 @@ __global__ void gemm_norm_finalize(int nprob, int nparts, double scale, double* 
     partial[(int64_t)p * nparts] = ss > 0.0 ? scale / sqrt(ss) : 0.0;
 }
 
+// Eight consecutive iterate elements (operand type) as fp32 / from fp32;
+// `vec` when the chunk is whole and 16-byte aligned.
+template <GemmOperand OP>
+__device__ __forceinline__ void load_x8(const void* xv, int64_t idx, int n, bool vec, float (&v)[8])
+{
+    typedef typename OpType<OP>::T OT;
+    const OT* x = static_cast<const OT*>(xv) + idx;
+    if constexpr (OP == GemmOperand::F32) {
+        load8<GemmStore::F32>(x, 0, n, vec, v);
+    } else {
+        if (vec) {
+            const uint4 r = *reinterpret_cast<const uint4*>(x);
+            const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint16_t h = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+                v[e] = (float)__builtin_bit_cast(OT, h);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = e < n ? (float)x[e] : 0.f;
+        }
+    }
+}
+
+template <GemmOperand OP>
+__device__ __forceinline__ void store_x8(void* xv, int64_t idx, int n, bool vec, const float (&v)[8])
+{
+    typedef typename OpType<OP>::T OT;
+    OT* x = static_cast<OT*>(xv) + idx;
+    if constexpr (OP == GemmOperand::F32) {
+        float t[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t[e] = v[e];
+        store8<GemmStore::F32>(x, 0, n, vec, t);
+    } else {
+        if (vec) {
+            uint16_t h[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) h[e] = __builtin_bit_cast(uint16_t, (OT)v[e]);
+            uint4 r;
+            r.x = h[0] | ((uint32_t)h[1] << 16);
+            r.y = h[2] | ((uint32_t)h[3] << 16);
+            r.z = h[4] | ((uint32_t)h[5] << 16);
+            r.w = h[6] | ((uint32_t)h[7] << 16);
+            *reinterpret_cast<uint4*>(x) = r;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (e < n) x[e] = (OT)v[e];
+        }
+    }
+}
+
 template <GemmStore ST, GemmOperand OP, bool OPT>
 __global__ void __launch_bounds__(kThreads) gemm_gather(const GemmProb* probs, int m, int n, int nparts,
                                                         const double* partial, void* xv, const OptArgs o)
@@ -158,35 +204,48 @@ __global__ void __launch_bounds__(kThreads) gemm_gather(const GemmProb* probs, i
     const int p = blockIdx.y;
     const GemmProb P = probs[p];
     const double s = partial[(int64_t)p * nparts];
-    const int tiles_n = (n + 31) / 32;
-    const int i0 = (int)(blockIdx.x / tiles_n) * 32, j0 = (int)(blockIdx.x % tiles_n) * 32;
+    const int blk_n = (n + kBlkCols - 1) / kBlkCols;
+    const int i0 = (int)(blockIdx.x / blk_n) * kBlkRows, j0 = (int)(blockIdx.x % blk_n) * kBlkCols;
     OT* x = static_cast<OT*>(xv) + (int64_t)p * m * n;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
     if (!P.trans) {
+        const int i = i0 + (int)(threadIdx.x >> 3), j = j0 + 8 * (int)(threadIdx.x & 7);
+        if (i >= m || j >= n) return;
+        float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        if (i < P.h && j < P.w) {
+            const int nv = min(8, P.w - j);
+            const bool vec = (P.vec & GEMM_VEC_IN) && nv == 8;
+            const int64_t idx = (P.row0 + i) * P.ld_in + P.col0 + j;
+            load8<ST>(P.in, idx, nv, vec, v);
+            if constexpr (OPT) {
+                float mm[8];
+                load8<ST>(P.mom, idx, nv, vec, mm);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int i = i0 + ty + 8 * k, j = j0 + tx;
-            if (i < m && j < n) {
-                double v = 0.0;
-                if (i < P.h && j < P.w) v = (double)input_elem<ST, OPT>(P, (P.row0 + i) * P.ld_in + P.col0 + j, o) * s;
-                x[(int64_t)i * n + j] = (OT)(float)v;
+                for (int e = 0; e < 8; ++e) v[e] = lookahead(v[e], mm[e], o);
             }
         }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (float)((double)v[e] * s);
+        store_x8<OP>(x, (int64_t)i * n + j, min(8, n - j), n % 8 == 0, v);
     } else {
         // iterate (i, j) = block (j, i): block rows j0.., columns i0.. through LDS
         __shared__ float t[32][33];
+        const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+        for (int half = 0; half < 2; ++half) {
+            const int jh = j0 + 32 * half;
+            if (half) __syncthreads();
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int r = j0 + ty + 8 * k, c = i0 + tx;
-            double v = 0.0;
-            if (r < P.h && c < P.w) v = (double)input_elem<ST, OPT>(P, (P.row0 + r) * P.ld_in + P.col0 + c, o) * s;
-            t[ty + 8 * k][tx] = (float)v;
-        }
-        __syncthreads();
+            for (int k = 0; k < 4; ++k) {
+                const int r = jh + ty + 8 * k, c = i0 + tx;
+                double v = 0.0;
+                if (r < P.h && c < P.w) v = (double)input_elem<ST, OPT>(P, (P.row0 + r) * P.ld_in + P.col0 + c, o) * s;
+                t[ty + 8 * k][tx] = (float)v;
+            }
+            __syncthreads();
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int i = i0 + ty + 8 * k, j = j0 + tx;
-            if (i < m && j < n) x[(int64_t)i * n + j] = (OT)t[tx][ty + 8 * k];
+            for (int k = 0; k < 4; ++k) {
+                const int i = i0 + ty + 8 * k, j = jh + tx;
+                if (i < m && j < n) x[(int64_t)i * n + j] = (OT)t[tx][ty + 8 * k];
+            }
         }
     }
 }
@@ -198,37 +257,54 @@ __global__ void __launch_bounds__(kThreads) gemm_scatter(const GemmProb* probs, 
     typedef typename OpType<OP>::T OT;
     const int p = blockIdx.y;
     const GemmProb P = probs[p];
-    const int tiles_n = (n + 31) / 32;
-    const int i0 = (int)(blockIdx.x / tiles_n) * 32, j0 = (int)(blockIdx.x % tiles_n) * 32;
+    const int blk_n = (n + kBlkCols - 1) / kBlkCols;
+    const int i0 = (int)(blockIdx.x / blk_n) * kBlkRows, j0 = (int)(blockIdx.x % blk_n) * kBlkCols;
     const OT* x = static_cast<const OT*>(xv) + (int64_t)p * m * n;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
     if (!P.trans) {
+        const int i = i0 + (int)(threadIdx.x >> 3), j = j0 + 8 * (int)(threadIdx.x & 7);
+        if (i >= P.h || j >= P.w) return;
+        const int nv = min(8, P.w - j);
+        float u[8];
+        load_x8<OP>(x, (int64_t)i * n + j, nv, n % 8 == 0 && nv == 8, u);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int i = i0 + ty + 8 * k, j = j0 + tx;
-            if (i < P.h && j < P.w)
-                output_elem<ST, OPT>(P, (P.row0 + i) * P.ld_out + P.col0 + j, (float)x[(int64_t)i * n + j] * inv_scale, o);
+        for (int e = 0; e < 8; ++e) u[e] *= inv_scale;
+        const bool vec = (P.vec & GEMM_VEC_OUT) && nv == 8;
+        const int64_t idx = (P.row0 + i) * P.ld_out + P.col0 + j;
+        if constexpr (OPT) {
+            float w[8];
+            load8<ST>(P.out, idx, nv, vec, w);
+            const float step = o.lr * P.tau;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) w[e] = o.decay * w[e] - step * u[e];
+            store8<ST>(P.out, idx, nv, vec, w);
+        } else {
+            store8<ST>(P.out, idx, nv, vec, u);
         }
     } else {
         __shared__ float t[32][33];
+        const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+        for (int half = 0; half < 2; ++half) {
+            const int jh = j0 + 32 * half;
+            if (half) __syncthreads();
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int i = i0 + ty + 8 * k, j = j0 + tx;
-            t[ty + 8 * k][tx] = (i < m && j < n) ? (float)x[(int64_t)i * n + j] * inv_scale : 0.f;
-        }
-        __syncthreads();
-        // block (r, c) = iterate (c, r): block rows j0.., columns i0..
+            for (int k = 0; k < 4; ++k) {
+                const int i = i0 + ty + 8 * k, j = jh + tx;
+                t[ty + 8 * k][tx] = (i < m && j < n) ? (float)x[(int64_t)i * n + j] * inv_scale : 0.f;
+            }
+            __syncthreads();
+            // block (r, c) = iterate (c, r): block rows jh.., columns i0..
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int r = j0 + ty + 8 * k, c = i0 + tx;
-            if (r < P.h && c < P.w) output_elem<ST, OPT>(P, (P.row0 + r) * P.ld_out + P.col0 + c, t[tx][ty + 8 * k], o);
+            for (int k = 0; k < 4; ++k) {
+                const int r = jh + ty + 8 * k, c = i0 + tx;
+                if (r < P.h && c < P.w) output_elem<ST, OPT>(P, (P.row0 + r) * P.ld_out + P.col0 + c, t[tx][ty + 8 * k], o);
+            }
         }
     }
 }
 
 dim3 tile_grid(int m, int n, int nprob)
 {
-    return dim3((unsigned)(((m + 31) / 32) * ((n + 31) / 32)), (unsigned)nprob, 1);
+    return dim3((unsigned)(((m + kBlkRows - 1) / kBlkRows) * ((n + kBlkCols - 1) / kBlkCols)), (unsigned)nprob, 1);
 }
 
 }  // namespace

@@ -171,14 +171,19 @@ int resolve_operand(int dtype, int compute, int K, float a, float b, float c, in
 std::mutex g_lt_mu;
 hipblasLtHandle_t g_lt[kMaxDevices] = {};
 
+constexpr int kCandidates = 8;  // heuristic results kept per GEMM for himuon_gemm_tune
+
 struct Gemm {
     hipblasLtMatmulDesc_t desc = nullptr;
     hipblasLtMatrixLayout_t la = nullptr, lb = nullptr, lc = nullptr;
-    hipblasLtMatmulAlgo_t algo{};
+    hipblasLtMatmulAlgo_t algo{};  // in use: the heuristic's first choice, or the tuned one
+    hipblasLtMatmulAlgo_t cand[kCandidates];
+    int n_cand = 0;
 };
 
 struct Plan {
     Gemm gram, poly, apply;  // A = X X^T; B = alpha A A + beta A; X' = X B + a X (column-major view)
+    bool tuned = false;
 };
 
 std::map<std::tuple<int, int, int, int, int>, Plan> g_plans;  // (dev, m, n, batch, op)
@@ -216,18 +221,22 @@ bool make_gemm(hipblasLtHandle_t h, Gemm& g, hipblasOperation_t ta, hipDataType 
     const uint64_t wsmax = kLtWorkspace;
     bool ok = hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &wsmax,
                                                     sizeof(wsmax)) == HIPBLAS_STATUS_SUCCESS;
-    hipblasLtMatmulHeuristicResult_t res[1];
+    hipblasLtMatmulHeuristicResult_t res[kCandidates];
     int found = 0;
-    ok = ok && hipblasLtMatmulAlgoGetHeuristic(h, g.desc, g.la, g.lb, g.lc, g.lc, pref, 1, res, &found) ==
+    ok = ok && hipblasLtMatmulAlgoGetHeuristic(h, g.desc, g.la, g.lb, g.lc, g.lc, pref, kCandidates, res, &found) ==
                    HIPBLAS_STATUS_SUCCESS;
     hipblasLtMatmulPreferenceDestroy(pref);
-    if (!ok || found < 1 || res[0].workspaceSize > kLtWorkspace) return false;
-    g.algo = res[0].algo;
+    if (!ok) return false;
+    g.n_cand = 0;
+    for (int i = 0; i < found && i < kCandidates; ++i)
+        if (res[i].state == HIPBLAS_STATUS_SUCCESS && res[i].workspaceSize <= kLtWorkspace) g.cand[g.n_cand++] = res[i].algo;
+    if (g.n_cand < 1) return false;
+    g.algo = g.cand[0];
     return true;
 }
 
 // The three GEMMs for a batch of m x n iterates (built once per shape).
-int get_plan(int dev, int m, int n, int batch, GemmOperand op, hipblasLtHandle_t* handle, const Plan** plan)
+int get_plan(int dev, int m, int n, int batch, GemmOperand op, hipblasLtHandle_t* handle, Plan** plan)
 {
     std::lock_guard<std::mutex> lock(g_lt_mu);
     if (dev < 0 || dev >= kMaxDevices) return himuon::set_hip_error(hipErrorInvalidDevice);
@@ -263,6 +272,34 @@ int run_gemm(hipblasLtHandle_t h, const Gemm& g, float alpha, const void* A, con
     const hipblasStatus_t s = hipblasLtMatmul(h, g.desc, &alpha, A, g.la, B, g.lb, &beta, C, g.lc, D, g.lc, &g.algo,
                                               lt_ws, kLtWorkspace, stream);
     return s == HIPBLAS_STATUS_SUCCESS ? HIMUON_OK : himuon::set_hip_error(hipErrorLaunchFailure);
+}
+
+// Times every kept candidate of `g` on the given operands (three runs after
+// one warm-up, on `stream`, synchronising) and keeps the fastest in g.algo.
+int tune_gemm(hipblasLtHandle_t h, Gemm& g, float alpha, const void* A, const void* B, float beta, const void* C,
+              void* D, void* lt_ws, hipStream_t stream, hipEvent_t e0, hipEvent_t e1)
+{
+    float best = 0.f;
+    int best_i = -1;
+    for (int i = 0; i < g.n_cand; ++i) {
+        g.algo = g.cand[i];
+        if (run_gemm(h, g, alpha, A, B, beta, C, D, lt_ws, stream) != HIMUON_OK) continue;
+        if (hipEventRecord(e0, stream) != hipSuccess) return himuon::set_hip_error(hipGetLastError());
+        int st = HIMUON_OK;
+        for (int r = 0; r < 3 && st == HIMUON_OK; ++r) st = run_gemm(h, g, alpha, A, B, beta, C, D, lt_ws, stream);
+        if (st != HIMUON_OK) continue;
+        hipError_t e = hipEventRecord(e1, stream);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float ms = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+        if (e != hipSuccess) return himuon::set_hip_error(e);
+        if (best_i < 0 || ms < best) {
+            best = ms;
+            best_i = i;
+        }
+    }
+    g.algo = g.cand[best_i < 0 ? 0 : best_i];
+    return HIMUON_OK;
 }
 
 }  // namespace
@@ -318,6 +355,13 @@ int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_p
             p.ld_out = ld_out ? ld_out[l] : cols[l];
             p.mom = opt ? mom_ptrs[l] : nullptr;
             p.tau = opt ? tau[l] : 0.f;
+            // 16-byte chunks at every 8th column of a block (block origins are multiples of T)
+            const int64_t mult = dtype == HIMUON_BF16 ? 8 : 4;
+            const bool origins = T == 0 || T % 8 == 0;
+            const bool vin = origins && (uintptr_t)p.in % 16 == 0 && p.ld_in % mult == 0 &&
+                             (!opt || (uintptr_t)p.mom % 16 == 0);
+            const bool vout = origins && (uintptr_t)p.out % 16 == 0 && p.ld_out % mult == 0;
+            p.vec = (vin ? himuon::GEMM_VEC_IN : 0) | (vout ? himuon::GEMM_VEC_OUT : 0);
             if (whole_matrix(rows[l], cols[l], T)) {
                 p.row0 = p.col0 = 0;
                 p.h = (int32_t)rows[l];
@@ -355,7 +399,7 @@ int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_p
     int status = HIMUON_OK;
     for (const Group& g : groups) {
         const int64_t small = g.count / g.n_chunks, big = ceil_div(g.count, g.n_chunks);
-        const Plan* pl = nullptr;
+        Plan* pl = nullptr;
         status = get_plan(dev, g.m, g.n, (int)big, op, &lt, &pl);
         if (status == HIMUON_OK && small != big && small > 0) status = get_plan(dev, g.m, g.n, (int)small, op, &lt, &pl);
         if (status != HIMUON_OK) break;
@@ -390,7 +434,7 @@ int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_p
             const int64_t p1 = (int64_t)(((__int128)(ci + 1) * g.count) / g.n_chunks);
             const int np = (int)(p1 - p0);
             const GemmProb* tp = table + g.first + p0;
-            const Plan* pl = nullptr;
+            Plan* pl = nullptr;
             status = get_plan(dev, g.m, g.n, np, op, &lt, &pl);
             if (status != HIMUON_OK) break;
             if ((e = himuon::launch_gemm_norm_partials(sto, tp, np, g.nparts, partial, opt, hs)) != hipSuccess ||
@@ -450,6 +494,84 @@ int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_
 {
     return himuon::run_gemm_path(n_mats, in_ptrs, out_ptrs, nullptr, nullptr, rows, cols, ld_in, ld_out, T, K, a, b, c,
                                  dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream, nullptr);
+}
+
+
+int himuon_gemm_tune(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype, int compute, int K,
+                     float a, float b, float c, void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
+                     void* stream)
+{
+    if (n_mats < 1 || !rows || !cols || K < 0 || T < 0 || !isfinite(a) || !isfinite(b) || !isfinite(c))
+        return HIMUON_ERR_INVALID_ARG;
+    if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
+    if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
+    std::vector<Group> groups;
+    int st = plan_groups(n_mats, rows, cols, T, groups, nullptr);
+    if (st != HIMUON_OK) return st;
+    int m_max = 0;
+    int64_t total = 0;
+    for (const Group& g : groups) {
+        m_max = std::max(m_max, g.m);
+        total += g.count;
+    }
+    GemmOperand op;
+    st = resolve_operand(dtype, compute, K, a, b, c, m_max, &op);
+    if (st != HIMUON_OK) return st;
+    size_t need = 0;
+    st = plan_chunks(groups, op, chunk_budget_bytes, &need);
+    if (st != HIMUON_OK) return st;
+    if (!workspace || workspace_bytes < need) return HIMUON_ERR_WORKSPACE;
+
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    int cur = 0, dev = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return himuon::set_hip_error(e);
+    dev = cur;
+    if (hs) {
+        e = hipStreamGetDevice(hs, &dev);
+        if (e != hipSuccess) return himuon::set_hip_error(e);
+    }
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return himuon::set_hip_error(e);
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if ((e = hipEventCreate(&e0)) != hipSuccess || (e = hipEventCreate(&e1)) != hipSuccess) {
+        if (e0) (void)hipEventDestroy(e0);
+        if (dev != cur) (void)hipSetDevice(cur);
+        return himuon::set_hip_error(e);
+    }
+    const size_t es = op_size(op);
+    size_t part_max = 0, buf_max = 0;
+    for (const Group& g : groups) {
+        part_max = std::max(part_max, (size_t)g.cap * g.nparts * sizeof(double));
+        buf_max = std::max(buf_max, 2 * align_up((size_t)g.cap * g.m * g.n * es) + 2 * align_up((size_t)g.cap * g.m * g.m * es));
+    }
+    uint8_t* const bufs = static_cast<uint8_t*>(workspace) + align_up((size_t)total * sizeof(GemmProb)) + align_up(part_max);
+    void* const lt_ws = bufs + buf_max;
+    for (const Group& g : groups) {
+        if (st != HIMUON_OK) break;
+        const size_t xb = align_up((size_t)g.cap * g.m * g.n * es), ab = align_up((size_t)g.cap * g.m * g.m * es);
+        uint8_t* const X0 = bufs;
+        uint8_t* const X1 = bufs + xb;
+        uint8_t* const A = bufs + 2 * xb;
+        uint8_t* const B = bufs + 2 * xb + ab;
+        const double s = op == GemmOperand::F16 ? sqrt((double)g.m) : 1.0;
+        const float alpha2 = (float)((double)c / (s * s * s * s)), beta2 = (float)((double)b / (s * s));
+        const int64_t sizes[2] = {ceil_div(g.count, g.n_chunks), g.count / g.n_chunks};
+        for (int k = 0; k < 2 && st == HIMUON_OK; ++k) {
+            if (sizes[k] < 1 || (k == 1 && sizes[1] == sizes[0])) continue;
+            hipblasLtHandle_t lt = nullptr;
+            Plan* pl = nullptr;
+            st = get_plan(dev, g.m, g.n, (int)sizes[k], op, &lt, &pl);
+            if (st != HIMUON_OK || pl->tuned) continue;
+            st = tune_gemm(lt, pl->gram, 1.f, X0, X0, 0.f, A, A, lt_ws, hs, e0, e1);
+            if (st == HIMUON_OK) st = tune_gemm(lt, pl->poly, alpha2, A, A, beta2, A, B, lt_ws, hs, e0, e1);
+            if (st == HIMUON_OK) st = tune_gemm(lt, pl->apply, 1.f, X0, B, a, X0, X1, lt_ws, hs, e0, e1);
+            if (st == HIMUON_OK) pl->tuned = true;
+        }
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (dev != cur) (void)hipSetDevice(cur);
+    return st;
 }
 
 }  // extern "C"

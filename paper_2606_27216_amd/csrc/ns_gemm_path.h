@@ -23,9 +23,16 @@ struct alignas(64) GemmProb {
     int32_t trans;
     float tau;           // optimizer step: the update scale tau of the block's matrix
     void* mom;           // optimizer step: the momentum buffer (layout of `in`)
-    int64_t pad_[7];
+    int32_t vec;         // GEMM_VEC_IN / GEMM_VEC_OUT
+    int32_t pad0_;
+    int64_t pad_[6];
 };
 static_assert(sizeof(GemmProb) == 128, "problem descriptor layout");
+
+// Every 8-column chunk of the block's rows that starts at a multiple of 8
+// is 16-byte aligned in `in` and `mom` (GEMM_VEC_IN) or in `out` (GEMM_VEC_OUT).
+constexpr int32_t GEMM_VEC_IN = 1;
+constexpr int32_t GEMM_VEC_OUT = 2;
 
 // The optimizer step of Alg. 1 fused into the gather and scatter kernels:
 // `in` holds the gradient G, `mom` the momentum M and `out` the weights W.

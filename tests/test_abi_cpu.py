@@ -253,3 +253,19 @@ def _scall(**kw):
 ])
 def test_step_validation_rejects_before_any_hip_call(kw, status):
     assert _scall(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(rows=[0]), hm.ERR_INVALID_ARG),
+    (dict(T=-1), hm.ERR_INVALID_ARG),
+    (dict(K=-1), hm.ERR_INVALID_ARG),
+    (dict(dtype=7), hm.ERR_INVALID_ARG),
+    (dict(dtype=hm.F32, compute=hm.COMPUTE_BF16), hm.ERR_UNSUPPORTED),
+    (dict(workspace=0), hm.ERR_WORKSPACE),
+    (dict(workspace_bytes=1024), hm.ERR_WORKSPACE),
+])
+def test_gemm_tune_validation_rejects_before_any_hip_call(kw, status):
+    args = dict(rows=[64], cols=[64], T=0, dtype=hm.BF16, compute=hm.COMPUTE_DEFAULT, K=5, a=3.4445, b=-4.775,
+                c=2.0315, workspace=FAKE, workspace_bytes=256, chunk_budget_bytes=0, stream=None)
+    args.update(kw)
+    assert hm.himuon_gemm_tune(**args) == status

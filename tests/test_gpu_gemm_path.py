@@ -108,3 +108,19 @@ def test_transpose_equivariance():
     y = gemm([x], T=0)[0]
     yt = gemm([x.t().contiguous()], T=0)[0]
     assert rel(to_f64(yt).T, to_f64(y)) <= 2e-6
+
+
+def test_tuned_kernels_match_oracle():
+    """After the GEMM library's candidates are timed and the fastest kept,
+    results still meet the bars (T = 512 tiles and whole matrices)."""
+    announce("gemm tune, then T=512 and T=0 vs oracle, bf16")
+    x = rand((700, 900), torch.bfloat16, 17)
+    hm.gemm_tune([(700, 900)], 512, hm.BF16, K=5, coeffs=COEF32)
+    hm.gemm_tune([(700, 900)], 0, hm.BF16, K=5, coeffs=COEF32)
+    torch.cuda.synchronize()
+    y = gemm([x], T=512)[0]
+    e = tile_errors(to_f64(y), oracle.ns_tiled(to_f64(x), 512, 5, *COEF32), 512)
+    assert e.max() <= 2e-2, f"T=512: {e.max():.3e}"
+    y0 = gemm([x], T=0)[0]
+    e0 = rel(to_f64(y0), oracle.phi_k(to_f64(x), 5, *COEF32))
+    assert e0 <= 2e-2, f"T=0: {e0:.3e}"

@@ -256,14 +256,15 @@ def bench_optstep(args, hm, torch, np, dev):
         del Ws, Gs
         torch.cuda.empty_cache()
     h_last = str(hs[-1])
+    headline = "himuon_T512_batched" if "himuon_T512_batched" in out[h_last] else next(iter(out[h_last]))
     rec = {
-        "metric": "optimizer-step time, 8 x Linear(H,H) bf16, HiMuon T=512 K=5 (batched) [ms]",
-        "value": out[h_last].get("himuon_T512_batched", next(iter(out[h_last].values())))["median_ms"],
+        "metric": "optimizer-step time, 8 x Linear(H,H) bf16, K=5, median [ms]",
+        "value": out[h_last][headline]["median_ms"],
         "unit": "ms", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "higher_is_better": False, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"8 x Linear({h_last},{h_last}) bf16, fresh N(0,1) gradients each step",
-                   "T": 512, "K": 5, "momentum": 0.95, "nesterov": True, "scale_c": 0.2,
+                   "variant": headline, "T": 0 if headline.startswith("muon_full") else 512, "K": 5, "momentum": 0.95, "nesterov": True, "scale_c": 0.2,
                    "gemm_tuned": bool(args.tune)},
         "results": out,
     }

@@ -100,25 +100,27 @@ __global__ void __launch_bounds__(kThreads) gemm_norm_partials(const GemmProb* p
     const int r0 = (int)blockIdx.x * rpp;
     const int r1 = min(P.h, r0 + rpp);
     double acc = 0.0;
-    for (int r = r0; r < r1; ++r) {
+    // the part's rows x 8-column chunks, flattened: element e = (row, chunk)
+    const int cpr = (P.w + 7) / 8;
+    const int64_t n_e = (int64_t)max(r1 - r0, 0) * cpr;
+    for (int64_t e0 = threadIdx.x; e0 < n_e; e0 += kThreads) {
+        const int r = r0 + (int)(e0 / cpr), c = 8 * (int)(e0 % cpr);
         const int64_t rowoff = (P.row0 + r) * P.ld_in + P.col0;
-        for (int c = 8 * (int)threadIdx.x; c < P.w; c += 8 * kThreads) {
-            const int nv = min(8, P.w - c);
-            const bool vec = (P.vec & GEMM_VEC_IN) && nv == 8;
-            float g[8];
-            load8<ST>(P.in, rowoff + c, nv, vec, g);
-            if constexpr (OPT) {
-                float m[8];
-                load8<ST>(P.mom, rowoff + c, nv, vec, m);
+        const int nv = min(8, P.w - c);
+        const bool vec = (P.vec & GEMM_VEC_IN) && nv == 8;
+        float g[8];
+        load8<ST>(P.in, rowoff + c, nv, vec, g);
+        if constexpr (OPT) {
+            float m[8];
+            load8<ST>(P.mom, rowoff + c, nv, vec, m);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) m[e] = o.beta * m[e] + g[e];
-                store8<ST>(P.mom, rowoff + c, nv, vec, m);
+            for (int e = 0; e < 8; ++e) m[e] = o.beta * m[e] + g[e];
+            store8<ST>(P.mom, rowoff + c, nv, vec, m);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) g[e] = lookahead(g[e], m[e], o);
-            }
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc += (double)g[e] * (double)g[e];
+            for (int e = 0; e < 8; ++e) g[e] = lookahead(g[e], m[e], o);
         }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc += (double)g[e] * (double)g[e];
     }
     __shared__ double red[kThreads];
     red[threadIdx.x] = acc;

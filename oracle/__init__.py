@@ -14,6 +14,8 @@ taken as given, so callers that want the GPU's fp32 coefficients pass
 
 * ``phi_k(A, K, a, b, c)``          Φ_K(A), Sec. 2.2 incl. orientation rule.
 * ``ns_tiled(A, T, K, a, b, c)``    Φ_{K,T}(A), eq. (tiled_ns).
+* ``ns_tiled_hw(A, Th, Tw, K, a, b, c)``  the same map with Th×Tw tiles (the
+                                    tile-shape study's rectangular tiles).
 * ``ns_tiles(A, T, K, a, b, c, ids)`` selected tiles of Φ_{K,T}, each T×T.
 * ``tile_count(H, W, T)``           R·C of the tiling operator B_T.
 * ``himuon_step(W, M, G, T, K, a, b, c, lr, beta, wd, nesterov, scale_c)``
@@ -59,6 +61,8 @@ def _bind(lib):
     lib.oracle_ns_tile.restype = ctypes.c_int
     lib.oracle_ns_tiled.argtypes = [p, i64, i64, i64, i64, ctypes.c_int, d, d, d, p, i64]
     lib.oracle_ns_tiled.restype = ctypes.c_int
+    lib.oracle_ns_tiled_hw.argtypes = [p, i64, i64, i64, i64, i64, ctypes.c_int, d, d, d, p, i64]
+    lib.oracle_ns_tiled_hw.restype = ctypes.c_int
     lib.oracle_ns_tiles.argtypes = [p, i64, i64, i64, i64, ctypes.c_int, d, d, d, i64, p, p]
     lib.oracle_ns_tiles.restype = ctypes.c_int
     lib.oracle_himuon_step.argtypes = [p, p, p, i64, i64, i64, ctypes.c_int, d, d, d, d, d, d, ctypes.c_int,
@@ -112,6 +116,16 @@ def ns_tiled(A, T, K, a, b, c, lib=None):
     Y = np.empty_like(A)
     _check(lib.oracle_ns_tiled(A.ctypes.data, H, W, W, int(T), int(K), float(a), float(b), float(c),
                                Y.ctypes.data, W), "ns_tiled")
+    return Y
+
+
+def ns_tiled_hw(A, Th, Tw, K, a, b, c, lib=None):
+    lib = lib or load()
+    A = _f64(A)
+    H, W = A.shape
+    Y = np.empty_like(A)
+    _check(lib.oracle_ns_tiled_hw(A.ctypes.data, H, W, W, int(Th), int(Tw), int(K), float(a), float(b), float(c),
+                                  Y.ctypes.data, W), "ns_tiled_hw")
     return Y
 
 

@@ -130,51 +130,63 @@ int64_t oracle_tile_count(int64_t H, int64_t W, int64_t T)
 }
 
 /*
- * Phi_K of tile `tile_id` of B_T(A), returned as the full T x T tile Y
- * (padding included, contiguous). The tile is cut from the zero-padded
- * (RT) x (CT) matrix: entry (i, j) of tile (r, c) is A[rT+i][cT+j] when that
- * lies inside A and 0 otherwise.
+ * Rectangular tiles (T_h, T_w), used by the paper's tile-shape study (Sec.
+ * 2.1 with T_h x T_w blocks in place of T x T): A is zero-padded to
+ * (R T_h) x (C T_w), R = ceil(H/T_h), C = ceil(W/T_w), and cut into an R x C
+ * grid of T_h x T_w tiles; square tiles are the case T_h = T_w = T.
+ *
+ * Phi_K of tile `tile_id` of that tiling, returned as the full T_h x T_w
+ * tile Y (padding included, contiguous). Entry (i, j) of tile (r, c) is
+ * A[r T_h + i][c T_w + j] when that lies inside A and 0 otherwise. A tile
+ * with T_h > T_w goes through the orientation rule of oracle_phi_k.
  */
-int oracle_ns_tile(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t T,
-                   int64_t tile_id, int K, double a, double b, double c, double* Y)
+int oracle_ns_tile_hw(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t Th, int64_t Tw,
+                      int64_t tile_id, int K, double a, double b, double c, double* Y)
 {
-    if (!A || !Y || H < 1 || W < 1 || ld_in < W || T < 1 || K < 0) return ORACLE_BAD_ARG;
-    int64_t R = (H + T - 1) / T, C = (W + T - 1) / T;
+    if (!A || !Y || H < 1 || W < 1 || ld_in < W || Th < 1 || Tw < 1 || K < 0) return ORACLE_BAD_ARG;
+    int64_t R = (H + Th - 1) / Th, C = (W + Tw - 1) / Tw;
     if (tile_id < 0 || tile_id >= R * C) return ORACLE_BAD_ARG;
     int64_t r = tile_id / C, cc = tile_id % C;
-    double* S = (double*)malloc(sizeof(double) * T * T);
+    double* S = (double*)malloc(sizeof(double) * Th * Tw);
     if (!S) return ORACLE_NO_MEM;
-    for (int64_t i = 0; i < T; ++i)
-        for (int64_t j = 0; j < T; ++j) {
-            int64_t gi = r * T + i, gj = cc * T + j;
-            S[i * T + j] = (gi < H && gj < W) ? A[gi * ld_in + gj] : 0.0;
+    for (int64_t i = 0; i < Th; ++i)
+        for (int64_t j = 0; j < Tw; ++j) {
+            int64_t gi = r * Th + i, gj = cc * Tw + j;
+            S[i * Tw + j] = (gi < H && gj < W) ? A[gi * ld_in + gj] : 0.0;
         }
-    int st = oracle_phi_k(S, T, T, T, K, a, b, c, Y, T);
+    int st = oracle_phi_k(S, Th, Tw, Tw, K, a, b, c, Y, Tw);
     free(S);
     return st;
 }
 
-/*
- * Phi_{K,T}(A), eq. (tiled_ns): every tile of B_T(A) through Phi_K, then
- * B_T^{-1} (reassemble, drop the padding) into Y (H x W, leading dim ld_out).
- * Tiles are independent; they are spread over OpenMP threads.
- */
-int oracle_ns_tiled(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t T, int K,
-                    double a, double b, double c, double* Y, int64_t ld_out)
+/* Phi_K of tile `tile_id` of B_T(A): the square case T_h = T_w = T. */
+int oracle_ns_tile(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t T,
+                   int64_t tile_id, int K, double a, double b, double c, double* Y)
 {
-    if (!A || !Y || H < 1 || W < 1 || ld_in < W || ld_out < W || T < 1 || K < 0) return ORACLE_BAD_ARG;
-    int64_t R = (H + T - 1) / T, C = (W + T - 1) / T;
+    return oracle_ns_tile_hw(A, H, W, ld_in, T, T, tile_id, K, a, b, c, Y);
+}
+
+/*
+ * The tiled map with T_h x T_w tiles: every tile through Phi_K, then the
+ * tiles reassembled and the padding dropped, into Y (H x W, leading dim
+ * ld_out). Tiles are independent; they are spread over OpenMP threads.
+ */
+int oracle_ns_tiled_hw(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t Th, int64_t Tw, int K,
+                       double a, double b, double c, double* Y, int64_t ld_out)
+{
+    if (!A || !Y || H < 1 || W < 1 || ld_in < W || ld_out < W || Th < 1 || Tw < 1 || K < 0) return ORACLE_BAD_ARG;
+    int64_t R = (H + Th - 1) / Th, C = (W + Tw - 1) / Tw;
     int status = ORACLE_OK;
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t t = 0; t < R * C; ++t) {
-        double* Yt = (double*)malloc(sizeof(double) * T * T);
-        int st = Yt ? oracle_ns_tile(A, H, W, ld_in, T, t, K, a, b, c, Yt) : ORACLE_NO_MEM;
+        double* Yt = (double*)malloc(sizeof(double) * Th * Tw);
+        int st = Yt ? oracle_ns_tile_hw(A, H, W, ld_in, Th, Tw, t, K, a, b, c, Yt) : ORACLE_NO_MEM;
         if (st == ORACLE_OK) {
             int64_t r = t / C, cc = t % C;
-            for (int64_t i = 0; i < T; ++i)
-                for (int64_t j = 0; j < T; ++j) {
-                    int64_t gi = r * T + i, gj = cc * T + j;
-                    if (gi < H && gj < W) Y[gi * ld_out + gj] = Yt[i * T + j];
+            for (int64_t i = 0; i < Th; ++i)
+                for (int64_t j = 0; j < Tw; ++j) {
+                    int64_t gi = r * Th + i, gj = cc * Tw + j;
+                    if (gi < H && gj < W) Y[gi * ld_out + gj] = Yt[i * Tw + j];
                 }
         } else {
 #pragma omp critical
@@ -183,6 +195,16 @@ int oracle_ns_tiled(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_
         free(Yt);
     }
     return status;
+}
+
+/*
+ * Phi_{K,T}(A), eq. (tiled_ns): every tile of B_T(A) through Phi_K, then
+ * B_T^{-1} (reassemble, drop the padding): the square case of the above.
+ */
+int oracle_ns_tiled(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_t T, int K,
+                    double a, double b, double c, double* Y, int64_t ld_out)
+{
+    return oracle_ns_tiled_hw(A, H, W, ld_in, T, T, K, a, b, c, Y, ld_out);
 }
 
 /*

@@ -17,6 +17,7 @@ relative error it saw. The routes:
   orthogonal equivariance, odd homogeneity of degree 0, tile permutation;
 * the textbook special case: cubic Newton–Schulz (1.5, −0.5, 0) converges to
   the polar factor (``scipy.linalg.polar``) for well-conditioned input;
+* rectangular tiles: the same slicing with T_h x T_w blocks;
 * for the optimizer step of Alg. 1: geometric sums over repeated steps with a
   constant gradient (the momentum buffer and the decayed weights have closed
   forms, and Φ_K is blind to positive scaling), the sign of the second
@@ -269,6 +270,29 @@ def pin_tile_count(lib=None):
     return float(bad)
 
 
+def pin_rect_tiled_blocks(lib=None):
+    """Rectangular tiles (the tile-shape study): pad to (R T_h) x (C T_w) by
+    numpy, cut T_h x T_w blocks, each by the SVD closed form (which needs no
+    orientation choice); tall and wide tiles, ragged edges, and one tile
+    covering the matrix (the full map)."""
+    g = np.random.default_rng(31)
+    worst = 0.0
+    for (H, W, Th, Tw) in [(100, 150, 32, 64), (100, 150, 64, 16), (70, 45, 48, 48), (37, 90, 40, 100),
+                           (90, 37, 16, 8)]:
+        S = g.standard_normal((H, W))
+        Y = oracle.ns_tiled_hw(S, Th, Tw, 5, *QUINTIC, lib=lib)
+        R, C = -(-H // Th), -(-W // Tw)
+        P = np.zeros((R * Th, C * Tw))
+        P[:H, :W] = S
+        Ref = np.zeros_like(P)
+        for r in range(R):
+            for q in range(C):
+                blk = np.s_[r * Th:(r + 1) * Th, q * Tw:(q + 1) * Tw]
+                Ref[blk] = svd_closed_form(P[blk], 5)
+        worst = max(worst, rel(Y, Ref[:H, :W]))
+    return worst
+
+
 STEP = dict(a=QUINTIC[0], b=QUINTIC[1], c=QUINTIC[2], K=5)
 
 
@@ -351,7 +375,7 @@ PINS = [
     pin_svd_closed_form, pin_tiled_blocks, pin_sampled_tiles, pin_rank_one, pin_scaled_orthogonal,
     pin_diagonal, pin_zero, pin_special_coefficients, pin_cubic_polar, pin_invariances,
     pin_tile_permutation, pin_single_tile_is_full_map, pin_tile_count,
-    pin_step_constant_gradient, pin_step_nesterov_sign, pin_step_scale_branch,
+    pin_step_constant_gradient, pin_step_nesterov_sign, pin_step_scale_branch, pin_rect_tiled_blocks,
 ]
 
 

@@ -26,8 +26,10 @@ MUTATIONS = [
     ("pad_with_ones", "? A[gi * ld_in + gj] : 0.0;", "? A[gi * ld_in + gj] : 1.0;"),
     ("tile_index_colmajor", "int64_t r = tile_id / C, cc = tile_id % C;",
      "int64_t r = tile_id % R, cc = tile_id / R;"),
-    ("floor_tile_count", "    int64_t R = (H + T - 1) / T, C = (W + T - 1) / T;\n    int status",
-     "    int64_t R = H / T, C = W / T;\n    int status"),
+    ("floor_tile_count", "    int64_t R = (H + Th - 1) / Th, C = (W + Tw - 1) / Tw;\n    int status",
+     "    int64_t R = H / Th, C = W / Tw;\n    int status"),
+    ("rect_tile_rows_cols_swapped", "int64_t gi = r * Th + i, gj = cc * Tw + j;\n            S[",
+     "int64_t gi = r * Tw + i, gj = cc * Th + j;\n            S["),
     ("zero_tile_not_zero", "if (nrm == 0.0) {", "if (nrm < 0.0) {"),
     ("step_momentum_no_beta", "Mt[i] = beta * Mt[i] + G[i];", "Mt[i] = Mt[i] + G[i];"),
     ("step_nesterov_old_buffer",

@@ -137,26 +137,33 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
     the GEMMs issue (no symmetry is exploited on this path)."""
     rows = [x.shape[0] for x in mats]
     cols = [x.shape[1] for x in mats]
+    Th, Tw = args.T, (args.T if args.Tw is None else args.Tw)
     if args.T == 0:
         flops_step = sum((4.0 * min(h, w) ** 2 * max(h, w) + 2.0 * min(h, w) ** 3) * args.K for h, w in zip(rows, cols))
         metric = "full-matrix NS TFLOP/s ((4m^2n + 2m^3)K, m = min(H,W)), 7B layer stack K=%d" % args.K
-    else:
+    elif Th == Tw:
         flops_step = sum(6.0 * h * w * args.T * args.K for h, w in zip(rows, cols))
         metric = "tiled-NS TFLOP/s (6*H*W*T*K) + %% bf16 MFMA peak, 7B layer stack T=%d K=%d (library GEMMs)" % (args.T, args.K)
-    need = hm.himuon_ns_gemm_workspace_size(rows, cols, args.T, code, compute, args.K, *coeffs, int(args.budget))
+    else:
+        # per tile and step (4 m^2 n + 2 m^3), m = min(Th, Tw), n = max: per entry (4m + 2m^2/n)
+        m, n = min(Th, Tw), max(Th, Tw)
+        flops_step = sum((4.0 * m + 2.0 * m * m / n) * h * w * args.K for h, w in zip(rows, cols))
+        metric = ("tiled-NS TFLOP/s ((4m^2n + 2m^3)K per tile), 7B layer stack %dx%d tiles K=%d (library GEMMs)"
+                  % (Th, Tw, args.K))
+    need = hm.himuon_ns_gemm_hw_workspace_size(rows, cols, Th, Tw, code, compute, args.K, *coeffs, int(args.budget))
     if need == 0:
         raise SystemExit("no plan for this call (budget below one problem?)")
     log(f"gemm path workspace {need / 2**30:.2f} GiB")
     ws = torch.empty(need, dtype=torch.uint8, device=mats[0].device)
     if args.tune:
         t0 = time.perf_counter()
-        hm.gemm_tune(list(zip(rows, cols)), args.T, code, K=args.K, coeffs=coeffs, compute=compute,
-                     chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
+        hm.gemm_tune(list(zip(rows, cols)), Th, code, K=args.K, coeffs=coeffs, compute=compute,
+                     chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream, Tw=Tw)
         log(f"GEMM candidates timed in {time.perf_counter() - t0:.1f} s")
 
     def step():
-        hm.ns_gemm(mats, outputs=outs, T=args.T, K=args.K, coeffs=coeffs, compute=compute,
-                   chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
+        hm.ns_gemm(mats, outputs=outs, T=Th, K=args.K, coeffs=coeffs, compute=compute,
+                   chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream, Tw=Tw)
 
     for _ in range(args.warmup):
         step()
@@ -177,7 +184,7 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
         "metric": metric, "value": round(flops_step / (wall / args.steps) / 1e12, 3), "unit": "TFLOP/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": op_name, "data": "synthetic",
-        "config": {"workload": desc, "path": "gemm", "T": args.T, "K": args.K, "matrices": len(mats),
+        "config": {"workload": desc, "path": "gemm", "T": args.T, "Tw": Tw, "K": args.K, "matrices": len(mats),
                    "storage": args.dtype, "mfma_operands": op_name, "accumulate": "f32",
                    "chunk_budget_bytes": int(args.budget), "workspace_bytes": need, "gemm_tuned": bool(args.tune)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
@@ -279,6 +286,8 @@ def main():
     ap.add_argument("--workload", default="stack7b", choices=["stack7b", "layer7b", "square4096", "hetero"])
     ap.add_argument("--T", type=int, default=128)
     ap.add_argument("--K", type=int, default=5)
+    ap.add_argument("--Tw", type=int, default=None,
+                    help="--path gemm: tile width (tiles are T x Tw; default square)")
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--compute", default="default", choices=["default", "f16", "bf16", "f32"])
     ap.add_argument("--budget", type=float, default=16e9, help="chunk budget in bytes (0: one chunk)")

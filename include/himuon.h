@@ -168,6 +168,31 @@ int himuon_ns_gemm(int64_t n_mats,
                    void* stream);
 
 /*
+ * himuon_ns_gemm with rectangular Th x Tw tiles (the tile-shape study of
+ * Sec. 5 and Sec. 2.1's tiling with T_h x T_w blocks): each matrix is padded
+ * to (R Th) x (C Tw), R = ceil(H/Th), C = ceil(W/Tw), and every tile goes
+ * through Phi_K, a tile with Th > Tw by the orientation rule (its transpose
+ * is iterated, so the Gram matrix is min(Th, Tw) square). Th = Tw = T is
+ * himuon_ns_gemm; Th = Tw = 0 is the full-matrix branch; exactly one of them
+ * zero is HIMUON_ERR_INVALID_ARG. A matrix that one tile covers (Th >= H and
+ * Tw >= W) is worked on whole. Other arguments, workspace and errors as
+ * himuon_ns_gemm.
+ */
+size_t himuon_ns_gemm_hw_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols,
+                                        int Th, int Tw, int dtype, int compute, int K,
+                                        float a, float b, float c, size_t chunk_budget_bytes);
+
+int himuon_ns_gemm_hw(int64_t n_mats,
+                      const void* const* in_ptrs, void* const* out_ptrs,
+                      const int64_t* rows, const int64_t* cols,
+                      const int64_t* ld_in, const int64_t* ld_out,
+                      int Th, int Tw, int K, float a, float b, float c,
+                      int dtype, int compute,
+                      void* workspace, size_t workspace_bytes,
+                      size_t chunk_budget_bytes,
+                      void* stream);
+
+/*
  * Picks, for every GEMM that a himuon_ns_gemm (or GEMM-route himuon_step)
  * call with these shapes and arguments would run, the fastest of the GEMM
  * library's leading heuristic candidates (up to 8), by timing each on the
@@ -185,6 +210,12 @@ int himuon_gemm_tune(int64_t n_mats, const int64_t* rows, const int64_t* cols, i
                      int dtype, int compute, int K, float a, float b, float c,
                      void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
                      void* stream);
+
+/* himuon_gemm_tune for the Th x Tw tilings of himuon_ns_gemm_hw. */
+int himuon_gemm_tune_hw(int64_t n_mats, const int64_t* rows, const int64_t* cols, int Th, int Tw,
+                        int dtype, int compute, int K, float a, float b, float c,
+                        void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
+                        void* stream);
 
 /*
  * One HiMuon optimizer step (Alg. 1) on n_mats parameter matrices, in place:

@@ -68,6 +68,15 @@ def lib():
         L.himuon_gemm_tune.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        f, f, f, vp, sz, sz, vp]
         L.himuon_gemm_tune.restype = ctypes.c_int
+        L.himuon_gemm_tune_hw.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_int, f, f, f, vp, sz, sz, vp]
+        L.himuon_gemm_tune_hw.restype = ctypes.c_int
+        L.himuon_ns_gemm_hw_workspace_size.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                       ctypes.c_int, ctypes.c_int, f, f, f, sz]
+        L.himuon_ns_gemm_hw_workspace_size.restype = sz
+        L.himuon_ns_gemm_hw.argtypes = [i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                        f, f, f, ctypes.c_int, ctypes.c_int, vp, sz, sz, vp]
+        L.himuon_ns_gemm_hw.restype = ctypes.c_int
         L.himuon_plan_chunks.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, sz, vp, vp, vp, i64]
         L.himuon_plan_chunks.restype = ctypes.c_int
         L.himuon_select_compute.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -148,6 +157,33 @@ def himuon_step(n_mats, weights, grads, moms, rows, cols, ld, T, K, a, b, c, lr,
         int(chunk_budget_bytes), int(stream) if stream else None))
 
 
+def himuon_ns_gemm_hw_workspace_size(rows, cols, Th, Tw, dtype, compute, K, a, b, c, chunk_budget_bytes=0) -> int:
+    """Workspace bytes of a himuon_ns_gemm_hw call (0 on an invalid plan)."""
+    return int(lib().himuon_ns_gemm_hw_workspace_size(
+        len(rows), _i64_array(rows), _i64_array(cols), int(Th), int(Tw), int(dtype), int(compute), int(K),
+        float(a), float(b), float(c), int(chunk_budget_bytes)))
+
+
+def himuon_ns_gemm_hw(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, Th, Tw, K, a, b, c,
+                      dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream) -> int:
+    """Same arguments as the C function (see himuon_ns_tiled). Returns the status code."""
+    return int(lib().himuon_ns_gemm_hw(
+        int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
+        None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
+        int(Th), int(Tw), int(K), float(a), float(b), float(c), int(dtype), int(compute),
+        int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes),
+        int(stream) if stream else None))
+
+
+def himuon_gemm_tune_hw(rows, cols, Th, Tw, dtype, compute, K, a, b, c, workspace, workspace_bytes,
+                        chunk_budget_bytes=0, stream=None) -> int:
+    """Same arguments as the C function. Returns the status code."""
+    return int(lib().himuon_gemm_tune_hw(
+        len(rows), _i64_array(rows), _i64_array(cols), int(Th), int(Tw), int(dtype), int(compute), int(K),
+        float(a), float(b), float(c), int(workspace) if workspace else None, int(workspace_bytes),
+        int(chunk_budget_bytes), int(stream) if stream else None))
+
+
 def himuon_gemm_tune(rows, cols, T, dtype, compute, K, a, b, c, workspace, workspace_bytes,
                      chunk_budget_bytes=0, stream=None) -> int:
     """Same arguments as the C function (``workspace`` a device pointer). Returns the status code."""
@@ -158,25 +194,26 @@ def himuon_gemm_tune(rows, cols, T, dtype, compute, K, a, b, c, workspace, works
 
 
 def gemm_tune(shapes, T, dtype, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0,
-              workspace=None, stream=None, device="cuda"):
+              workspace=None, stream=None, device="cuda", Tw=None):
     """Time the GEMM library's candidates for the GEMM-path calls over matrices
-    of these ``(rows, cols)`` shapes (T = 0 or large tiles) and keep the
-    fastest; synchronises. ``dtype`` is F32 or BF16."""
+    of these ``(rows, cols)`` shapes (T = 0, square T x T tiles, or T x Tw
+    tiles) and keep the fastest; synchronises. ``dtype`` is F32 or BF16."""
     import torch
     a, b, c = coeffs
+    Th, Tw = int(T), int(T if Tw is None else Tw)
     rows = [int(h) for h, _ in shapes]
     cols = [int(w) for _, w in shapes]
-    need = himuon_ns_gemm_workspace_size(rows, cols, T, dtype, compute, K, a, b, c, chunk_budget_bytes)
+    need = himuon_ns_gemm_hw_workspace_size(rows, cols, Th, Tw, dtype, compute, K, a, b, c, chunk_budget_bytes)
     if need == 0:
-        raise HimuonError(ERR_INVALID_ARG, "himuon_ns_gemm_workspace_size")
+        raise HimuonError(ERR_INVALID_ARG, "himuon_ns_gemm_hw_workspace_size")
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=device)
     if stream is None:
         stream = torch.cuda.current_stream(workspace.device)
-    st = himuon_gemm_tune(rows, cols, T, dtype, compute, K, a, b, c, workspace.data_ptr(),
-                          workspace.numel() * workspace.element_size(), chunk_budget_bytes, stream.cuda_stream)
+    st = himuon_gemm_tune_hw(rows, cols, Th, Tw, dtype, compute, K, a, b, c, workspace.data_ptr(),
+                             workspace.numel() * workspace.element_size(), chunk_budget_bytes, stream.cuda_stream)
     if st != OK:
-        raise HimuonError(st, "himuon_gemm_tune")
+        raise HimuonError(st, "himuon_gemm_tune_hw")
 
 
 def himuon_plan_chunks(rows, cols, T, dtype=BF16, chunk_budget_bytes=0):
@@ -268,11 +305,12 @@ def ns_tiled(inputs, outputs=None, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_D
 
 
 def ns_gemm(inputs, outputs=None, T=0, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT,
-            chunk_budget_bytes=0, workspace=None, stream=None):
+            chunk_budget_bytes=0, workspace=None, stream=None, Tw=None):
     """Phi_K of every whole matrix (T = 0) or Phi_{K,T} with T x T tiles
-    (T >= 1, e.g. 512) through library GEMMs, in one call. Arguments and
-    return value as ``ns_tiled``; ``workspace`` (if given) must hold
-    ``himuon_ns_gemm_workspace_size`` bytes for these shapes."""
+    (T >= 1, e.g. 512) through library GEMMs, in one call; with ``Tw`` the
+    tiles are T x Tw (rows x columns). Arguments and return value as
+    ``ns_tiled``; ``workspace`` (if given) must hold
+    ``himuon_ns_gemm_hw_workspace_size`` bytes for these shapes."""
     import torch
     inputs = list(inputs)
     if not inputs:
@@ -294,20 +332,21 @@ def ns_gemm(inputs, outputs=None, T=0, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFA
     a, b, c = coeffs
     rows = [x.shape[0] for x in inputs]
     cols = [x.shape[1] for x in inputs]
-    need = himuon_ns_gemm_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
+    Th, Tw = int(T), int(T if Tw is None else Tw)
+    need = himuon_ns_gemm_hw_workspace_size(rows, cols, Th, Tw, code, compute, K, a, b, c, chunk_budget_bytes)
     if need == 0:
-        raise HimuonError(ERR_INVALID_ARG, "himuon_ns_gemm_workspace_size")
+        raise HimuonError(ERR_INVALID_ARG, "himuon_ns_gemm_hw_workspace_size")
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
-    st = himuon_ns_gemm(
+    st = himuon_ns_gemm_hw(
         n, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs], rows, cols,
         [x.stride(0) for x in inputs], [y.stride(0) for y in outputs],
-        T, K, a, b, c, code, compute, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+        Th, Tw, K, a, b, c, code, compute, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
         chunk_budget_bytes, stream.cuda_stream)
     if st != OK:
-        raise HimuonError(st, "himuon_ns_gemm")
+        raise HimuonError(st, "himuon_ns_gemm_hw")
     return outputs
 
 

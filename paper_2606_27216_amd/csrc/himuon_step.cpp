@@ -95,7 +95,7 @@ size_t himuon_step_workspace_size(int64_t n_mats, const int64_t* rows, const int
         if (plan_step_groups(n_mats, rows, cols, dtype, chunk_budget_bytes, &bounds, &buf_max) != HIMUON_OK) return 0;
         return fused_route_workspace(n_mats, buf_max);
     }
-    return himuon::gemm_path_workspace(n_mats, rows, cols, T, dtype, compute, K, a, b, c, chunk_budget_bytes);
+    return himuon::gemm_path_workspace(n_mats, rows, cols, T, T, dtype, compute, K, a, b, c, chunk_budget_bytes);
 }
 
 int himuon_step(int64_t n_mats, void* const* weights, const void* const* grads, void* const* moms,
@@ -135,7 +135,7 @@ int himuon_step(int64_t n_mats, void* const* weights, const void* const* grads, 
             lds[(size_t)l] = ld ? ld[l] : cols[l];
         }
         return himuon::run_gemm_path(n_mats, in.data(), weights, moms, tau.data(), rows, cols, lds.data(), lds.data(),
-                                     T, K, a, b, c, dtype, compute, workspace, workspace_bytes, chunk_budget_bytes,
+                                     T, T, K, a, b, c, dtype, compute, workspace, workspace_bytes, chunk_budget_bytes,
                                      stream, &opt);
     }
 

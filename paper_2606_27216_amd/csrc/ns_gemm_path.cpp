@@ -63,32 +63,37 @@ struct Group {
 
 int group_nparts(int n) { return (int)std::min<int64_t>(256, std::max<int64_t>(1, ceil_div(n, 64))); }
 
-// A matrix is one whole problem when T = 0 (the branch T = infinity) or
-// T >= max(H, W): the tiling operator then gives a single padded tile, and
-// Phi_K of a zero-padded matrix is the padded Phi_K of the matrix (Sec.
-// 4.4.3), so the smaller unpadded problem is worked on instead.
-bool whole_matrix(int64_t rows, int64_t cols, int T) { return T == 0 || T >= std::max(rows, cols); }
+// Tiles are Th x Tw (square: Th = Tw = T; rectangular tiles are the
+// tile-shape study's); Th = Tw = 0 stands for T = infinity. A matrix is one
+// whole problem on that branch or when one tile covers it (Th >= H and
+// Tw >= W): the tiling operator then gives a single padded tile, and Phi_K
+// of a zero-padded matrix is the padded Phi_K of the matrix (Sec. 4.4.3), so
+// the smaller unpadded problem is worked on instead.
+bool whole_matrix(int64_t rows, int64_t cols, int Th, int Tw) { return Th == 0 || (Th >= rows && Tw >= cols); }
+
+bool valid_tiling(int Th, int Tw) { return Th >= 0 && Tw >= 0 && (Th == 0) == (Tw == 0); }
 
 // Groups (in order of first appearance) and, when `probs` is given, the
 // problem list in group order. Whole matrices: one problem each; otherwise
 // the R x C tiles of the matrix, row-major.
-int plan_groups(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, std::vector<Group>& groups,
+int plan_groups(int64_t n_mats, const int64_t* rows, const int64_t* cols, int Th, int Tw, std::vector<Group>& groups,
                 std::vector<std::vector<int64_t>>* members)
 {
-    if (n_mats < 1 || !rows || !cols || T < 0) return HIMUON_ERR_INVALID_ARG;
+    if (n_mats < 1 || !rows || !cols || !valid_tiling(Th, Tw)) return HIMUON_ERR_INVALID_ARG;
     groups.clear();
     std::map<std::pair<int, int>, size_t> index;
     std::vector<std::vector<int64_t>> mem;
     for (int64_t l = 0; l < n_mats; ++l) {
         if (rows[l] < 1 || cols[l] < 1) return HIMUON_ERR_INVALID_ARG;
         int64_t m, n, cnt;
-        if (whole_matrix(rows[l], cols[l], T)) {
+        if (whole_matrix(rows[l], cols[l], Th, Tw)) {
             m = std::min(rows[l], cols[l]);
             n = std::max(rows[l], cols[l]);
             cnt = 1;
         } else {
-            m = n = T;
-            cnt = ceil_div(rows[l], T) * ceil_div(cols[l], T);
+            m = std::min(Th, Tw);
+            n = std::max(Th, Tw);
+            cnt = ceil_div(rows[l], Th) * ceil_div(cols[l], Tw);
         }
         if (m > 32768 || n > INT32_MAX / 32) return HIMUON_ERR_UNSUPPORTED;
         const auto key = std::make_pair((int)m, (int)n);
@@ -308,13 +313,13 @@ namespace himuon {
 
 int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, void* const* mom_ptrs,
                   const float* tau, const int64_t* rows, const int64_t* cols, const int64_t* ld_in,
-                  const int64_t* ld_out, int T, int K, float a, float b, float c, int dtype, int compute,
+                  const int64_t* ld_out, int Th, int Tw, int K, float a, float b, float c, int dtype, int compute,
                   void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes, void* stream,
                   const OptArgs* opt)
 {
     // ---- validation and plan: nothing is enqueued unless every check passes
     if (n_mats < 1 || n_mats > INT32_MAX || !in_ptrs || !out_ptrs || !rows || !cols) return HIMUON_ERR_INVALID_ARG;
-    if (K < 0 || T < 0 || !isfinite(a) || !isfinite(b) || !isfinite(c)) return HIMUON_ERR_INVALID_ARG;
+    if (K < 0 || !valid_tiling(Th, Tw) || !isfinite(a) || !isfinite(b) || !isfinite(c)) return HIMUON_ERR_INVALID_ARG;
     if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
     if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
     for (int64_t l = 0; l < n_mats; ++l) {
@@ -328,7 +333,7 @@ int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_p
     }
     std::vector<Group> groups;
     std::vector<std::vector<int64_t>> members;
-    int st = plan_groups(n_mats, rows, cols, T, groups, &members);
+    int st = plan_groups(n_mats, rows, cols, Th, Tw, groups, &members);
     if (st != HIMUON_OK) return st;
     int m_max = 0;
     for (const Group& g : groups) m_max = std::max(m_max, g.m);
@@ -355,28 +360,28 @@ int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_p
             p.ld_out = ld_out ? ld_out[l] : cols[l];
             p.mom = opt ? mom_ptrs[l] : nullptr;
             p.tau = opt ? tau[l] : 0.f;
-            // 16-byte chunks at every 8th column of a block (block origins are multiples of T)
+            // 16-byte chunks at every 8th column of a block (block origins are multiples of Tw)
             const int64_t mult = dtype == HIMUON_BF16 ? 8 : 4;
-            const bool origins = T == 0 || T % 8 == 0;
+            const bool origins = Tw % 8 == 0;
             const bool vin = origins && (uintptr_t)p.in % 16 == 0 && p.ld_in % mult == 0 &&
                              (!opt || (uintptr_t)p.mom % 16 == 0);
             const bool vout = origins && (uintptr_t)p.out % 16 == 0 && p.ld_out % mult == 0;
             p.vec = (vin ? himuon::GEMM_VEC_IN : 0) | (vout ? himuon::GEMM_VEC_OUT : 0);
-            if (whole_matrix(rows[l], cols[l], T)) {
+            if (whole_matrix(rows[l], cols[l], Th, Tw)) {
                 p.row0 = p.col0 = 0;
                 p.h = (int32_t)rows[l];
                 p.w = (int32_t)cols[l];
                 p.trans = rows[l] > cols[l] ? 1 : 0;
                 probs.push_back(p);
             } else {
-                const int64_t R = ceil_div(rows[l], T), C = ceil_div(cols[l], T);
-                p.trans = 0;
+                const int64_t R = ceil_div(rows[l], Th), C = ceil_div(cols[l], Tw);
+                p.trans = Th > Tw ? 1 : 0;  // the orientation rule on a tall tile
                 for (int64_t r = 0; r < R; ++r)
                     for (int64_t q = 0; q < C; ++q) {
-                        p.row0 = r * T;
-                        p.col0 = q * T;
-                        p.h = (int32_t)std::min<int64_t>(T, rows[l] - r * T);
-                        p.w = (int32_t)std::min<int64_t>(T, cols[l] - q * T);
+                        p.row0 = r * Th;
+                        p.col0 = q * Tw;
+                        p.h = (int32_t)std::min<int64_t>(Th, rows[l] - r * Th);
+                        p.w = (int32_t)std::min<int64_t>(Tw, cols[l] - q * Tw);
                         probs.push_back(p);
                     }
             }
@@ -462,11 +467,11 @@ int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_p
     return status;
 }
 
-size_t gemm_path_workspace(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype, int compute,
+size_t gemm_path_workspace(int64_t n_mats, const int64_t* rows, const int64_t* cols, int Th, int Tw, int dtype, int compute,
                            int K, float a, float b, float c, size_t chunk_budget_bytes)
 {
     std::vector<Group> groups;
-    if (plan_groups(n_mats, rows, cols, T, groups, nullptr) != HIMUON_OK) return 0;
+    if (plan_groups(n_mats, rows, cols, Th, Tw, groups, nullptr) != HIMUON_OK) return 0;
     int m_max = 0;
     for (const Group& g : groups) m_max = std::max(m_max, g.m);
     GemmOperand op;
@@ -481,10 +486,27 @@ size_t gemm_path_workspace(int64_t n_mats, const int64_t* rows, const int64_t* c
 
 extern "C" {
 
+size_t himuon_ns_gemm_hw_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols, int Th, int Tw,
+                                        int dtype, int compute, int K, float a, float b, float c,
+                                        size_t chunk_budget_bytes)
+{
+    return himuon::gemm_path_workspace(n_mats, rows, cols, Th, Tw, dtype, compute, K, a, b, c, chunk_budget_bytes);
+}
+
 size_t himuon_ns_gemm_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
                                      int compute, int K, float a, float b, float c, size_t chunk_budget_bytes)
 {
-    return himuon::gemm_path_workspace(n_mats, rows, cols, T, dtype, compute, K, a, b, c, chunk_budget_bytes);
+    if (T < 0) return 0;
+    return himuon::gemm_path_workspace(n_mats, rows, cols, T, T, dtype, compute, K, a, b, c, chunk_budget_bytes);
+}
+
+int himuon_ns_gemm_hw(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+                      const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int Th, int Tw, int K, float a,
+                      float b, float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
+                      size_t chunk_budget_bytes, void* stream)
+{
+    return himuon::run_gemm_path(n_mats, in_ptrs, out_ptrs, nullptr, nullptr, rows, cols, ld_in, ld_out, Th, Tw, K, a,
+                                 b, c, dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream, nullptr);
 }
 
 int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
@@ -492,21 +514,23 @@ int himuon_ns_gemm(int64_t n_mats, const void* const* in_ptrs, void* const* out_
                    float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
                    size_t chunk_budget_bytes, void* stream)
 {
-    return himuon::run_gemm_path(n_mats, in_ptrs, out_ptrs, nullptr, nullptr, rows, cols, ld_in, ld_out, T, K, a, b, c,
-                                 dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream, nullptr);
+    if (T < 0) return HIMUON_ERR_INVALID_ARG;
+    return himuon::run_gemm_path(n_mats, in_ptrs, out_ptrs, nullptr, nullptr, rows, cols, ld_in, ld_out, T, T, K, a, b,
+                                 c, dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream, nullptr);
 }
 
 
-int himuon_gemm_tune(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype, int compute, int K,
-                     float a, float b, float c, void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
-                     void* stream)
+int himuon_gemm_tune_hw(int64_t n_mats, const int64_t* rows, const int64_t* cols, int Th, int Tw, int dtype,
+                        int compute, int K, float a, float b, float c, void* workspace, size_t workspace_bytes,
+                        size_t chunk_budget_bytes, void* stream)
 {
-    if (n_mats < 1 || !rows || !cols || K < 0 || T < 0 || !isfinite(a) || !isfinite(b) || !isfinite(c))
+    if (n_mats < 1 || !rows || !cols || K < 0 || !valid_tiling(Th, Tw) || !isfinite(a) || !isfinite(b) ||
+        !isfinite(c))
         return HIMUON_ERR_INVALID_ARG;
     if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
     if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
     std::vector<Group> groups;
-    int st = plan_groups(n_mats, rows, cols, T, groups, nullptr);
+    int st = plan_groups(n_mats, rows, cols, Th, Tw, groups, nullptr);
     if (st != HIMUON_OK) return st;
     int m_max = 0;
     int64_t total = 0;
@@ -572,6 +596,15 @@ int himuon_gemm_tune(int64_t n_mats, const int64_t* rows, const int64_t* cols, i
     (void)hipEventDestroy(e1);
     if (dev != cur) (void)hipSetDevice(cur);
     return st;
+}
+
+int himuon_gemm_tune(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype, int compute, int K,
+                     float a, float b, float c, void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
+                     void* stream)
+{
+    if (T < 0) return HIMUON_ERR_INVALID_ARG;
+    return himuon_gemm_tune_hw(n_mats, rows, cols, T, T, dtype, compute, K, a, b, c, workspace, workspace_bytes,
+                               chunk_budget_bytes, stream);
 }
 
 }  // extern "C"

@@ -67,15 +67,16 @@ hipError_t launch_gemm_gather(GemmStore st, GemmOperand op, const GemmProb* prob
 hipError_t launch_gemm_scatter(GemmStore st, GemmOperand op, const GemmProb* probs, int nprob, int m, int n,
                                float inv_scale, const void* x, const OptArgs* opt, hipStream_t stream);
 
-// Core of himuon_ns_gemm and of the optimizer step on the GEMM path (`opt`
-// null: Phi of `in` into `out`). Returns a himuon status.
+// Core of himuon_ns_gemm(_hw) and of the optimizer step on the GEMM path
+// (`opt` null: Phi of `in` into `out`), with Th x Tw tiles (0 x 0: whole
+// matrices). Returns a himuon status.
 int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, void* const* mom_ptrs,
                   const float* tau, const int64_t* rows, const int64_t* cols, const int64_t* ld_in,
-                  const int64_t* ld_out, int T, int K, float a, float b, float c, int dtype, int compute,
+                  const int64_t* ld_out, int Th, int Tw, int K, float a, float b, float c, int dtype, int compute,
                   void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes, void* stream,
                   const OptArgs* opt);
 // Workspace of run_gemm_path (0 when the call has no plan).
-size_t gemm_path_workspace(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype, int compute,
-                           int K, float a, float b, float c, size_t chunk_budget_bytes);
+size_t gemm_path_workspace(int64_t n_mats, const int64_t* rows, const int64_t* cols, int Th, int Tw, int dtype,
+                           int compute, int K, float a, float b, float c, size_t chunk_budget_bytes);
 
 }  // namespace himuon

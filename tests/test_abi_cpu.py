@@ -269,3 +269,27 @@ def test_gemm_tune_validation_rejects_before_any_hip_call(kw, status):
                 c=2.0315, workspace=FAKE, workspace_bytes=256, chunk_budget_bytes=0, stream=None)
     args.update(kw)
     assert hm.himuon_gemm_tune(**args) == status
+
+
+def test_gemm_hw_workspace_and_validation():
+    a, b, c = hm.QUINTIC
+    ws = lambda rows, cols, Th, Tw, budget=0: \
+        hm.himuon_ns_gemm_hw_workspace_size(rows, cols, Th, Tw, hm.BF16, hm.COMPUTE_DEFAULT, 5, a, b, c, budget)
+    lt = 64 << 20
+    # square tiles: the same plan as himuon_ns_gemm
+    assert ws([1024], [1024], 512, 512) == hm.himuon_ns_gemm_workspace_size([1024], [1024], 512, hm.BF16, 0, 5, a, b, c)
+    # a tall and a wide tile of the same size are one (m, n) problem shape: the same workspace
+    assert ws([1024], [1024], 256, 128) == ws([1024], [1024], 128, 256) > lt
+    # 32 tiles of 128 x 256: X, X' (128 x 256) and A, B (128 x 128) in fp16 per tile
+    need = ws([1024], [1024], 128, 256)
+    assert need >= lt + 32 * (2 * 128 * 256 + 2 * 128 * 128) * 2
+    # one tile covering the matrix is the whole matrix: the T = 0 plan
+    assert ws([300], [500], 512, 600) == ws([300], [500], 0, 0)
+    # exactly one of Th, Tw zero, or negative, has no plan
+    assert ws([64], [64], 0, 64) == 0 and ws([64], [64], 64, 0) == 0 and ws([64], [64], -1, 64) == 0
+    args = dict(n_mats=1, in_ptrs=[FAKE], out_ptrs=[FAKE], rows=[64], cols=[64], ld_in=None, ld_out=None, Th=0, Tw=32,
+                K=5, a=a, b=b, c=c, dtype=hm.BF16, compute=hm.COMPUTE_DEFAULT, workspace=FAKE, workspace_bytes=256,
+                chunk_budget_bytes=0, stream=None)
+    assert hm.himuon_ns_gemm_hw(**args) == hm.ERR_INVALID_ARG
+    args.update(Th=32, Tw=64)
+    assert hm.himuon_ns_gemm_hw(**args) == hm.ERR_WORKSPACE

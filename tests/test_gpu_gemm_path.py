@@ -124,3 +124,39 @@ def test_tuned_kernels_match_oracle():
     y0 = gemm([x], T=0)[0]
     e0 = rel(to_f64(y0), oracle.phi_k(to_f64(x), 5, *COEF32))
     assert e0 <= 2e-2, f"T=0: {e0:.3e}"
+
+
+RECT = [(256, 128), (128, 512), (64, 1024), (512, 96)]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_rectangular_tiles(dtype):
+    """T_h x T_w tiles (the tile-shape study) against the oracle's rectangular
+    tiling, tile by tile; tall tiles go through the orientation rule."""
+    x = rand((700, 900), dtype, 23)
+    for Th, Tw in RECT:
+        announce(f"gemm rectangular tiles {Th}x{Tw} dtype={dtype} on 700x900")
+        y = hm.ns_gemm([x], T=Th, Tw=Tw, K=5, coeffs=COEF32)[0]
+        torch.cuda.synchronize()
+        R = oracle.ns_tiled_hw(to_f64(x), Th, Tw, 5, *COEF32)
+        Y = to_f64(y)
+        worst = 0.0
+        for r0 in range(0, 700, Th):
+            for c0 in range(0, 900, Tw):
+                sl = np.s_[r0:r0 + Th, c0:c0 + Tw]
+                worst = max(worst, rel(Y[sl], R[sl]))
+        assert worst <= TOL[dtype], f"{Th}x{Tw}: max per-tile error {worst:.3e}"
+
+
+def test_rectangular_square_and_covering_tiles():
+    """Th = Tw reproduces the square call bit for bit; one tile covering the
+    matrix is the full map."""
+    announce("gemm rectangular: square case and a covering tile, bf16")
+    x = rand((300, 500), torch.bfloat16, 29)
+    a = hm.ns_gemm([x], T=128, K=5, coeffs=COEF32)[0]
+    b = hm.ns_gemm([x], T=128, Tw=128, K=5, coeffs=COEF32)[0]
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    y = hm.ns_gemm([x], T=512, Tw=600, K=5, coeffs=COEF32)[0]
+    torch.cuda.synchronize()
+    assert rel(to_f64(y), oracle.phi_k(to_f64(x), 5, *COEF32)) <= 2e-2

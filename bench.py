@@ -215,8 +215,9 @@ def bench_optstep(args, hm, torch, np, dev):
         Ws = [(torch.randn(H, H, device=dev, generator=gen) * 0.02).to(torch.bfloat16) for _ in range(8)]
         Gs = [torch.empty(H, H, dtype=torch.bfloat16, device=dev) for _ in range(8)]
         res = {}
-        variants = [("muon_full_per_layer", 0, False), ("muon_full_batched", 0, True),
-                    ("himuon_T512_per_layer", 512, False), ("himuon_T512_batched", 512, True)]
+        variants = [("muon_full_per_layer", 0, False), ("muon_full_batched", 0, True)]
+        for t in (int(v) for v in args.optstep_T.split(",")):
+            variants += [(f"himuon_T{t}_per_layer", t, False), (f"himuon_T{t}_batched", t, True)]
         if args.variants != "all":
             keep = args.variants.split(",")
             variants = [v for v in variants if v[0] in keep]
@@ -247,7 +248,7 @@ def bench_optstep(args, hm, torch, np, dev):
                     times.append((a, b))
             torch.cuda.synchronize()
             ms = np.array([a.elapsed_time(b) for a, b in times])
-            flops = 8 * (6.0 * H * H * 512 * 5 if T else 6.0 * H ** 3 * 5)
+            flops = 8 * (6.0 * H * H * min(T, H) * 5 if T else 6.0 * H ** 3 * 5)
             res[name] = {"median_ms": round(float(np.median(ms)), 4),
                          "iqr_ms": round(float(np.percentile(ms, 75) - np.percentile(ms, 25)), 4),
                          "ns_tflops": round(flops / (float(np.median(ms)) * 1e-3) / 1e12, 2),
@@ -300,6 +301,8 @@ def main():
     ap.add_argument("--tune", type=int, default=1,
                     help="time the GEMM library's candidates for the GEMM path before the run (1) or not (0)")
     ap.add_argument("--hidden", default="1024,2048,4096", help="H values of --optstep")
+    ap.add_argument("--optstep-T", dest="optstep_T", default="512",
+                    help="--optstep: HiMuon tile sizes to run (comma-separated; the paper's is 512)")
     ap.add_argument("--variants", default="all",
                     help="--optstep variants to run (comma-separated names, or all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,

@@ -189,12 +189,7 @@ int upload_table(const void* data, size_t bytes, void* workspace, hipStream_t st
 
 extern "C" {
 
-size_t himuon_ns_tiled_workspace_size(int64_t n_mats)
-{
-    if (n_mats < 1) return 0;
-    const size_t b = (size_t)n_mats * sizeof(MatDesc);
-    return (b + 255) / 256 * 256;
-}
+size_t himuon_ns_tiled_workspace_size(int64_t n_mats) { return himuon::tiled_workspace(n_mats, false); }
 
 int himuon_plan_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
                        size_t chunk_budget_bytes, int64_t* total_tiles, int64_t* n_chunks,
@@ -219,10 +214,27 @@ int himuon_select_compute(int dtype, int compute, int K, float a, float b, float
     return resolve_compute(dtype, compute, K, a, b, c);
 }
 
-int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
-                    const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a,
-                    float b, float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
-                    size_t chunk_budget_bytes, void* stream)
+}  // extern "C"
+
+namespace himuon {
+
+size_t tiled_workspace(int64_t n_mats, bool step)
+{
+    if (n_mats < 1) return 0;
+    const size_t b = (size_t)n_mats * sizeof(MatDesc);
+    const size_t o = step ? (size_t)n_mats * sizeof(OptDesc) : 0;
+    return (b + 255) / 256 * 256 + (o + 255) / 256 * 256;
+}
+
+bool has_step_kernel(int T, Storage st, Operand op, float c)
+{
+    return (T == 32 || T == 64 || T == 128) && st == Storage::BF16 && op == Operand::F16 && c > 0.f;
+}
+
+int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+              const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
+              float c, int dtype, int compute, void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
+              void* stream, const OptDesc* opt_host, float beta, float decay, float lr, int nesterov)
 {
     // ---- validation: nothing is enqueued unless every check passes
     if (n_mats < 1 || n_mats > INT32_MAX || !in_ptrs || !out_ptrs || !rows || !cols) return HIMUON_ERR_INVALID_ARG;
@@ -242,7 +254,8 @@ int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out
     const himuon::Storage st = dtype == HIMUON_BF16 ? himuon::Storage::BF16 : himuon::Storage::F32;
     const himuon::Operand opnd = (himuon::Operand)op;
     if (!himuon::has_kernel(T, st, opnd)) return HIMUON_ERR_UNSUPPORTED;
-    if (!workspace || workspace_bytes < himuon_ns_tiled_workspace_size(n_mats)) return HIMUON_ERR_WORKSPACE;
+    if (opt_host && !has_step_kernel(T, st, opnd, c)) return HIMUON_ERR_UNSUPPORTED;
+    if (!workspace || workspace_bytes < tiled_workspace(n_mats, opt_host != nullptr)) return HIMUON_ERR_WORKSPACE;
 
     std::vector<int64_t> begin;
     int64_t total = 0, n_chunks = 0;
@@ -267,7 +280,10 @@ int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out
         d.tile_begin = begin[(size_t)m];
         d.tiles_c = (int32_t)ceil_div(cols[m], T);
         d.flags = 0;
-        if ((uintptr_t)d.in % align == 0 && d.ld_in % ld_mult == 0) d.flags |= himuon::MAT_VEC_IN;
+        // (a step's momentum shares the gradient's layout and alignment flag)
+        if ((uintptr_t)d.in % align == 0 && d.ld_in % ld_mult == 0 &&
+            (!opt_host || (uintptr_t)opt_host[m].mom % align == 0))
+            d.flags |= himuon::MAT_VEC_IN;
         if ((uintptr_t)d.out % align == 0 && d.ld_out % ld_mult == 0) d.flags |= himuon::MAT_VEC_OUT;
         if (ceil_div(cols[m], T) > INT32_MAX) return HIMUON_ERR_INVALID_ARG;
     }
@@ -284,10 +300,19 @@ int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out
     }
     if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e);
 
+    const size_t dbytes = ((size_t)n_mats * sizeof(MatDesc) + 255) / 256 * 256;
+    OptDesc* const otab = opt_host ? reinterpret_cast<OptDesc*>(static_cast<uint8_t*>(workspace) + dbytes) : nullptr;
     int status = himuon::upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
+    if (status == HIMUON_OK && opt_host)
+        status = himuon::upload_table(opt_host, (size_t)n_mats * sizeof(OptDesc), otab, hs, dev);
     if (status == HIMUON_OK) {
         himuon::KernelArgs ka;
         ka.descs = static_cast<const MatDesc*>(workspace);
+        ka.odescs = otab;
+        ka.beta = beta;
+        ka.decay = decay;
+        ka.lr = lr;
+        ka.nesterov = nesterov;
         ka.n_mats = (int32_t)n_mats;
         ka.K = K;
         ka.a = a;
@@ -315,6 +340,19 @@ int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out
     }
     if (dev != cur) (void)hipSetDevice(cur);
     return status;
+}
+
+}  // namespace himuon
+
+extern "C" {
+
+int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+                    const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a,
+                    float b, float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
+                    size_t chunk_budget_bytes, void* stream)
+{
+    return himuon::run_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c, dtype, compute,
+                             workspace, workspace_bytes, chunk_budget_bytes, stream, nullptr, 0.f, 1.f, 0.f, 0);
 }
 
 const char* himuon_status_string(int status)

@@ -29,9 +29,27 @@ constexpr int32_t MAT_VEC_OUT = 2;
 enum class Storage : int { F32 = 0, BF16 = 1 };
 enum class Operand : int { F32 = 1, F16 = 2, BF16 = 3 };
 
+// The optimizer step of Alg. 1 fused into the fp16 tile kernels, per
+// matrix: `in` is the gradient G, `out` the weights W (updated in place),
+// `mom` the momentum M (layout of `in`, updated in place), tau the update
+// scale of eq. (scaled_update).
+struct alignas(16) OptDesc {
+    void* mom;
+    float tau;
+    int32_t pad_;
+};
+static_assert(sizeof(OptDesc) == 16, "optimizer descriptor layout");
+
 // Kernel arguments of one chunk launch: tiles [tile_begin, tile_end).
 struct KernelArgs {
     const MatDesc* descs;
+    // non-null: the launch is an optimizer step (OptDesc per matrix). The
+    // tile staging forms M <- beta M + G (stored, rounded to bf16) and the
+    // lookahead G + beta M (nesterov) or M as the tile's input; the
+    // write-back stores W <- decay W - lr tau U.
+    const OptDesc* odescs;
+    float beta, decay, lr;
+    int32_t nesterov;
     int64_t tile_begin;
     int64_t tile_end;
     int32_t n_mats;
@@ -52,6 +70,20 @@ hipError_t launch_ns_tiled(int T, Storage st, Operand op, const KernelArgs& args
 
 // True when a kernel exists for the triple (no HIP call).
 bool has_kernel(int T, Storage st, Operand op);
+
+// True when the optimizer step can run inside the tile kernel for this
+// tile size, storage, operand type and sign of c (no HIP call).
+bool has_step_kernel(int T, Storage st, Operand op, float c);
+
+// The plan, descriptor upload and chunk launches of himuon_ns_tiled; with
+// `opt_host` (one OptDesc per matrix) and the step's scalars, the fused
+// optimizer step (has_step_kernel must hold). Returns a himuon status.
+int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+              const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
+              float c, int dtype, int compute, void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
+              void* stream, const OptDesc* opt_host, float beta, float decay, float lr, int nesterov);
+// Workspace of run_tiled: the MatDesc table, and the OptDesc table for a step.
+size_t tiled_workspace(int64_t n_mats, bool step);
 
 // The fp16-operand kernel family (bf16 storage), T in {32, 64, 128, 256}.
 hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream);

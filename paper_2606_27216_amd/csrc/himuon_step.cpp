@@ -4,16 +4,19 @@
 //       else Phi_{K,T}(Ghat);
 //   W <- (1 - lr lambda) W - lr tau U, tau = c sqrt(max(H, W)) on the full
 //       branch and c sqrt(T) when tiled (Sec. 4.3, eq. scaled_update).
-// Two execution routes, chosen from T:
-//   - T in {32, 64, 128, 256} with a fused tile kernel for the storage and
-//     operand types: an element-wise prologue (momentum and lookahead into a
-//     contiguous buffer), the tiled map in place on that buffer, and an
-//     element-wise epilogue (decay and update); matrices are taken in
-//     consecutive groups whose buffers fit the chunk budget;
+// Three execution routes, chosen from T and the types:
+//   - T in {32, 64, 128}, bf16 storage, fp16 operands, c > 0: the step
+//     inside the fused tile kernel (its staging forms the momentum and the
+//     lookahead, its write-back the weight update), so every matrix is read
+//     and written once;
+//   - other T in {32, 64, 128, 256} with a fused tile kernel for the types:
+//     an element-wise prologue (momentum and lookahead into a contiguous
+//     buffer), the tiled map in place on that buffer, and an element-wise
+//     epilogue (decay and update); matrices are taken in consecutive groups
+//     whose buffers fit the chunk budget;
 //   - otherwise (T = 0, large tiles such as 512): the library-GEMM path with
 //     the momentum fused into its norm and gather kernels and the update into
-//     its scatter kernel, so the matrices are read and written once each
-//     outside the Newton-Schulz iterations.
+//     its scatter kernel.
 #include "himuon_internal.h"
 #include "ns_gemm_path.h"
 #include "optim_kernels.h"
@@ -39,6 +42,15 @@ bool fused_route(int T, int dtype, int compute, int K, float a, float b, float c
     if (op < 0) return false;
     const himuon::Storage st = dtype == HIMUON_BF16 ? himuon::Storage::BF16 : himuon::Storage::F32;
     return himuon::has_kernel(T, st, (himuon::Operand)op);
+}
+
+// The step can run inside the tile kernel (see the file comment).
+bool in_kernel_route(int T, int dtype, int compute, int K, float a, float b, float c)
+{
+    if (!fused_route(T, dtype, compute, K, a, b, c)) return false;
+    const int op = himuon_select_compute(dtype, compute, K, a, b, c);
+    const himuon::Storage st = dtype == HIMUON_BF16 ? himuon::Storage::BF16 : himuon::Storage::F32;
+    return himuon::has_step_kernel(T, st, (himuon::Operand)op, c);
 }
 
 size_t elem_size(int dtype) { return dtype == HIMUON_BF16 ? 2 : 4; }
@@ -89,6 +101,7 @@ size_t himuon_step_workspace_size(int64_t n_mats, const int64_t* rows, const int
     if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return 0;
     for (int64_t l = 0; l < n_mats; ++l)
         if (rows[l] < 1 || cols[l] < 1) return 0;
+    if (in_kernel_route(T, dtype, compute, K, a, b, c)) return himuon::tiled_workspace(n_mats, true);
     if (fused_route(T, dtype, compute, K, a, b, c)) {
         std::vector<int64_t> bounds;
         size_t buf_max = 0;
@@ -139,7 +152,21 @@ int himuon_step(int64_t n_mats, void* const* weights, const void* const* grads, 
                                      stream, &opt);
     }
 
-    // ---- fused-kernel route
+    if (in_kernel_route(T, dtype, compute, K, a, b, c)) {
+        std::vector<himuon::OptDesc> od((size_t)n_mats);
+        std::vector<const void*> in((size_t)n_mats);
+        for (int64_t l = 0; l < n_mats; ++l) {
+            od[(size_t)l].mom = moms[l];
+            od[(size_t)l].tau = tau[(size_t)l];
+            od[(size_t)l].pad_ = 0;
+            in[(size_t)l] = grads[l];
+        }
+        return himuon::run_tiled(n_mats, in.data(), weights, rows, cols, ld, ld, T, K, a, b, c, dtype, compute,
+                                 workspace, workspace_bytes, chunk_budget_bytes, stream, od.data(), opt.beta,
+                                 opt.decay, opt.lr, opt.nesterov);
+    }
+
+    // ---- fused-kernel route with element-wise prologue and epilogue
     std::vector<int64_t> bounds;
     size_t buf_max = 0;
     int st = plan_step_groups(n_mats, rows, cols, dtype, chunk_budget_bytes, &bounds, &buf_max);

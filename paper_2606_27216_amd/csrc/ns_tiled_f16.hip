@@ -154,7 +154,11 @@ template <int T, int RB> struct F16Shape {
 // shortcut are compile-time, so no branch of the K loop is if-converted).
 // RB: 32-row blocks owned by one wave; a tile is spread over NB / RB waves.
 // Every operand read from LDS feeds RB MFMAs.
-template <int T, int RB, int CMODE>
+// OPT: the optimizer step of Alg. 1 rides on the tile I/O (KernelArgs):
+// the staging turns the loaded G and M into the stored new M and the
+// lookahead, and the write-back turns U into the decayed, tau-scaled update
+// of the loaded W. Without OPT the kernel is the map alone.
+template <int T, int RB, int CMODE, bool OPT>
 __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>::kMinWavesPerEU)) ns_tiled_f16_kernel(const KernelArgs args)
 {
     constexpr Storage ST = Storage::BF16;
@@ -163,7 +167,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     constexpr int WT = NB / RB;     // waves per tile
     static_assert(NB % RB == 0 && WT >= 1 && WT <= 4, "tile split");
     constexpr int TPW = F16Shape<T, RB>::TPW;  // tiles per workgroup
-    constexpr bool EARLY = F16Shape<T, RB>::kEarlyPrefetch;
+    constexpr bool EARLY = F16Shape<T, RB>::kEarlyPrefetch && !OPT;  // (a step holds G and M: no room)
     constexpr int S = 2;
     constexpr int MAT = NB * NB * S * 64;  // 16-byte slots of H
     constexpr bool SHARED = WT > 1;
@@ -236,6 +240,8 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         int64_t rows, cols, ld_in, ld_out;
         int64_t row0, col0;
         bool vin, vout;
+        void* mom;  // OPT: the momentum buffer (layout of `in`) and tau
+        float tau;
     };
     int mhint = 0;
     auto locate = [&](int64_t local, TileLoc& L) {
@@ -255,6 +261,15 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         const bool full = L.row0 + T <= L.rows && L.col0 + T <= L.cols;
         L.vin = full && (D.flags & MAT_VEC_IN);
         L.vout = full && (D.flags & MAT_VEC_OUT);
+        if constexpr (OPT) {
+            typedef __attribute__((address_space(4))) const OptDesc ConstOpt;
+            const ConstOpt& O = ((const ConstOpt*)(uintptr_t)args.odescs)[mhint];
+            L.mom = O.mom;
+            L.tau = O.tau;
+        } else {
+            L.mom = nullptr;
+            L.tau = 0.f;
+        }
     };
     // HBM traffic in whole row segments: a lane moves 16 bytes (8 bf16), a
     // row takes LPR lanes and one wave instruction RPI rows. The wave's own
@@ -265,28 +280,35 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     constexpr int NI = 32 * RB / RPI;
     const int io_row = lane / LPR, io_cc = lane % LPR;  // row within an instruction, 16-byte chunk
     u32x4 raw[NI];
-    auto issue_loads = [&](const TileLoc& L) {
+    u32x4 rawm[OPT ? NI : 1];  // OPT: the momentum rows of the tile
+    // the wave's rows of the tile in `base` (leading dimension ld), zero
+    // outside the matrix
+    auto load_rows = [&](const TileLoc& L, const void* base, int64_t ld, bool vec, u32x4 (&dst)[NI]) {
         const int64_t gr0 = L.row0 + 32 * p0 + io_row;
         const int64_t gc = L.col0 + 8 * io_cc;
-        if (L.vin) {  // whole tile inside, 16-byte aligned: straight vector loads
-            const gbl_u32x4* src = (const gbl_u32x4*)(static_cast<const uint16_t*>(L.in) + gr0 * L.ld_in + gc);
-            const int64_t step = (int64_t)RPI * L.ld_in / 8;  // u32x4 per RPI rows
+        if (vec) {  // whole tile inside, 16-byte aligned: straight vector loads
+            const gbl_u32x4* src = (const gbl_u32x4*)(static_cast<const uint16_t*>(base) + gr0 * ld + gc);
+            const int64_t step = (int64_t)RPI * ld / 8;  // u32x4 per RPI rows
 #pragma unroll
-            for (int i = 0; i < NI; ++i) raw[i] = src[i * step];
+            for (int i = 0; i < NI; ++i) dst[i] = src[i * step];
         } else {
 #pragma unroll
             for (int i = 0; i < NI; ++i) {
                 const int64_t gr = gr0 + RPI * i;
-                const uint16_t* ptr = static_cast<const uint16_t*>(L.in) + gr * L.ld_in + gc;
+                const uint16_t* ptr = static_cast<const uint16_t*>(base) + gr * ld + gc;
                 uint32_t h[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
                 if (gr < L.rows) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
                         if (gc + e < L.cols) h[e] = ptr[e];
                 }
-                raw[i] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+                dst[i] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
             }
         }
+    };
+    auto issue_loads = [&](const TileLoc& L) {
+        load_rows(L, L.in, L.ld_in, L.vin, raw);
+        if constexpr (OPT) load_rows(L, L.mom, L.ld_in, L.vin, rawm);
     };
     // byte offset of the 16-byte chunk io_cc of tile row `row` in the row-major
     // copy: its two 8-byte halves sit in one aligned 16-byte pair, swapped
@@ -314,26 +336,68 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     };
 
     // Whole row segments of the own rows to HBM (16-byte chunks read back from
-    // the row-major copy into `outv`).
-    auto store_rows = [&](const TileLoc& L, const u32x4 (&outv)[NI]) {
+    // the row-major copy into `outv`), inside the matrix only.
+    auto put_rows = [&](const TileLoc& L, void* base, int64_t ld, bool vec, const u32x4 (&v)[NI]) {
         const int64_t gr0 = L.row0 + 32 * p0 + io_row;
         const int64_t gc = L.col0 + 8 * io_cc;
-        if (L.vout) {
-            gbl_u32x4* dst = (gbl_u32x4*)(static_cast<uint16_t*>(L.out) + gr0 * L.ld_out + gc);
-            const int64_t step = (int64_t)RPI * L.ld_out / 8;
+        if (vec) {
+            gbl_u32x4* dst = (gbl_u32x4*)(static_cast<uint16_t*>(base) + gr0 * ld + gc);
+            const int64_t step = (int64_t)RPI * ld / 8;
 #pragma unroll
-            for (int i = 0; i < NI; ++i) dst[i * step] = outv[i];
+            for (int i = 0; i < NI; ++i) dst[i * step] = v[i];
         } else {
 #pragma unroll
             for (int i = 0; i < NI; ++i) {
                 const int64_t gr = gr0 + RPI * i;
-                uint16_t* ptr = static_cast<uint16_t*>(L.out) + gr * L.ld_out + gc;
+                uint16_t* ptr = static_cast<uint16_t*>(base) + gr * ld + gc;
                 if (gr < L.rows) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
-                        if (gc + e < L.cols) ptr[e] = (uint16_t)(outv[i][e >> 1] >> (16 * (e & 1)));
+                        if (gc + e < L.cols) ptr[e] = (uint16_t)(v[i][e >> 1] >> (16 * (e & 1)));
                 }
             }
+        }
+    };
+    // two bf16 of a packed word as fp32, and back (round to nearest even)
+    auto bf_lo = [](uint32_t w) { return __uint_as_float(w << 16); };
+    auto bf_hi = [](uint32_t w) { return __uint_as_float(w & 0xffff0000u); };
+    auto bf_pack = [](float lo, float hi) {
+        const f32x2 v = {lo, hi};
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+    };
+    auto store_rows = [&](const TileLoc& L, const u32x4 (&outv)[NI]) {
+        if constexpr (OPT) {
+            // W <- (1 - lr lambda) W - lr tau U, U the tile's bf16 result
+            u32x4 wv[NI];
+            load_rows(L, L.out, L.ld_out, L.vout, wv);
+            const float step = args.lr * L.tau;
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+#pragma unroll
+                for (int x = 0; x < 4; ++x)
+                    wv[i][x] = bf_pack(args.decay * bf_lo(wv[i][x]) - step * bf_lo(outv[i][x]),
+                                       args.decay * bf_hi(wv[i][x]) - step * bf_hi(outv[i][x]));
+            put_rows(L, L.out, L.ld_out, L.vout, wv);
+        } else {
+            put_rows(L, L.out, L.ld_out, L.vout, outv);
+        }
+    };
+    // OPT, on the staged rows of the current tile: M <- beta M + G, stored
+    // (bf16), and the lookahead from the stored M replaces G in `raw`
+    auto step_prologue = [&](const TileLoc& L) {
+        if constexpr (OPT) {
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    const uint32_t g = raw[i][x];
+                    const uint32_t m = bf_pack(args.beta * bf_lo(rawm[i][x]) + bf_lo(g),
+                                               args.beta * bf_hi(rawm[i][x]) + bf_hi(g));
+                    rawm[i][x] = m;
+                    raw[i][x] = args.nesterov ? bf_pack(bf_lo(g) + args.beta * bf_lo(m), bf_hi(g) + args.beta * bf_hi(m))
+                                              : m;
+                }
+            put_rows(L, L.mom, L.ld_in, L.vin, rawm);
         }
     };
 
@@ -379,6 +443,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         const bool has_next = nlocal < n_tiles;
         TileLoc nxt = cur;
         if (has_next) locate(nlocal, nxt);
+        step_prologue(cur);
 
         // own rows into the row-major copy, then back as row pieces of packed
         // bf16 words; only this wave touches these rows until its first
@@ -1311,7 +1376,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 
 constexpr int kMaxDevices = 64;
 
-template <int T, int RB, int CMODE>
+template <int T, int RB, int CMODE, bool OPT = false>
 hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
 {
     constexpr int TPW = F16Shape<T, RB>::TPW;
@@ -1324,7 +1389,7 @@ hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
     int cap = resident[dev].load(std::memory_order_relaxed);
     if (cap == 0) {
         int per_cu = 0, cus = 0;
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ns_tiled_f16_kernel<T, RB, CMODE>, NT, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ns_tiled_f16_kernel<T, RB, CMODE, OPT>, NT, 0);
         if (e != hipSuccess) return e;
         e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
@@ -1335,7 +1400,7 @@ hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
     if (n <= 0) return hipSuccess;
     const int64_t groups = (n + TPW - 1) / TPW;
     const int grid = (int)(groups < cap ? groups : cap);
-    hipLaunchKernelGGL((ns_tiled_f16_kernel<T, RB, CMODE>), dim3(grid), dim3(NT), 0, stream, args);
+    hipLaunchKernelGGL((ns_tiled_f16_kernel<T, RB, CMODE, OPT>), dim3(grid), dim3(NT), 0, stream, args);
     return hipGetLastError();
 }
 
@@ -1343,6 +1408,15 @@ hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
 
 hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream)
 {
+    if (args.odescs) {  // the optimizer step (c > 0, T <= 128; has_step_kernel)
+        if (!(args.c > 0.f)) return hipErrorInvalidValue;
+        switch (T) {
+        case 32: return launch_f16<32, 1, 0, true>(args, stream);
+        case 64: return launch_f16<64, 2, 0, true>(args, stream);
+        case 128: return launch_f16<128, 2, 0, true>(args, stream);
+        default: return hipErrorInvalidValue;
+        }
+    }
     const int cm = args.c > 0.f ? 0 : (args.c < 0.f ? 1 : 2);
     switch (T * 4 + cm) {
     case 32 * 4 + 0: return launch_f16<32, 1, 0>(args, stream);

@@ -420,6 +420,7 @@ bool has_kernel(int T, Storage st, Operand op)
 hipError_t launch_ns_tiled(int T, Storage st, Operand op, const KernelArgs& args, hipStream_t stream)
 {
     if (!has_kernel(T, st, op)) return hipErrorInvalidValue;
+    if (args.odescs && op != Operand::F16) return hipErrorInvalidValue;  // the step rides on the fp16 kernels only
     if (st == Storage::F32) return launch_T<Storage::F32, Operand::F32>(T, args, stream);
     if (op == Operand::F16) return launch_ns_tiled_f16(T, args, stream);
     return launch_T<Storage::BF16, Operand::BF16>(T, args, stream);

@@ -213,12 +213,18 @@ def test_step_workspace_size():
     # T = 512 and T = 0 run the library-GEMM path: the same plan as himuon_ns_gemm
     assert ws([1024] * 8, [1024] * 8, 512) == gemm([1024] * 8, [1024] * 8, 512)
     assert ws([300], [500], 0, hm.F32) == gemm([300], [500], 0, hm.F32)
-    # fused tile sizes: the lookahead buffers of all matrices plus two descriptor tables
-    need = ws([1024] * 8, [1024] * 8, 128)
+    # T <= 128, bf16, fp16 operands, c > 0: the step runs inside the tile kernel; the workspace is
+    # the two descriptor tables (64 + 16 bytes per matrix, each rounded up to 256)
+    assert ws([1024] * 8, [1024] * 8, 128) == 512 + 256
+    assert ws([1024] * 300, [1024] * 300, 64) == 19200 + 4864
+    # other fused tile sizes (T = 256; fp32 storage): the lookahead buffers of all matrices
+    # plus two descriptor tables
+    need = ws([1024] * 8, [1024] * 8, 256)
     assert need >= 8 * 1024 * 1024 * 2 and need < 8 * 1024 * 1024 * 2 + 4096
+    assert ws([1024] * 8, [1024] * 8, 128, dtype=hm.F32) >= 8 * 1024 * 1024 * 4
     # a budget groups matrices; one matrix above it has no plan
-    assert ws([1024] * 8, [1024] * 8, 128, budget=2 * 1024 * 1024 * 2) < need
-    assert ws([1024] * 8, [1024] * 8, 128, budget=1024 * 1024 * 2 - 1) == 0
+    assert ws([1024] * 8, [1024] * 8, 256, budget=2 * 1024 * 1024 * 2) < need
+    assert ws([1024] * 8, [1024] * 8, 256, budget=1024 * 1024 * 2 - 1) == 0
     assert ws([0], [64], 128) == 0
     assert ws([64], [64], -1) == 0
 
@@ -247,7 +253,8 @@ def _scall(**kw):
     (dict(dtype=7), hm.ERR_INVALID_ARG),
     (dict(T=0, dtype=hm.F32, compute=hm.COMPUTE_BF16), hm.ERR_UNSUPPORTED),
     (dict(T=0, compute=hm.COMPUTE_F16, a=50.0, b=0.0, c=0.0), hm.ERR_RANGE),
-    (dict(workspace=0), hm.ERR_WORKSPACE),              # fused route: buffers do not fit
+    (dict(workspace=0), hm.ERR_WORKSPACE),              # in-kernel route: no descriptor tables
+    (dict(T=256, workspace_bytes=1024), hm.ERR_WORKSPACE),  # prologue/epilogue route: buffers do not fit
     (dict(T=512, workspace_bytes=1 << 20), hm.ERR_WORKSPACE),  # GEMM route
     (dict(chunk_budget_bytes=100), hm.ERR_WORKSPACE),
 ])

@@ -1,9 +1,10 @@
 """The optimizer step (himuon_step, Alg. 1) against the fp64 oracle's step.
 
-Both routes are covered: the library-GEMM path (T = 0, the full-matrix
-branch, and T = 512) with the momentum fused into its gather and the update
-into its scatter, and the fused tile kernels (T = 128, 32) with element-wise
-prologue and epilogue. Bars:
+All three routes are covered: the library-GEMM path (T = 0, the
+full-matrix branch, and T = 512) with the momentum fused into its gather and
+the update into its scatter; the step inside the fused tile kernels (bf16,
+T = 128, 64, 32); and the fused tile kernels with element-wise prologue and
+epilogue (T = 256; fp32 storage). Bars:
   - momentum M: each element within one unit in the last place of the
     storage type of the oracle's value (the GPU rounds beta M + G once to
     storage; the oracle keeps fp64);
@@ -93,7 +94,7 @@ def test_gemm_route(T, dtype):
         check_step(W0[i], G[i], M0[i], W1[i], M1[i], T, dtype, 0.02, 0.95, 0.1, True, 0.2)
 
 
-@pytest.mark.parametrize("T", [128, 32])
+@pytest.mark.parametrize("T", [128, 64, 32, 256])
 @pytest.mark.parametrize("nesterov", [True, False])
 def test_fused_route_bf16(T, nesterov):
     shapes = [(384, 520), (100, 60), (257, 131)]
@@ -204,3 +205,18 @@ def test_zero_gradient_and_momentum():
         assert not torch.any(M)
         d = np.float32(1.0) - np.float32(0.1) * np.float32(0.5)
         assert np.allclose(to_f64(W), d * to_f64(W0), rtol=2 ** -23, atol=0)
+
+
+def test_fused_route_fp32_prologue_epilogue():
+    """fp32 storage at T = 128: the generic tile kernel between the element-wise
+    prologue and epilogue."""
+    shapes = [(384, 520), (100, 60)]
+    announce(f"step fp32 T=128 shapes={shapes}")
+    W0 = [rand(s, torch.float32, 150 + i) for i, s in enumerate(shapes)]
+    G = [rand(s, torch.float32, 160 + i, 1e-2) for i, s in enumerate(shapes)]
+    M0 = [rand(s, torch.float32, 170 + i, 1e-2) for i, s in enumerate(shapes)]
+    W1 = [w.clone() for w in W0]
+    M1 = [m.clone() for m in M0]
+    run_step(W1, G, M1, 128, torch.float32)
+    for i in range(len(shapes)):
+        check_step(W0[i], G[i], M0[i], W1[i], M1[i], 128, torch.float32, 0.02, 0.95, 0.1, True, 0.2)

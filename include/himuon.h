@@ -236,18 +236,23 @@ int himuon_gemm_tune_hw(int64_t n_mats, const int64_t* rows, const int64_t* cols
  *                          rounded to `dtype`, and the lookahead is formed from
  *                          the stored value.
  * T, K, a, b, c            as himuon_ns_gemm: T = 0 or any positive tile size.
- *                          T in {32, 64, 128, 256} runs the fused tile kernels
- *                          (an element-wise prologue and epilogue around the
- *                          tiled map, with the lookahead held in `dtype` in the
- *                          workspace); any other T runs the library-GEMM path
- *                          with the momentum fused into its gather and the
- *                          update into its scatter.
+ *                          Routes: T in {32, 64, 128} with bf16 storage, fp16
+ *                          operands and c > 0 runs the step inside the fused
+ *                          tile kernel (the lookahead is rounded to bf16 as
+ *                          the tile is staged, U as it is written back); other
+ *                          T in {32, 64, 128, 256} with a fused kernel runs an
+ *                          element-wise prologue and epilogue around it, with
+ *                          the lookahead held in `dtype` in the workspace; any
+ *                          other T runs the library-GEMM path with the
+ *                          momentum fused into its gather and the update into
+ *                          its scatter.
  * lr, momentum, weight_decay, nesterov, scale_c   the step's scalars (finite).
  * workspace                device memory of at least himuon_step_workspace_size
  *                          (same arguments) bytes, owned by the caller.
- * chunk_budget_bytes       fused tile sizes: bound on the lookahead buffers of
+ * chunk_budget_bytes       in-kernel route: as himuon_ns_tiled; prologue and
+ *                          epilogue route: bound on the lookahead buffers of
  *                          one group of consecutive matrices (0: one group);
- *                          other T: as himuon_ns_gemm.
+ *                          GEMM route: as himuon_ns_gemm.
  *
  * Errors as himuon_ns_gemm; nothing is enqueued when one is returned.
  * Matrices with non-finite gradients or momenta give non-finite weights

@@ -111,7 +111,33 @@ int set_hip_error(hipError_t e)
 // each singular value of the normalised tile starts in [0, 1] and follows p
 // exactly, so this bounds every entry of the operand X at every step. The
 // interval is sampled densely; a factor of 4 covers what falls between points.
+double iterate_bound_uncached(int K, double a, double b, double c);
+
+// (8193 samples times K: tens of microseconds, so the last few results are
+// kept; a call with the same K and coefficients reuses them.)
 double iterate_bound(int K, double a, double b, double c)
+{
+    struct Entry {
+        int K;
+        double a, b, c, bound;
+    };
+    static std::mutex mu;
+    static Entry cache[8];
+    static int n_cached = 0, next_slot = 0;
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        for (int i = 0; i < n_cached; ++i)
+            if (cache[i].K == K && cache[i].a == a && cache[i].b == b && cache[i].c == c) return cache[i].bound;
+    }
+    const double bound = iterate_bound_uncached(K, a, b, c);
+    std::lock_guard<std::mutex> lock(mu);
+    cache[next_slot] = Entry{K, a, b, c, bound};
+    next_slot = (next_slot + 1) % 8;
+    if (n_cached < 8) ++n_cached;
+    return bound;
+}
+
+double iterate_bound_uncached(int K, double a, double b, double c)
 {
     constexpr int kPts = 8193;
     double m = 1.0;

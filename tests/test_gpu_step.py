@@ -220,3 +220,38 @@ def test_fused_route_fp32_prologue_epilogue():
     run_step(W1, G, M1, 128, torch.float32)
     for i in range(len(shapes)):
         check_step(W0[i], G[i], M0[i], W1[i], M1[i], 128, torch.float32, 0.02, 0.95, 0.1, True, 0.2)
+
+
+def _p_iter(K, s=1.0):
+    a, b, c = COEF32
+    for _ in range(K):
+        s = a * s + b * s ** 3 + c * s ** 5
+    return s
+
+
+@pytest.mark.parametrize("T,dtype", [(128, torch.float32), (0, torch.float32), (128, torch.bfloat16)])
+def test_more_matrices_than_one_grid_row(T, dtype):
+    """70,000 matrices of 1 x 8 in one call: more than the 65,535 a launch
+    covers per grid row (the element-wise kernels and the GEMM path split
+    them). Each is rank one, so Phi_K(G) = p^K(1) G / ||G|| with one tau =
+    c sqrt(8) (T >= max(H, W): the full branch); the oracle checks a sample."""
+    n = 70000
+    announce(f"step with {n} matrices of 1x8, T={T}, {dtype}")
+    W = rand((n, 8), dtype, 180)
+    G = rand((n, 8), dtype, 181, 1e-2)
+    M = torch.zeros_like(W)
+    W0 = W.clone()
+    Ws, Gs, Ms = [W[i:i + 1] for i in range(n)], [G[i:i + 1] for i in range(n)], [M[i:i + 1] for i in range(n)]
+    run_step(Ws, Gs, Ms, T, dtype, lr=0.05, beta=0.9, wd=0.0)
+    g = to_f64(G)
+    mm = f32(0.9) * 0 + g                       # M = 0 + G
+    gh = g + f32(0.9) * to_f64(M)               # Nesterov lookahead from the stored M
+    assert np.allclose(to_f64(M), mm, rtol=ULP[dtype], atol=0)
+    U = _p_iter(5) * gh / np.linalg.norm(gh, axis=1, keepdims=True)
+    ref = to_f64(W0) - f32(0.05) * f32(0.2) * np.sqrt(8.0) * U
+    err = np.abs(to_f64(W) - ref).max(axis=1)
+    bound = TOL[dtype] * f32(0.05) * f32(0.2) * np.sqrt(8.0) * np.abs(U).max(axis=1) + 2 * UNIT[dtype] * np.abs(ref).max(axis=1)
+    assert np.all(err <= bound), f"worst row {int(np.argmax(err / bound))}: {np.max(err / bound):.3f} of the bar"
+    for i in (0, 1, 65534, 65535, 65536, n - 1):
+        check_step(W0[i:i + 1], G[i:i + 1], torch.zeros_like(W0[i:i + 1]), W[i:i + 1], M[i:i + 1], T, dtype, 0.05, 0.9,
+                   0.0, True, 0.2)

@@ -310,8 +310,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: the tiled map needs no communication, and this build measures "
-              "one GPU's share (use --gpus 1).", file=sys.stderr)
+        print("bench.py runs on one GPU only: the tiled map needs no communication between GPUs, and the "
+              "figure is one GPU's share of the work (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

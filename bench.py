@@ -279,6 +279,57 @@ def bench_optstep(args, hm, torch, np, dev):
     print(json.dumps(rec), flush=True)
 
 
+def bench_layershapes(args, hm, torch, np, dev):
+    """Per-layer speedup of the tiled map over the full-matrix map on the
+    Qwen3 Block-0 shapes (Sec. 6.2): one random bf16 Gaussian matrix per
+    shape, Phi_K (T = 0) and Phi_{K,512} through the library-GEMM path, K = 5,
+    one call per matrix; the paired ratio t_full / t_tile is the median over
+    `--steps` timed calls after `--warmup` (the paper: 30 after 3). The fused
+    T = 128 kernel is timed beside them."""
+    import workloads
+    coeffs = tuple(float(np.float32(v)) for v in hm.QUINTIC)
+    stream = torch.cuda.current_stream(dev)
+    out = {}
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for a, b in ev:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in ev])
+
+    for model, shapes in workloads.QWEN3_BLOCK0.items():
+        res = {}
+        for j, (name, H, W) in enumerate(shapes):
+            x = workloads.gaussian(H, W, 7000 + j, "bf16", dev)
+            y = torch.empty_like(x)
+            for T in (0, 512):
+                hm.gemm_tune([(H, W)], T, hm.BF16, K=5, coeffs=coeffs)
+            t_full = timed(lambda: hm.ns_gemm([x], outputs=[y], T=0, K=5, coeffs=coeffs, stream=stream))
+            t_tile = timed(lambda: hm.ns_gemm([x], outputs=[y], T=512, K=5, coeffs=coeffs, stream=stream))
+            t_128 = timed(lambda: hm.ns_tiled([x], outputs=[y], T=128, K=5, coeffs=coeffs, stream=stream))
+            res[name] = {"shape": [H, W], "full_ms": round(float(np.median(t_full)), 4),
+                         "tiled512_ms": round(float(np.median(t_tile)), 4),
+                         "speedup_512": round(float(np.median(t_full / t_tile)), 3),
+                         "fused128_ms": round(float(np.median(t_128)), 4),
+                         "speedup_128": round(float(np.median(t_full / t_128)), 3)}
+            log(f"{model} {name} {H}x{W}: {res[name]}")
+        out[model] = res
+    sp = [r["speedup_512"] for m in out.values() for r in m.values()]
+    rec = {
+        "metric": "per-layer tiled/full NS speedup t_full/t_tile, Qwen3 Block-0 shapes, T=512 K=5 (median of paired ratios)",
+        "value": round(float(np.median(sp)), 3), "unit": "x", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "Qwen3 0.6B/1.7B/4B Block-0 shapes, one N(0,1) bf16 matrix each", "T": 512, "K": 5},
+        "results": out,
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -296,6 +347,8 @@ def main():
     ap.add_argument("--path", default="tiled", choices=["tiled", "gemm"],
                     help="tiled: the fused per-tile kernels (T <= 256); gemm: himuon_ns_gemm, whole matrices "
                          "(--T 0) or large tiles (e.g. --T 512) through batched library GEMMs")
+    ap.add_argument("--layershapes", action="store_true",
+                    help="run the per-layer tiled (T=512) vs full-matrix comparison on Qwen3 Block-0 shapes instead")
     ap.add_argument("--optstep", action="store_true",
                     help="run the optimizer-step benchmark (8 x Linear(H,H), HiMuon T=512 vs full Muon) instead")
     ap.add_argument("--tune", type=int, default=1,
@@ -333,6 +386,8 @@ def main():
 
     if args.optstep:
         return bench_optstep(args, hm, torch, np, dev)
+    if args.layershapes:
+        return bench_layershapes(args, hm, torch, np, dev)
 
     coeffs = tuple(float(np.float32(v)) for v in hm.QUINTIC)
     compute = {"default": hm.COMPUTE_DEFAULT, "f16": hm.COMPUTE_F16, "bf16": hm.COMPUTE_BF16,

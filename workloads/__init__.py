@@ -42,6 +42,18 @@ LAYER_7B = (
 
 HETERO_SHAPES = tuple([(1024, 4096)] * 8 + [(4096, 1024)] * 8 + [(2048, 2048)] * 8)
 
+# The seven Muon-eligible matrices of one transformer block of each Qwen3
+# model, output x input (Sec. 6.2, Tab. qwen3_shapes), for the per-layer
+# tiled/full comparison; the inputs themselves are random Gaussian.
+QWEN3_BLOCK0 = {
+    "0.6B": (("q_proj", 2048, 1024), ("k_proj", 1024, 1024), ("v_proj", 1024, 1024), ("o_proj", 1024, 2048),
+             ("gate_proj", 3072, 1024), ("up_proj", 3072, 1024), ("down_proj", 1024, 3072)),
+    "1.7B": (("q_proj", 2048, 2048), ("k_proj", 1024, 2048), ("v_proj", 1024, 2048), ("o_proj", 2048, 2048),
+             ("gate_proj", 6144, 2048), ("up_proj", 6144, 2048), ("down_proj", 2048, 6144)),
+    "4B": (("q_proj", 4096, 2560), ("k_proj", 1024, 2560), ("v_proj", 1024, 2560), ("o_proj", 2560, 4096),
+           ("gate_proj", 9728, 2560), ("up_proj", 9728, 2560), ("down_proj", 2560, 9728)),
+}
+
 _TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16, "f64": torch.float64}
 
 

@@ -20,6 +20,10 @@
  * arrays, device pointers for matrix data and workspace, and a HIP stream
  * passed as void* (a hipStream_t; NULL is the null stream). No entry point
  * allocates device memory or synchronises the device on the compute path.
+ * Each call copies its descriptor table to the workspace from a ring of
+ * pinned host slots (allocated on first use, reused once the copy that last
+ * used a slot has completed), so calls are not meant for stream capture into
+ * a HIP graph: a captured copy would read whatever a slot holds at replay.
  *
  * Matrices are row-major: element (i, j) of matrix l sits at
  * ptr_l + i*ld_l + j (in elements). One call uses one storage dtype for all

@@ -160,3 +160,17 @@ def test_rectangular_square_and_covering_tiles():
     y = hm.ns_gemm([x], T=512, Tw=600, K=5, coeffs=COEF32)[0]
     torch.cuda.synchronize()
     assert rel(to_f64(y), oracle.phi_k(to_f64(x), 5, *COEF32)) <= 2e-2
+
+
+@pytest.mark.parametrize("dtype,compute", [(torch.float32, hm.COMPUTE_DEFAULT), (torch.bfloat16, hm.COMPUTE_BF16)])
+def test_tiles_256_where_no_fused_kernel_exists(dtype, compute):
+    """T = 256 with fp32 storage, or with bf16 operands, has no fused kernel
+    (the tile does not fit one CU's LDS in those forms); the GEMM path serves it."""
+    announce(f"gemm T=256 dtype={dtype} compute={compute}")
+    x = rand((600, 700), dtype, 31)
+    code = hm.F32 if dtype == torch.float32 else hm.BF16
+    assert hm.himuon_ns_tiled(1, [x.data_ptr()], [x.data_ptr()], [600], [700], None, None, 256, 5, *COEF32, code,
+                              compute, 1, 256, 0, None) == hm.ERR_UNSUPPORTED
+    y = gemm([x], T=256, compute=compute)[0]
+    e = tile_errors(to_f64(y), oracle.ns_tiled(to_f64(x), 256, 5, *COEF32), 256)
+    assert e.max() <= TOL[dtype], f"max per-tile error {e.max():.3e}"

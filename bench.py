@@ -94,9 +94,12 @@ def issued_fraction(T, op_name, c):
     """MFMA work a launch issues, as a fraction of the 6T^3 per tile-step the
     metric counts. The fp16 128-tile kernel evaluates only the ten upper
     32x32 blocks of the symmetric H and aI + P (of 16 each) plus the full PZ
-    product; with c = 0 there is no P product (aI + P = aI + bH)."""
+    product, the fp16 64-tile kernel the three upper blocks (of 4) of each
+    when c != 0; with c = 0 there is no P product (aI + P = aI + bH)."""
     if op_name == "f16" and T == 128:
         return (10 + (10 if c != 0 else 0) + 16) / 48.0
+    if op_name == "f16" and T == 64 and c != 0:
+        return (3 + 3 + 4) / 12.0
     return 1.0 if c != 0 else 2.0 / 3.0
 
 

@@ -179,7 +179,13 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     constexpr int IT = NB * S;      // k iterations of one product
 
     // H slots; for the symmetric 128-tile step, 18 blocks of 32x32 fp16 (12 of H, 6 of aI + P)
-    constexpr int NSLOT = F16Shape<T, RB>::kSym ? 18 * 2048 / 16 : ((SHARED && !F16Shape<T, RB>::kChain) ? TPW * MAT : 1);
+    // A 64-tile (one wave) evaluates only the upper blocks of H and aI + P
+    // too; its lower off-diagonal blocks come back through two 32x32 fp16
+    // blocks of LDS per tile (c != 0 only).
+    constexpr bool SYM64 = T == 64 && RB == 2 && WT == 1 && CMODE != 2;
+    constexpr int NSLOT = F16Shape<T, RB>::kSym ? 18 * 2048 / 16
+                          : SYM64 ? TPW * 2 * 2048 / 16
+                          : ((SHARED && !F16Shape<T, RB>::kChain) ? TPW * MAT : 1);
     __shared__ u32x4 s_slots[NSLOT];
     __shared__ __attribute__((aligned(16))) uint8_t s_rm[TPW * RM];
     __shared__ float s_red[6][SHARED ? WT : 1];  // 2 tile parities x 3 reductions
@@ -1133,6 +1139,26 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 
         // One Newton-Schulz step.
         auto ns_step = [&]() {
+            // SYM64: 32x32 fp16 blocks in LDS in the pair layout of the
+            // symmetric 128-tile step (64-byte rows); a block stored from its
+            // row pieces is read back transposed with ds_read_b64_tr_b16
+            uint8_t* const sblk = reinterpret_cast<uint8_t*>(s_slots) + (SYM64 ? tslot * 4096 : 0);
+            auto sym_put = [&](uint8_t* b, const u32x4 (&v)[S]) {
+#pragma unroll
+                for (int x = 0; x < S; ++x)
+                    *reinterpret_cast<u32x4*>(b + li * 64 + 16 * ((2 * x + lh) ^ tsw(li))) = v[x];
+            };
+            auto sym_tr = [&](const uint8_t* b, int x) -> u32x4 {
+                auto phys = [&](int c, int r) { return 2 * ((((c >> 2) << 1) | (c & 1)) ^ tsw(r)) + ((c >> 1) & 1); };
+                u32x2 h[2];
+#pragma unroll
+                for (int y = 0; y < 2; ++y) {
+                    const int row = 16 * x + 8 * y + 4 * (grp16 >> 1) + ((lane & 15) >> 2);
+                    const int chunk = 4 * (grp16 & 1) + (lane & 3);
+                    h[y] = tr_read(b + row * 64 + 8 * phys(chunk, row));
+                }
+                return u32x4{h[0][0], h[0][1], h[1][0], h[1][1]};
+            };
             u32x4 Zop[RB][NB][S];
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
@@ -1182,7 +1208,10 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     for (int j = 0; j < NB; ++j) {
                         const u32x4 opa = j < RB ? Zop[j < RB ? j : 0][q][s] : cur_op[j < RB ? 0 : j - RB];
 #pragma unroll
-                        for (int rb = 0; rb < RB; ++rb) G[rb][j] = mma1<OP>(opa, Zop[rb][q][s], G[rb][j]);
+                        for (int rb = 0; rb < RB; ++rb) {
+                            if (SYM64 && rb == 1 && j == 0) continue;  // the transpose of block (0, 1)
+                            G[rb][j] = mma1<OP>(opa, Zop[rb][q][s], G[rb][j]);
+                        }
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
@@ -1196,12 +1225,19 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
                     for (int j = 0; j < NB; ++j)
 #pragma unroll
-                        for (int s = 0; s < S; ++s) Hop[rb][j][s] = make_slot<OP>(G[rb][j], s);
+                        for (int s = 0; s < S; ++s)
+                            if (!(SYM64 && rb == 1 && j == 0)) Hop[rb][j][s] = make_slot<OP>(G[rb][j], s);
                     f32x16 gd = G[rb][rb];  // H + sigma b' I on the diagonal block (p0 + rb, p0 + rb)
 #pragma unroll
                     for (int v = 0; v < 16; ++v) gd[v] += v == vdiag ? args.bq : 0.f;
 #pragma unroll
                     for (int s = 0; s < S; ++s) Q0[rb][s] = make_slot<OP>(gd, s);
+                }
+                if constexpr (SYM64) {
+                    // H(1, 0) = H(0, 1)^T
+                    sym_put(sblk, Hop[0][1]);
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Hop[1][0][s] = sym_tr(sblk, s);
                 }
                 if constexpr (SHARED) {
                     // the H slots were last read before the previous step's final barrier
@@ -1250,6 +1286,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                         const u32x4 opa = j < RB ? Hop[j < RB ? j : 0][jk][s] : cur_op[j < RB ? 0 : j - RB];
 #pragma unroll
                         for (int rb = 0; rb < RB; ++rb) {
+                            if (SYM64 && rb == 1 && j == 0) continue;  // aI + P is symmetric too
                             const u32x4 opb = jk == rb ? Q0[rb][s] : Hop[rb][jk][s];
                             acc[rb][j] = mma1<OP>(opa, opb, acc[rb][j]);
                         }
@@ -1262,9 +1299,16 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     for (int j = 0; j < NB; ++j)
 #pragma unroll
                         for (int s = 0; s < S; ++s) {
+                            if (SYM64 && rb == 1 && j == 0) continue;
                             if constexpr (CMODE == 0) Pop[rb][j][s] = make_slot<OP>(acc[rb][j], s);
                             else Pop[rb][j][s] = make_slot<OP>(-acc[rb][j], s);
                         }
+                if constexpr (SYM64) {
+                    // (aI + P)(1, 0) = (aI + P)(0, 1)^T
+                    sym_put(sblk + 2048, Pop[0][1]);
+#pragma unroll
+                    for (int s = 0; s < S; ++s) Pop[1][0][s] = sym_tr(sblk + 2048, s);
+                }
             } else {
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)

@@ -240,13 +240,14 @@ int himuon_gemm_tune_hw(int64_t n_mats, const int64_t* rows, const int64_t* cols
  *                          rounded to `dtype`, and the lookahead is formed from
  *                          the stored value.
  * T, K, a, b, c            as himuon_ns_gemm: T = 0 or any positive tile size.
- *                          Routes: T in {32, 64, 128} with bf16 storage, fp16
- *                          operands and c > 0 runs the step inside the fused
- *                          tile kernel (the lookahead is rounded to bf16 as
- *                          the tile is staged, U as it is written back); other
- *                          T in {32, 64, 128, 256} with a fused kernel runs an
- *                          element-wise prologue and epilogue around it, with
- *                          the lookahead held in `dtype` in the workspace; any
+ *                          Routes: T in {32, 64, 128} runs the step inside the
+ *                          fused tile kernel (fp32 storage, bf16 operands, or
+ *                          fp16 operands with c > 0; U is rounded to `dtype`
+ *                          before the update, and with fp16 operands so is the
+ *                          lookahead as the tile is staged); T = 256, and fp16
+ *                          operands with c <= 0, run an element-wise prologue
+ *                          and epilogue around the fused kernel, with the
+ *                          lookahead held in `dtype` in the workspace; any
  *                          other T runs the library-GEMM path with the
  *                          momentum fused into its gather and the update into
  *                          its scatter.

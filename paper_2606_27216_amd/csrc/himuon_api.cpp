@@ -254,7 +254,9 @@ size_t tiled_workspace(int64_t n_mats, bool step)
 
 bool has_step_kernel(int T, Storage st, Operand op, float c)
 {
-    return (T == 32 || T == 64 || T == 128) && st == Storage::BF16 && op == Operand::F16 && c > 0.f;
+    if (T != 32 && T != 64 && T != 128) return false;
+    if (op == Operand::F16) return st == Storage::BF16 && c > 0.f;  // the fp16 kernels' step variants
+    return has_kernel(T, st, op);                                   // fp32 storage, bf16 operands
 }
 
 int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,

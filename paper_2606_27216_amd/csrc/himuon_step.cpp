@@ -5,15 +5,15 @@
 //   W <- (1 - lr lambda) W - lr tau U, tau = c sqrt(max(H, W)) on the full
 //       branch and c sqrt(T) when tiled (Sec. 4.3, eq. scaled_update).
 // Three execution routes, chosen from T and the types:
-//   - T in {32, 64, 128}, bf16 storage, fp16 operands, c > 0: the step
-//     inside the fused tile kernel (its staging forms the momentum and the
-//     lookahead, its write-back the weight update), so every matrix is read
-//     and written once;
-//   - other T in {32, 64, 128, 256} with a fused tile kernel for the types:
-//     an element-wise prologue (momentum and lookahead into a contiguous
-//     buffer), the tiled map in place on that buffer, and an element-wise
-//     epilogue (decay and update); matrices are taken in consecutive groups
-//     whose buffers fit the chunk budget;
+//   - T in {32, 64, 128} (fp32 storage; bf16 storage with bf16 operands; bf16
+//     storage with fp16 operands when c > 0): the step inside the fused tile
+//     kernel (its gather forms the momentum and the lookahead, its
+//     write-back the weight update), so every matrix is read and written once;
+//   - T = 256, or c <= 0 with fp16 operands: an element-wise prologue
+//     (momentum and lookahead into a contiguous buffer), the tiled map in
+//     place on that buffer, and an element-wise epilogue (decay and update);
+//     matrices are taken in consecutive groups whose buffers fit the chunk
+//     budget;
 //   - otherwise (T = 0, large tiles such as 512): the library-GEMM path with
 //     the momentum fused into its norm and gather kernels and the update into
 //     its scatter kernel.

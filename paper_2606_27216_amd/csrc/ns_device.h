@@ -181,6 +181,20 @@ HM_DEV f32x4 load4(const void* base, int64_t gr, int64_t gc, int64_t ld, int64_t
     }
 }
 
+// The values a store4 of v leaves in memory (bf16: rounded to nearest even).
+template <Storage ST>
+HM_DEV f32x4 stored4(const f32x4& v)
+{
+    if constexpr (ST == Storage::BF16) {
+        f32x4 r;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r[e] = (float)(__bf16)v[e];
+        return r;
+    } else {
+        return v;
+    }
+}
+
 // Store four values (rounded to nearest even for bf16), dropping the
 // padding (inverse tiling operator).
 template <Storage ST>

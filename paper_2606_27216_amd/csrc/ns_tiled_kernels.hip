@@ -47,7 +47,11 @@ constexpr int kThreads = 256;  // four waves per workgroup
 
 // T: tile size; RB: 32-row blocks per wave. A tile is spread over
 // WT = T/(32 RB) waves, and a workgroup of four waves runs 4/WT tiles.
-template <int T, int RB, Storage ST, Operand OP>
+// OPT: the optimizer step of Alg. 1 rides on the tile I/O (KernelArgs): the
+// gather loads G and M, stores M <- beta M + G and takes the lookahead
+// G + beta M (Nesterov) or M, formed from the stored M, as the tile; the
+// write-back loads W and stores (1 - lr lambda) W - lr tau U.
+template <int T, int RB, Storage ST, Operand OP, bool OPT = false>
 __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs args)
 {
     constexpr int NB = T / 32;
@@ -100,6 +104,15 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
         const bool vout = full && (d.flags & MAT_VEC_OUT);
         const int64_t rows_eff = valid ? d.rows : 0;  // an idle wave reads zeros
 
+        void* mom = nullptr;
+        float tau = 0.f;
+        if constexpr (OPT) {
+            typedef __attribute__((address_space(4))) const OptDesc ConstOpt;
+            const ConstOpt& O = ((const ConstOpt*)(uintptr_t)args.odescs)[lo];
+            mom = O.mom;
+            tau = O.tau;
+        }
+
         // ---- gather the tile (zero padded) into fp32 row pieces
         f32x16 X[RB][NB];
 #pragma unroll
@@ -109,11 +122,25 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
             for (int q = 0; q < NB; ++q)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
-                    const f32x4 v = load4<ST>(d.in, gr, col0 + 32 * q + 8 * g + 4 * lh, d.ld_in, rows_eff, d.cols, vin);
-                    X[rb][q][4 * g + 0] = v[0];
-                    X[rb][q][4 * g + 1] = v[1];
-                    X[rb][q][4 * g + 2] = v[2];
-                    X[rb][q][4 * g + 3] = v[3];
+                    const int64_t gc = col0 + 32 * q + 8 * g + 4 * lh;
+                    const f32x4 v = load4<ST>(d.in, gr, gc, d.ld_in, rows_eff, d.cols, vin);
+                    float x4[4] = {v[0], v[1], v[2], v[3]};
+                    if constexpr (OPT) {
+                        // (the momentum shares the gradient's layout; padding stays zero)
+                        const f32x4 m = load4<ST>(mom, gr, gc, d.ld_in, rows_eff, d.cols, vin);
+                        const f32x4 mn = stored4<ST>(f32x4{args.beta * m[0] + x4[0], args.beta * m[1] + x4[1],
+                                                           args.beta * m[2] + x4[2], args.beta * m[3] + x4[3]});
+                        if (valid) store4<ST>(mom, gr, gc, d.ld_in, d.rows, d.cols, vin, mn);
+                        const float nb = args.nesterov ? args.beta : 0.f;
+                        const float keep = args.nesterov ? 1.f : 0.f;
+                        const float mb = args.nesterov ? 0.f : 1.f;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) x4[e] = keep * x4[e] + nb * mn[e] + mb * mn[e];
+                    }
+                    X[rb][q][4 * g + 0] = x4[0];
+                    X[rb][q][4 * g + 1] = x4[1];
+                    X[rb][q][4 * g + 2] = x4[2];
+                    X[rb][q][4 * g + 3] = x4[3];
                 }
         }
 
@@ -352,9 +379,18 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
                 for (int q = 0; q < NB; ++q)
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
-                        const f32x4 v = {X[rb][q][4 * g + 0], X[rb][q][4 * g + 1], X[rb][q][4 * g + 2],
-                                         X[rb][q][4 * g + 3]};
-                        store4<ST>(d.out, gr, col0 + 32 * q + 8 * g + 4 * lh, d.ld_out, d.rows, d.cols, vout, v);
+                        const int64_t gc = col0 + 32 * q + 8 * g + 4 * lh;
+                        f32x4 v = {X[rb][q][4 * g + 0], X[rb][q][4 * g + 1], X[rb][q][4 * g + 2],
+                                   X[rb][q][4 * g + 3]};
+                        if constexpr (OPT) {
+                            // U as the storage type holds it, then the update of the loaded W
+                            const f32x4 u = stored4<ST>(v);
+                            const f32x4 w = load4<ST>(d.out, gr, gc, d.ld_out, d.rows, d.cols, vout);
+                            const float step = args.lr * tau;
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) v[e] = args.decay * w[e] - step * u[e];
+                        }
+                        store4<ST>(d.out, gr, gc, d.ld_out, d.rows, d.cols, vout, v);
                     }
             }
         }
@@ -365,7 +401,7 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
 
 constexpr int kMaxDevices = 64;
 
-template <int T, int RB, Storage ST, Operand OP>
+template <int T, int RB, Storage ST, Operand OP, bool OPT>
 hipError_t launch_one(const KernelArgs& args, hipStream_t stream)
 {
     constexpr int WT = (T / 32) / RB;
@@ -378,7 +414,7 @@ hipError_t launch_one(const KernelArgs& args, hipStream_t stream)
     int cap = resident[dev].load(std::memory_order_relaxed);
     if (cap == 0) {
         int per_cu = 0, cus = 0;
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ns_tiled_kernel<T, RB, ST, OP>, kThreads, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ns_tiled_kernel<T, RB, ST, OP, OPT>, kThreads, 0);
         if (e != hipSuccess) return e;
         e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
@@ -389,7 +425,7 @@ hipError_t launch_one(const KernelArgs& args, hipStream_t stream)
     if (n <= 0) return hipSuccess;
     const int64_t groups = (n + TPW - 1) / TPW;
     const int grid = (int)(groups < cap ? groups : cap);
-    hipLaunchKernelGGL((ns_tiled_kernel<T, RB, ST, OP>), dim3(grid), dim3(kThreads), 0, stream, args);
+    hipLaunchKernelGGL((ns_tiled_kernel<T, RB, ST, OP, OPT>), dim3(grid), dim3(kThreads), 0, stream, args);
     return hipGetLastError();
 }
 
@@ -398,10 +434,18 @@ hipError_t launch_one(const KernelArgs& args, hipStream_t stream)
 template <Storage ST, Operand OP>
 hipError_t launch_T(int T, const KernelArgs& args, hipStream_t stream)
 {
+    if (args.odescs) {
+        switch (T) {
+        case 32: return launch_one<32, 1, ST, OP, true>(args, stream);
+        case 64: return launch_one<64, 2, ST, OP, true>(args, stream);
+        case 128: return launch_one<128, 1, ST, OP, true>(args, stream);
+        default: return hipErrorInvalidValue;
+        }
+    }
     switch (T) {
-    case 32: return launch_one<32, 1, ST, OP>(args, stream);
-    case 64: return launch_one<64, 2, ST, OP>(args, stream);
-    case 128: return launch_one<128, 1, ST, OP>(args, stream);
+    case 32: return launch_one<32, 1, ST, OP, false>(args, stream);
+    case 64: return launch_one<64, 2, ST, OP, false>(args, stream);
+    case 128: return launch_one<128, 1, ST, OP, false>(args, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -420,7 +464,6 @@ bool has_kernel(int T, Storage st, Operand op)
 hipError_t launch_ns_tiled(int T, Storage st, Operand op, const KernelArgs& args, hipStream_t stream)
 {
     if (!has_kernel(T, st, op)) return hipErrorInvalidValue;
-    if (args.odescs && op != Operand::F16) return hipErrorInvalidValue;  // the step rides on the fp16 kernels only
     if (st == Storage::F32) return launch_T<Storage::F32, Operand::F32>(T, args, stream);
     if (op == Operand::F16) return launch_ns_tiled_f16(T, args, stream);
     return launch_T<Storage::BF16, Operand::BF16>(T, args, stream);

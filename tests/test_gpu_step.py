@@ -2,9 +2,9 @@
 
 All three routes are covered: the library-GEMM path (T = 0, the
 full-matrix branch, and T = 512) with the momentum fused into its gather and
-the update into its scatter; the step inside the fused tile kernels (bf16,
-T = 128, 64, 32); and the fused tile kernels with element-wise prologue and
-epilogue (T = 256; fp32 storage). Bars:
+the update into its scatter; the step inside the fused tile kernels (T = 128,
+64, 32: bf16 with fp16 or bf16 operands, fp32); and the fused tile kernels
+with element-wise prologue and epilogue (T = 256; c = 0). Bars:
   - momentum M: each element within one unit in the last place of the
     storage type of the oracle's value (the GPU rounds beta M + G once to
     storage; the oracle keeps fp64);
@@ -207,19 +207,60 @@ def test_zero_gradient_and_momentum():
         assert np.allclose(to_f64(W), d * to_f64(W0), rtol=2 ** -23, atol=0)
 
 
-def test_fused_route_fp32_prologue_epilogue():
-    """fp32 storage at T = 128: the generic tile kernel between the element-wise
-    prologue and epilogue."""
+@pytest.mark.parametrize("T", [128, 64, 32])
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_in_kernel_route_fp32(T, nesterov):
+    """fp32 storage: the step inside the generic tile kernel (fp32 operands)."""
     shapes = [(384, 520), (100, 60)]
-    announce(f"step fp32 T=128 shapes={shapes}")
+    announce(f"step fp32 T={T} nesterov={nesterov} shapes={shapes}")
     W0 = [rand(s, torch.float32, 150 + i) for i, s in enumerate(shapes)]
     G = [rand(s, torch.float32, 160 + i, 1e-2) for i, s in enumerate(shapes)]
     M0 = [rand(s, torch.float32, 170 + i, 1e-2) for i, s in enumerate(shapes)]
     W1 = [w.clone() for w in W0]
     M1 = [m.clone() for m in M0]
-    run_step(W1, G, M1, 128, torch.float32)
+    run_step(W1, G, M1, T, torch.float32, nesterov=nesterov)
     for i in range(len(shapes)):
-        check_step(W0[i], G[i], M0[i], W1[i], M1[i], 128, torch.float32, 0.02, 0.95, 0.1, True, 0.2)
+        check_step(W0[i], G[i], M0[i], W1[i], M1[i], T, torch.float32, 0.02, 0.95, 0.1, nesterov, 0.2)
+
+
+def test_in_kernel_route_bf16_operands():
+    """bf16 storage with bf16 MFMA operands: the step inside the generic kernel."""
+    shapes = [(384, 520), (100, 60)]
+    announce(f"step bf16 operands T=128 shapes={shapes}")
+    W0 = [rand(s, torch.bfloat16, 190 + i) for i, s in enumerate(shapes)]
+    G = [rand(s, torch.bfloat16, 191 + i, 1e-2) for i, s in enumerate(shapes)]
+    M0 = [rand(s, torch.bfloat16, 192 + i, 1e-2) for i, s in enumerate(shapes)]
+    W1 = [w.clone() for w in W0]
+    M1 = [m.clone() for m in M0]
+    hm.step(W1, G, M1, T=128, K=5, coeffs=COEF32, lr=0.02, momentum=0.95, weight_decay=0.1, nesterov=True,
+            scale_c=0.2, compute=hm.COMPUTE_BF16)
+    torch.cuda.synchronize()
+    for i in range(len(shapes)):
+        check_step(W0[i], G[i], M0[i], W1[i], M1[i], 128, torch.bfloat16, 0.02, 0.95, 0.1, True, 0.2)
+
+
+def test_prologue_epilogue_route_c_zero():
+    """c = 0 (the cubic (1.5, -0.5, 0)) at T = 128, bf16: the fp16 kernel has no
+    step variant for it, so the element-wise prologue and epilogue run around it."""
+    cubic = (1.5, -0.5, 0.0)
+    shapes = [(300, 200)]
+    announce("step c = 0 bf16 T=128 (prologue/epilogue)")
+    W0 = [rand(s, torch.bfloat16, 195) for s in shapes]
+    G = [rand(s, torch.bfloat16, 196, 1e-2) for s in shapes]
+    M0 = [rand(s, torch.bfloat16, 197, 1e-2) for s in shapes]
+    W1 = [w.clone() for w in W0]
+    M1 = [m.clone() for m in M0]
+    hm.step(W1, G, M1, T=128, K=5, coeffs=cubic, lr=0.02, momentum=0.95, weight_decay=0.1, nesterov=True,
+            scale_c=0.2)
+    torch.cuda.synchronize()
+    Wr, Mr, Ur = oracle.himuon_step(to_f64(W0[0]), to_f64(M0[0]), to_f64(G[0]), 128, 5, *cubic, f32(0.02),
+                                    f32(0.95), f32(0.1), True, f32(0.2))
+    upd = f32(0.02) * tau_of(300, 200, 128, 0.2) * Ur
+    for r0 in range(0, 300, 128):
+        for c0 in range(0, 200, 128):
+            sl = np.s_[r0:r0 + 128, c0:c0 + 128]
+            err = np.linalg.norm(to_f64(W1[0])[sl] - Wr[sl])
+            assert err <= 2e-2 * np.linalg.norm(upd[sl]) + 2.0 ** -8 * np.linalg.norm(Wr[sl])
 
 
 def _p_iter(K, s=1.0):

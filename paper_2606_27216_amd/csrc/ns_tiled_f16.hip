@@ -104,6 +104,16 @@ HM_DEV u32x2 load_bf16x4(const void* base, int64_t gr, int64_t gc, int64_t ld, i
     return u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
 }
 
+// Two packed fp16 additions (v_pk_add_f16), written out: for f16x2 adds on
+// the four words of a u32x4 operand slot the compiler emitted four
+// v_pk_add_f16 that all read the slot's first word.
+HM_DEV uint32_t pk_add_f16(uint32_t a, uint32_t b)
+{
+    uint32_t r;
+    asm("v_pk_add_f16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
 HM_DEV u32x2 tr_read(const uint8_t* ptr)
 {
     typedef short s4 __attribute__((ext_vector_type(4)));
@@ -217,6 +227,17 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     // A diagonal block holds row li's column 8g + 4lh + e in register 4g + e,
     // so the diagonal entry of this lane (if any) is register vdiag.
     const int vdiag = (lh == ((li >> 2) & 1)) ? 4 * (li >> 3) + (li & 3) : -1;
+    // sigma b' in the packed fp16 operand word of that diagonal entry (word x of
+    // slot s holds registers 8s + 2x and 8s + 2x + 1), zero elsewhere
+    uint32_t dq[2][4];
+    {
+        const uint32_t bq16 = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)args.bq);
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                dq[s][x] = (vdiag >= 0 && (vdiag >> 3) == s && ((vdiag & 7) >> 1) == x) ? (bq16 << (16 * (vdiag & 1))) : 0u;
+    }
     // sigma a I as a diagonal block (the seed of the aI + P accumulators)
     f32x16 diag_a = {};
 #pragma unroll
@@ -1227,11 +1248,13 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
                         for (int s = 0; s < S; ++s)
                             if (!(SYM64 && rb == 1 && j == 0)) Hop[rb][j][s] = make_slot<OP>(G[rb][j], s);
-                    f32x16 gd = G[rb][rb];  // H + sigma b' I on the diagonal block (p0 + rb, p0 + rb)
+                    // H + sigma b' I on the diagonal block (p0 + rb, p0 + rb): the
+                    // shift is added to the fp16 operand word that holds this
+                    // lane's diagonal entry (one packed add per word)
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) gd[v] += v == vdiag ? args.bq : 0.f;
+                    for (int s = 0; s < S; ++s)
 #pragma unroll
-                    for (int s = 0; s < S; ++s) Q0[rb][s] = make_slot<OP>(gd, s);
+                        for (int x = 0; x < 4; ++x) Q0[rb][s][x] = pk_add_f16(Hop[rb][rb][s][x], dq[s][x]);
                 }
                 if constexpr (SYM64) {
                     // H(1, 0) = H(0, 1)^T

@@ -141,7 +141,8 @@ int himuon_ns_tiled(int64_t n_mats,
  * norm of each problem is summed in fp64 in a fixed order, so a result does
  * not depend on the batch or chunk a problem lands in.
  *
- * Arguments are those of himuon_ns_tiled, except:
+ * Arguments are those of himuon_ns_tiled (out_ptrs[l] == in_ptrs[l] is
+ * allowed: a chunk gathers all its blocks before it scatters any), except:
  * T                   0 or any positive tile size.
  * workspace           device memory of at least himuon_ns_gemm_workspace_size
  *                     (same arguments) bytes, owned by the caller: the

@@ -174,3 +174,19 @@ def test_tiles_256_where_no_fused_kernel_exists(dtype, compute):
     y = gemm([x], T=256, compute=compute)[0]
     e = tile_errors(to_f64(y), oracle.ns_tiled(to_f64(x), 256, 5, *COEF32), 256)
     assert e.max() <= TOL[dtype], f"max per-tile error {e.max():.3e}"
+
+
+@pytest.mark.parametrize("T", [512, 0])
+def test_in_place_equals_out_of_place(T):
+    """out == in (allowed, as for himuon_ns_tiled): each chunk gathers all of
+    its blocks before it scatters any, and blocks of different problems do
+    not overlap, so the result is the out-of-place one, bit for bit."""
+    announce(f"gemm in place, T={T}, bf16, several chunks")
+    mats = [rand((700, 900), torch.bfloat16, 61), rand((1024, 512), torch.bfloat16, 62)]
+    budget = 2 * (2 * 512 * 512 + 2 * 512 * 512) * 2 if T else 0  # two 512-tiles per chunk
+    ref = hm.ns_gemm(mats, T=T, K=5, coeffs=COEF32, chunk_budget_bytes=budget)
+    inplace = [m.clone() for m in mats]
+    hm.ns_gemm(inplace, outputs=inplace, T=T, K=5, coeffs=COEF32, chunk_budget_bytes=budget)
+    torch.cuda.synchronize()
+    for a, b in zip(ref, inplace):
+        assert torch.equal(a, b)

@@ -62,8 +62,9 @@ typedef enum himuon_status {
     HIMUON_OK = 0,
     HIMUON_ERR_INVALID_ARG = -1, /* null pointer, rows/cols < 1, ld < cols, K < 0,
                                     n_mats < 1, non-finite a/b/c, unknown enum     */
-    HIMUON_ERR_UNSUPPORTED = -2, /* T not in {32, 64, 128, 256}, or a dtype/compute
-                                    pair that has no kernel                        */
+    HIMUON_ERR_UNSUPPORTED = -2, /* T not in {32, 64, 128, 256}, a dtype/compute
+                                    pair that has no kernel, or (himuon_ns_tiled)
+                                    2^32 or more tiles in one call                 */
     HIMUON_ERR_WORKSPACE = -3,   /* workspace smaller than
                                     himuon_ns_tiled_workspace_size(n_mats), or a
                                     chunk budget smaller than one tile             */

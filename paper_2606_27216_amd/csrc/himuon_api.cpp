@@ -291,6 +291,8 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
     if (s != HIMUON_OK) return s;
     s = plan_chunk_count(total, T, elem_size(dtype), chunk_budget_bytes, &n_chunks);
     if (s != HIMUON_OK) return s;
+    // the kernels number the tiles of a call with 32-bit ids
+    if (total > (int64_t)UINT32_MAX) return HIMUON_ERR_UNSUPPORTED;
 
     // ---- descriptor table
     // 16-byte accesses at every column multiple of 8 (bf16) or 4 (f32)

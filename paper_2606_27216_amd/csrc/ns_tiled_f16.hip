@@ -66,24 +66,28 @@ HM_DEV uint32_t wave_max_u32(uint32_t v)
 }
 
 // Matrix owning `tile`, searching from `hint` (the tiles one wave visits only
-// grow, so the owner of an earlier tile is a lower bound). The first tiles of
-// the next four matrices are loaded together (independent scalar loads), which
-// settles the usual case in one round trip; a binary search covers the rest.
+// grow, so the owner of an earlier tile is a lower bound). Tile ids of one
+// call fit in 32 bits (the host rejects larger calls), so every comparison is
+// a scalar 32-bit one. The first tiles of the next four matrices are loaded
+// unconditionally (indices clamped to the table), so the four scalar loads go
+// out together and the usual case costs one round trip; a binary search
+// covers the rest.
 HM_DEV int find_matrix_from(const KernelArgs& args, int64_t tile, int hint)
 {
     const ConstDesc* const descs = desc_table(args);
     constexpr int kAhead = 4;
+    const uint32_t t = (uint32_t)tile;
+    uint32_t tb[kAhead];
+#pragma unroll
+    for (int j = 0; j < kAhead; ++j) tb[j] = (uint32_t)descs[min(hint + 1 + j, args.n_mats - 1)].tile_begin;
     int passed = 0;
 #pragma unroll
-    for (int j = 1; j <= kAhead; ++j) {
-        const int idx = min(hint + j, args.n_mats - 1);
-        passed += (hint + j < args.n_mats && descs[idx].tile_begin <= tile) ? 1 : 0;
-    }
+    for (int j = 0; j < kAhead; ++j) passed += (hint + 1 + j < args.n_mats && tb[j] <= t) ? 1 : 0;
     if (passed < kAhead) return hint + passed;
     int lo = hint + kAhead, hi = args.n_mats - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (descs[mid].tile_begin <= tile) lo = mid;
+        if ((uint32_t)descs[mid].tile_begin <= t) lo = mid;
         else hi = mid - 1;
     }
     return __builtin_amdgcn_readfirstlane(lo);
@@ -281,13 +285,16 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         L.cols = D.cols;
         L.ld_in = D.ld_in;
         L.ld_out = D.ld_out;
-        const int64_t lt = tile - D.tile_begin;
-        const int64_t tr = lt / D.tiles_c;
-        L.row0 = tr * T;
-        L.col0 = (lt - tr * D.tiles_c) * T;
+        // (32-bit: a 64-bit division would expand to a long scalar sequence)
+        const uint32_t lt = (uint32_t)(tile - D.tile_begin);
+        const uint32_t tc = (uint32_t)D.tiles_c;
+        const uint32_t tr = lt / tc;
+        L.row0 = (int64_t)tr * T;
+        L.col0 = (int64_t)(lt - tr * tc) * T;
         const bool full = L.row0 + T <= L.rows && L.col0 + T <= L.cols;
-        L.vin = full && (D.flags & MAT_VEC_IN);
-        L.vout = full && (D.flags & MAT_VEC_OUT);
+        const int32_t fl = D.flags;  // (read unconditionally: no dependent scalar load)
+        L.vin = full & ((fl & MAT_VEC_IN) != 0);
+        L.vout = full & ((fl & MAT_VEC_OUT) != 0);
         if constexpr (OPT) {
             typedef __attribute__((address_space(4))) const OptDesc ConstOpt;
             const ConstOpt& O = ((const ConstOpt*)(uintptr_t)args.odescs)[mhint];

@@ -69,6 +69,8 @@ def _call(**kw):
     (dict(workspace_bytes=255), hm.ERR_WORKSPACE),
     (dict(chunk_budget_bytes=100), hm.ERR_WORKSPACE),
     (dict(compute=hm.COMPUTE_F16, a=50.0, b=0.0, c=0.0), hm.ERR_RANGE),
+    # 2^32 tiles in one call (the kernels number tiles with 32-bit ids)
+    (dict(rows=[1 << 37], cols=[32]), hm.ERR_UNSUPPORTED),
 ])
 def test_validation_rejects_before_any_hip_call(kw, status):
     assert _call(**kw) == status

@@ -648,12 +648,6 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
             auto zrow = [&](int br, int q, int s) -> u32x4 {
                 return *reinterpret_cast<const u32x4*>(rm + 32 * br * RS + 64 * q + rpB[s]);
             };
-            auto shifted = [&](const f32x16& gd) -> f32x16 {
-                f32x16 r = gd;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) r[v] += v == vdiag ? args.bq : 0.f;
-                return r;
-            };
 
             for (int k = 0; k < args.K; ++k) {
                 // ---- Gram. The operands of the current Z are made here, each
@@ -716,9 +710,12 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
                             for (int x = 0; x < S; ++x) hs[0][x] = make_slot<OP>(g[0], x);
                         } else if (it == 1) {
-                            const f32x16 gd = shifted(g[0]);
+                            // H + sigma b' I: one packed fp16 add on the operand
+                            // word that holds this lane's diagonal entry
 #pragma unroll
-                            for (int x = 0; x < S; ++x) qs[0][x] = make_slot<OP>(gd, x);
+                            for (int x = 0; x < S; ++x)
+#pragma unroll
+                                for (int y = 0; y < 4; ++y) qs[0][x][y] = pk_add_f16(hs[0][x][y], dq[x][y]);
                         } else if (it == 2) {
 #pragma unroll
                             for (int x = 0; x < S; ++x) hs[1][x] = make_slot<OP>(g[1], x);
@@ -728,9 +725,10 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
                             for (int x = 0; x < S; ++x) hs[2][x] = make_slot<OP>(g[2], x);
                         } else if (it == 4) {
-                            const f32x16 gd = shifted(g[2]);
 #pragma unroll
-                            for (int x = 0; x < S; ++x) qs[1][x] = make_slot<OP>(gd, x);
+                            for (int x = 0; x < S; ++x)
+#pragma unroll
+                                for (int y = 0; y < 4; ++y) qs[1][x][y] = pk_add_f16(hs[2][x][y], dq[x][y]);
                         } else if (it == 5) {
                             blk_put(hblk(w, 2), qs[1]);
 #pragma unroll

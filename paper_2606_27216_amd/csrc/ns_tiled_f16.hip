@@ -270,7 +270,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         void* out;
         int64_t rows, cols, ld_in, ld_out;
         int64_t row0, col0;
-        bool vin, vout;
+        int32_t vin, vout;  // (not bool: a struct with bools is not split into registers)
         void* mom;  // OPT: the momentum buffer (layout of `in`) and tau
         float tau;
     };

@@ -31,6 +31,34 @@ typedef __attribute__((address_space(1))) u32x4 gbl_u32x4;
 typedef __attribute__((address_space(4))) const MatDesc ConstDesc;
 HM_DEV const ConstDesc* desc_table(const KernelArgs& a) { return (const ConstDesc*)(uintptr_t)a.descs; }
 
+// Matrix owning `tile`, searching from `hint` (the tiles one wave visits only
+// grow, so the owner of an earlier tile is a lower bound). Tile ids of one
+// call fit in 32 bits (the host rejects larger calls), so every comparison is
+// a scalar 32-bit one. The first tiles of the next four matrices are loaded
+// unconditionally (indices clamped to the table), so the four scalar loads go
+// out together and the usual case costs one round trip; a binary search
+// covers the rest.
+HM_DEV int find_matrix_from(const KernelArgs& args, int64_t tile, int hint)
+{
+    const ConstDesc* const descs = desc_table(args);
+    constexpr int kAhead = 4;
+    const uint32_t t = (uint32_t)tile;
+    uint32_t tb[kAhead];
+#pragma unroll
+    for (int j = 0; j < kAhead; ++j) tb[j] = (uint32_t)descs[min(hint + 1 + j, args.n_mats - 1)].tile_begin;
+    int passed = 0;
+#pragma unroll
+    for (int j = 0; j < kAhead; ++j) passed += (hint + 1 + j < args.n_mats && tb[j] <= t) ? 1 : 0;
+    if (passed < kAhead) return hint + passed;
+    int lo = hint + kAhead, hi = args.n_mats - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if ((uint32_t)descs[mid].tile_begin <= t) lo = mid;
+        else hi = mid - 1;
+    }
+    return __builtin_amdgcn_readfirstlane(lo);
+}
+
 // 16-byte operand slots per lane per 32x32 block: a slot feeds one
 // 32x32x16 fp16/bf16 MFMA (8 values) or four 32x32x2 fp32 MFMAs (4 values).
 // kChains: independent accumulators per output block. The fp32 path spreads

@@ -65,34 +65,6 @@ HM_DEV uint32_t wave_max_u32(uint32_t v)
     return v;
 }
 
-// Matrix owning `tile`, searching from `hint` (the tiles one wave visits only
-// grow, so the owner of an earlier tile is a lower bound). Tile ids of one
-// call fit in 32 bits (the host rejects larger calls), so every comparison is
-// a scalar 32-bit one. The first tiles of the next four matrices are loaded
-// unconditionally (indices clamped to the table), so the four scalar loads go
-// out together and the usual case costs one round trip; a binary search
-// covers the rest.
-HM_DEV int find_matrix_from(const KernelArgs& args, int64_t tile, int hint)
-{
-    const ConstDesc* const descs = desc_table(args);
-    constexpr int kAhead = 4;
-    const uint32_t t = (uint32_t)tile;
-    uint32_t tb[kAhead];
-#pragma unroll
-    for (int j = 0; j < kAhead; ++j) tb[j] = (uint32_t)descs[min(hint + 1 + j, args.n_mats - 1)].tile_begin;
-    int passed = 0;
-#pragma unroll
-    for (int j = 0; j < kAhead; ++j) passed += (hint + 1 + j < args.n_mats && tb[j] <= t) ? 1 : 0;
-    if (passed < kAhead) return hint + passed;
-    int lo = hint + kAhead, hi = args.n_mats - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if ((uint32_t)descs[mid].tile_begin <= t) lo = mid;
-        else hi = mid - 1;
-    }
-    return __builtin_amdgcn_readfirstlane(lo);
-}
-
 // Four consecutive bf16 elements of row gr (columns gc..gc+3) as two packed
 // words, zero outside the matrix (the zero padding of the tiling operator).
 HM_DEV u32x2 load_bf16x4(const void* base, int64_t gr, int64_t gc, int64_t ld, int64_t rows, int64_t cols, bool vec)

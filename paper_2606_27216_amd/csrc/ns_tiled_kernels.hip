@@ -78,6 +78,7 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
     const int64_t n_tiles = args.tile_end - args.tile_begin;
     const int64_t n_groups = (n_tiles + TPW - 1) / TPW;
 
+    int mhint = 0;  // owner of the wave's previous valid tile
     for (int64_t grp = blockIdx.x; grp < n_groups; grp += gridDim.x) {
         const int64_t local = grp * TPW + tslot;
         const bool valid = local < n_tiles;
@@ -86,19 +87,29 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
         }
         const int64_t tile = args.tile_begin + (valid ? local : 0);
 
-        // matrix owning the tile: last descriptor with tile_begin <= tile
+        // matrix owning the tile: last descriptor with tile_begin <= tile.
+        // A wave's valid tiles only grow, so the search starts from the
+        // previous owner; an idle wave (the chunk's first tile) searches all.
         const ConstDesc* const descs = desc_table(args);
-        int lo = 0, hi = args.n_mats - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (descs[mid].tile_begin <= tile) lo = mid;
-            else hi = mid - 1;
+        int lo;
+        if (valid) {
+            mhint = find_matrix_from(args, tile, mhint);
+            lo = mhint;
+        } else {
+            int l = 0, hi = args.n_mats - 1;
+            while (l < hi) {
+                const int mid = (l + hi + 1) >> 1;
+                if (descs[mid].tile_begin <= tile) l = mid;
+                else hi = mid - 1;
+            }
+            lo = __builtin_amdgcn_readfirstlane(l);
         }
-        lo = __builtin_amdgcn_readfirstlane(lo);
         const ConstDesc& d = descs[lo];
-        const int64_t lt = tile - d.tile_begin;
-        const int64_t tr = lt / d.tiles_c;
-        const int64_t row0 = tr * T, col0 = (lt - tr * d.tiles_c) * T;
+        // (32-bit: tile ids of one call fit in 32 bits, checked on the host)
+        const uint32_t lt = (uint32_t)(tile - d.tile_begin);
+        const uint32_t tc = (uint32_t)d.tiles_c;
+        const uint32_t tr = lt / tc;
+        const int64_t row0 = (int64_t)tr * T, col0 = (int64_t)(lt - tr * tc) * T;
         const bool full = row0 + T <= d.rows && col0 + T <= d.cols;
         const bool vin = full && (d.flags & MAT_VEC_IN);
         const bool vout = full && (d.flags & MAT_VEC_OUT);

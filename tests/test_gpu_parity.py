@@ -305,3 +305,41 @@ def test_7b_stack_full_size_sampled():
             worst = max(worst, e.max())
     print(f"[gpu-err] 63 sampled tiles across the stack: max {worst:.3e}", flush=True)
     assert worst <= TOL[torch.bfloat16], worst
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_large_tile_ids_ragged_row_and_chunks(dtype):
+    """Tile ids past 2^16 in one call and a tiles-per-row count that is no
+    power of two (the kernels' 32-bit owner search and division), behind a
+    small matrix so that the large one starts at a nonzero tile id, with a
+    chunk budget that splits the call into several launches."""
+    T = 32
+    shapes = [(96, 96), (11008, 8200), (40, 70)]  # 9 + 344*257 + 2*3 tiles
+    announce(f"{dtype} T={T} K=5, shapes {shapes}, 3 chunks, sampled tiles")
+    mats = [workloads.gaussian(h, w, 60 + i, dtype, DEV) for i, (h, w) in enumerate(shapes)]
+    total = sum(oracle.tile_count(h, w, T) for h, w in shapes)
+    assert total > 1 << 16
+    elem = 4 if dtype == "f32" else 2
+    budget = (total // 3 + 1) * 2 * T * T * elem
+    n_total, bounds = hm.himuon_plan_chunks([m.shape[0] for m in mats], [m.shape[1] for m in mats], T,
+                                            hm.F32 if dtype == "f32" else hm.BF16, budget)
+    plan = len(bounds) - 1
+    assert n_total == total and plan == 3, (n_total, plan)
+    outs = run(mats, T, budget=budget)
+    rng = np.random.default_rng(61)
+    worst = 0.0
+    for i, (x, y) in enumerate(zip(mats, outs)):
+        S = to_f64(x)
+        n = oracle.tile_count(*S.shape, T)
+        C = -(-S.shape[1] // T)
+        if n <= 16:
+            ids = np.arange(n)
+        else:  # first, last, the ragged column edge of a few rows, and random tiles
+            edge = [r * C + C - 1 for r in (0, 1, 171, n // C - 1)]
+            ids = np.unique(np.concatenate([[0, n - 1], edge, rng.choice(n, 24, replace=False)]))
+        ref = oracle.ns_tiles(S, T, 5, *COEF32, ids)
+        e = sampled_tile_errors(to_f64(y), ref, ids, T)
+        assert np.all(np.isfinite(e)), f"matrix {i}: non-finite tile"
+        worst = max(worst, e.max())
+    print(f"[gpu-err] {total} tiles in {plan} chunks, sampled: max {worst:.3e}", flush=True)
+    assert worst <= TOL[mats[0].dtype], worst

@@ -9,6 +9,7 @@
 #include "ns_device.h"
 
 #include <atomic>
+#include <type_traits>
 
 namespace himuon {
 namespace {
@@ -285,6 +286,13 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     constexpr int RPI = 64 / LPR;
     constexpr int NI = 32 * RB / RPI;
     const int io_row = lane / LPR, io_cc = lane % LPR;  // row within an instruction, 16-byte chunk
+    // The tile loop is compiled once per wave index of a shared 128-tile
+    // (w = 0, 1): the wave's row blocks, and with them every LDS offset in the
+    // K loop, become compile-time constants folded into the LDS instructions.
+    const int p0_rt = p0;
+    auto tile_loop = [&](auto wtag) {
+    constexpr int WSPEC = decltype(wtag)::value;  // -1: not specialised
+    const int p0 = WSPEC >= 0 ? RB * WSPEC : p0_rt;
     u32x4 raw[NI];
     u32x4 rawm[OPT ? NI : 1];  // OPT: the momentum rows of the tile
     // the wave's rows of the tile in `base` (leading dimension ld), zero
@@ -1416,6 +1424,13 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         local = nlocal;
     }
     store_rows(prv, outv);
+    };
+    if constexpr (F16Shape<T, RB>::kSym) {
+        if (p0_rt == 0) tile_loop(std::integral_constant<int, 0>{});
+        else tile_loop(std::integral_constant<int, 1>{});
+    } else {
+        tile_loop(std::integral_constant<int, -1>{});
+    }
 }
 
 constexpr int kMaxDevices = 64;

@@ -62,9 +62,9 @@ def test_no_scratch_and_lds_within_a_cu(src, extra):
     kernels = resource_usage(src, extra)
     assert kernels, f"no kernels reported for {src}"
     for name, r in kernels.items():
+        # no spill or private array in memory (spills into AGPRs or VGPR lanes
+        # stay in registers and are allowed)
         assert r.get("ScratchSize") == 0, f"{name}: scratch {r.get('ScratchSize')} B/lane"
-        # (SGPR spills go to VGPR lanes, not memory, and are allowed)
-        assert r.get("VGPRs Spill", 0) == 0, f"{name}: VGPR spills {r}"
         assert r.get("LDS Size", 0) <= LDS_PER_CU, f"{name}: LDS {r.get('LDS Size')}"
         assert r.get("VGPRs", 0) + r.get("AGPRs", 0) <= 512, f"{name}: registers {r}"
 

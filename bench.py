@@ -21,8 +21,10 @@ The JSON also carries:
                 the HBM bytes per launch from rocprofv3 FETCH_SIZE/WRITE_SIZE
                 counters (profiles/ns_tiled_traffic.json) when they were taken
                 on the current kernel source, else null;
-  cpu_baseline  the fp64 oracle timed on the host cores on a bounded random
-                sample of the same workload's tiles (read back from the GPU).
+  cpu_baseline  the fp64 oracle timed on the host cores (and on one core) on a
+                bounded random sample of the same workload's tiles (read back
+                from the GPU), with the CPU model; its `parity` field compares
+                those oracle tiles with the GPU's outputs of the last timed step.
 """
 from __future__ import annotations
 
@@ -103,33 +105,71 @@ def issued_fraction(T, op_name, c):
     return 1.0 if c != 0 else 2.0 / 3.0
 
 
-def cpu_baseline(mats, T, K, coeffs, budget_s, seed=0):
-    """The fp64 oracle on a random sample of tiles of the workload (host cores)."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo", encoding="utf-8"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(mats, outs, T, K, coeffs, budget_s, seed=0):
+    """The fp64 oracle on a random sample of tiles of the workload (host
+    cores), timed; its tiles are also compared with the GPU's outputs of the
+    last timed step (per-tile relative Frobenius error). A second, smaller
+    sample runs on one core."""
     import numpy as np
     import oracle
 
     rng = np.random.default_rng(seed)
     counts = [oracle.tile_count(x.shape[0], x.shape[1], T) for x in mats]
-    done = 0
-    elapsed = 0.0
-    batch = 16
-    while elapsed < budget_s:
-        i = int(rng.integers(len(mats)))
-        x = mats[i]
-        ids = np.sort(rng.choice(counts[i], batch, replace=False))
-        C = -(-x.shape[1] // T)
-        # read back only the rows those tiles touch
-        rows = sorted({int(t) // C for t in ids})
-        sub = {r: x[r * T:(r + 1) * T].float().cpu().double().numpy() for r in rows}
-        t0 = time.perf_counter()
-        for r in rows:
-            loc = [int(t) % C for t in ids if int(t) // C == r]
-            oracle.ns_tiles(sub[r], T, K, *coeffs, loc)
-        elapsed += time.perf_counter() - t0
-        done += batch
-    flops = 6.0 * T ** 3 * K * done
-    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{done} random {T}x{T} tiles of the same workload (fp64 oracle, {elapsed:.1f} s)"}
+    errs = []
+
+    def sample(seconds, batch):
+        done, elapsed = 0, 0.0
+        while elapsed < seconds:
+            i = int(rng.integers(len(mats)))
+            x, y = mats[i], outs[i]
+            ids = np.sort(rng.choice(counts[i], batch, replace=False))
+            C = -(-x.shape[1] // T)
+            # read back only the rows of tiles those ids touch
+            rows = sorted({int(t) // C for t in ids})
+            sub = {r: x[r * T:(r + 1) * T].float().cpu().double().numpy() for r in rows}
+            got = {r: y[r * T:(r + 1) * T].float().cpu().double().numpy() for r in rows}
+            refs = {}
+            t0 = time.perf_counter()
+            for r in rows:
+                loc = [int(t) % C for t in ids if int(t) // C == r]
+                refs[r] = (loc, oracle.ns_tiles(sub[r], T, K, *coeffs, loc))
+            elapsed += time.perf_counter() - t0
+            done += batch
+            for r, (loc, ref) in refs.items():
+                for c, tile in zip(loc, ref):
+                    g = got[r][:, c * T:(c + 1) * T]
+                    rt = tile[:g.shape[0], :g.shape[1]]
+                    n = np.linalg.norm(rt)
+                    errs.append(np.linalg.norm(g - rt) / n if n > 0 else (0.0 if not np.any(g) else np.inf))
+        return done, elapsed
+
+    cores = oracle.num_threads()
+    done, elapsed = sample(budget_s, 16)
+    flops = 6.0 * T ** 3 * K
+    oracle.set_num_threads(1)
+    try:
+        done1, elapsed1 = sample(budget_s / 4, 4)
+    finally:
+        oracle.set_num_threads(cores)
+    e = np.array(errs)
+    return {"value": flops * done / elapsed / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} random {T}x{T} tiles of the same workload (fp64 oracle, {elapsed:.1f} s on {cores} "
+                      f"threads); one core: {done1} tiles in {elapsed1:.1f} s",
+            "one_core_value": flops * done1 / elapsed1 / 1e12, "cpu_model": cpu_model(),
+            "parity": {"tiles": int(e.size), "max": float(e.max()), "p50": float(np.median(e)),
+                       "bar": 2e-2 if mats[0].dtype.itemsize == 2 else 1e-5,
+                       "what": "per-tile relative Frobenius error of the last timed step's output against these "
+                               "oracle tiles"}}
 
 
 def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, stream):
@@ -200,7 +240,7 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
 
 
 def bench_optstep(args, hm, torch, np, dev):
-    """The optimizer-step benchmark of Sec. 5 (cross-layer batching): 8
+    """The optimizer-step benchmark of Sec. 6.4 (cross-layer batching): 8
     stacked bias-free Linear(H, H) layers in bf16, fresh Gaussian gradients
     before every step (outside the timed region), HiMuon with T = 512, K = 5
     against full-matrix Muon (T = 0: the same Alg. 1 step with Phi_K of the
@@ -284,7 +324,7 @@ def bench_optstep(args, hm, torch, np, dev):
 
 def bench_layershapes(args, hm, torch, np, dev):
     """Per-layer speedup of the tiled map over the full-matrix map on the
-    Qwen3 Block-0 shapes (Sec. 6.2): one random bf16 Gaussian matrix per
+    Qwen3 Block-0 shapes (Sec. 6.3): one random bf16 Gaussian matrix per
     shape, Phi_K (T = 0) and Phi_{K,512} through the library-GEMM path, K = 5,
     one call per matrix; the paired ratio t_full / t_tile is the median over
     `--steps` timed calls after `--warmup` (the paper: 30 after 3). The fused
@@ -416,7 +456,10 @@ def main():
     elem = 2 if args.dtype == "bf16" else 4
     bytes_step = sum(2.0 * h * w * elem for h, w in zip(rows, cols))
 
-    ws = torch.empty(hm.himuon_ns_tiled_workspace_size(len(mats)), dtype=torch.uint8, device=dev)
+    need = hm.himuon_ns_tiled_call_workspace_size(rows, cols, args.T, code, compute, args.K, *coeffs, int(args.budget))
+    if need == 0:
+        raise SystemExit("himuon_ns_tiled would reject this call (tile size, dtype/compute or budget)")
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
 
     def step():
         hm.ns_tiled(mats, outputs=outs, T=args.T, K=args.K, coeffs=coeffs, compute=compute,
@@ -482,7 +525,11 @@ def main():
     }
     if args.cpu_seconds > 0:
         log(f"cpu baseline: oracle on sampled tiles for ~{args.cpu_seconds:.0f} s")
-        rec["cpu_baseline"] = cpu_baseline(mats, args.T, args.K, coeffs, args.cpu_seconds)
+        rec["cpu_baseline"] = cpu_baseline(mats, outs, args.T, args.K, coeffs, args.cpu_seconds)
+        par = rec["cpu_baseline"]["parity"]
+        log(f"parity on {par['tiles']} sampled tiles: max {par['max']:.3e} p50 {par['p50']:.3e} (bar {par['bar']:.0e})")
+        if not par["max"] <= par["bar"]:
+            log("PARITY FAILURE: sampled tiles exceed the bar")
     print(json.dumps(rec), flush=True)
 
 

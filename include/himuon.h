@@ -50,10 +50,14 @@ typedef enum himuon_dtype {
 typedef enum himuon_compute {
     HIMUON_COMPUTE_DEFAULT = 0, /* F32 for f32 storage; for bf16 storage F16 when the
                                    coefficients keep every operand inside the fp16
-                                   range (himuon_select_compute), else BF16          */
+                                   range (himuon_select_compute), else the call
+                                   fails with HIMUON_ERR_RANGE (it never switches
+                                   to BF16 operands on its own)                      */
     HIMUON_COMPUTE_F32 = 1,     /* fp32 operands (v_mfma_f32_32x32x2_f32)            */
     HIMUON_COMPUTE_F16 = 2,     /* fp16 operands, round-to-nearest-even              */
-    HIMUON_COMPUTE_BF16 = 3     /* bf16 operands, round-to-nearest-even              */
+    HIMUON_COMPUTE_BF16 = 3     /* bf16 operands, round-to-nearest-even; fp32 range,
+                                   but 8 significant bits: per-tile errors reach
+                                   several 1e-2 at T <= 64 or K >= 8              */
 } himuon_compute_t;
 
 /* Status codes. Every error is detected before anything is enqueued: a call
@@ -65,19 +69,32 @@ typedef enum himuon_status {
     HIMUON_ERR_UNSUPPORTED = -2, /* T not in {32, 64, 128, 256}, a dtype/compute
                                     pair that has no kernel, or (himuon_ns_tiled)
                                     2^32 or more tiles in one call                 */
-    HIMUON_ERR_WORKSPACE = -3,   /* workspace smaller than
-                                    himuon_ns_tiled_workspace_size(n_mats), or a
-                                    chunk budget smaller than one tile             */
+    HIMUON_ERR_WORKSPACE = -3,   /* workspace smaller than the call's
+                                    *_workspace_size, or a chunk budget smaller
+                                    than one tile or problem                      */
     HIMUON_ERR_HIP = -4,         /* a HIP runtime call failed (see
                                     himuon_last_hip_error)                         */
-    HIMUON_ERR_RANGE = -5        /* HIMUON_COMPUTE_F16 requested but the iterates can
-                                    leave the fp16 range for these a, b, c, K      */
+    HIMUON_ERR_RANGE = -5        /* fp16 operands (HIMUON_COMPUTE_F16, or DEFAULT
+                                    with bf16 storage) requested but the iterates
+                                    can leave the fp16 range for these a, b, c, K  */
 } himuon_status_t;
 
-/* Device workspace bytes a himuon_ns_tiled call over n_mats matrices needs:
- * the per-matrix descriptor table the kernels read (64 bytes per matrix,
- * rounded up to 256). Host-only; returns 0 for n_mats < 1. */
+/* Device workspace bytes a himuon_ns_tiled call over n_mats matrices needs
+ * when a fused tile kernel serves it (every T, dtype and compute mode except
+ * the T = 256 calls below): the per-matrix descriptor table the kernels read
+ * (64 bytes per matrix, rounded up to 256). Host-only; returns 0 for
+ * n_mats < 1. */
 size_t himuon_ns_tiled_workspace_size(int64_t n_mats);
+
+/* Device workspace bytes of the himuon_ns_tiled call with these arguments,
+ * whatever serves it: himuon_ns_tiled_workspace_size(n_mats) for a fused
+ * kernel; for T = 256 with fp32 storage or bf16 operands, which have no fused
+ * 256-tile kernel and run as 256 x 256 problems of the library-GEMM path
+ * inside the same call, what himuon_ns_gemm_workspace_size gives for T = 256.
+ * Host-only; 0 when the call would be rejected. */
+size_t himuon_ns_tiled_call_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T,
+                                           int dtype, int compute, int K, float a, float b, float c,
+                                           size_t chunk_budget_bytes);
 
 /*
  * Y_l = Phi_{K,T}(X_l) for l = 0 .. n_mats-1, enqueued on `stream`.
@@ -92,16 +109,21 @@ size_t himuon_ns_tiled_workspace_size(int64_t n_mats);
  *                          may be NULL, meaning contiguous rows (ld = cols).
  * T                        tile size, one of 32, 64, 128, 256. A matrix with
  *                          T >= max(H, W) is one zero-padded tile, which gives
- *                          Phi_K of the whole matrix (Sec. 4.4.3).
+ *                          Phi_K of the whole matrix (Sec. 4.4.3). T = 256 with
+ *                          fp32 storage or bf16 operands has no fused kernel:
+ *                          the call runs each 256-tile through the library
+ *                          GEMMs of himuon_ns_gemm (same results up to
+ *                          rounding; workspace and chunk budget as there).
  * K                        Newton-Schulz steps (>= 0). K = 0 returns S/||S||_F
  *                          per tile.
  * a, b, c                  the polynomial coefficients (finite), e.g. Muon's
  *                          quintic (3.4445, -4.7750, 2.0315), eq. (ns_quintic).
  * dtype, compute           himuon_dtype_t and himuon_compute_t values.
  * workspace                device memory of at least
- *                          himuon_ns_tiled_workspace_size(n_mats) bytes, owned by
- *                          the caller; it must stay untouched until the work
- *                          enqueued by this call has completed on `stream`.
+ *                          himuon_ns_tiled_call_workspace_size(...) bytes (for a
+ *                          fused kernel, himuon_ns_tiled_workspace_size(n_mats)),
+ *                          owned by the caller; it must stay untouched until the
+ *                          work enqueued by this call has completed on `stream`.
  * chunk_budget_bytes       bound on the bytes a chunk of tiles stands for
  *                          (input tile + output tile, 2*T*T*sizeof(dtype) per
  *                          tile); 0 means one chunk. Chunking never changes a
@@ -175,7 +197,7 @@ int himuon_ns_gemm(int64_t n_mats,
 
 /*
  * himuon_ns_gemm with rectangular Th x Tw tiles (the tile-shape study of
- * Sec. 5 and Sec. 2.1's tiling with T_h x T_w blocks): each matrix is padded
+ * Sec. 6.3 and Sec. 2.1's tiling with T_h x T_w blocks): each matrix is padded
  * to (R Th) x (C Tw), R = ceil(H/Th), C = ceil(W/Tw), and every tile goes
  * through Phi_K, a tile with Th > Tw by the orientation rule (its transpose
  * is iterated, so the Gram matrix is min(Th, Tw) square). Th = Tw = T is
@@ -232,7 +254,7 @@ int himuon_gemm_tune_hw(int64_t n_mats, const int64_t* rows, const int64_t* cols
  *          Phi_{K,T}(Ghat)  otherwise                 eq. (tiled_ns)
  *   W_l <- (1 - lr weight_decay) W_l - lr tau_l U     eq. (scaled_update)
  *   tau_l = scale_c sqrt(max(H_l, W_l)) on the full branch, scale_c sqrt(T)
- *           when tiled (Sec. 4.3; the paper's runs use scale_c = 0.2).
+ *           when tiled (Sec. 4.2; the paper's runs use scale_c = 0.2).
  *
  * weights[l], grads[l], moms[l]  device pointers, storage `dtype`, one
  *                          row-major layout (leading dimension ld[l]; ld may
@@ -281,7 +303,9 @@ int himuon_step(int64_t n_mats,
 
 /*
  * Host-only planner (no HIP call): the tiles and chunks himuon_ns_tiled
- * would use. Tiles are numbered matrix by matrix, row-major over each
+ * would use, i.e. the memory-bounded chunking of cross-layer batches of
+ * Sec. 4.4.2 (a batch larger than the memory budget is split into the
+ * fewest chunks that fit). Tiles are numbered matrix by matrix, row-major over each
  * matrix's R x C grid. The chunk count is the fewest whose per-chunk bytes
  * (2*T*T*sizeof(dtype) per tile) fit chunk_budget_bytes (0: one chunk), and
  * the chunks are balanced: chunk i covers [bounds[i], bounds[i+1]) with
@@ -303,7 +327,7 @@ int himuon_plan_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols,
  * and HIMUON_COMPUTE_DEFAULT it returns F16 when the scalar iterates
  * p^k(s), s in [0, 1], k <= K (p(s) = as + bs^3 + cs^5, which is what every
  * singular value of the normalised tile follows, Sec. 2.2) bound |X|, |A|,
- * |A^2| and |bA + cA^2| well inside fp16's range, else BF16.
+ * |A^2| and |bA + cA^2| well inside fp16's range, else HIMUON_ERR_RANGE.
  */
 int himuon_select_compute(int dtype, int compute, int K, float a, float b, float c);
 

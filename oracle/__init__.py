@@ -161,6 +161,17 @@ def himuon_step(W, M, G, T, K, a, b, c, lr, beta, weight_decay, nesterov, scale_
     return W1, M1, U
 
 
+def set_num_threads(n: int, lib=None) -> None:
+    """Thread count of the oracle's OpenMP loops over tiles (through the
+    OpenMP runtime the library is linked with; results do not depend on it,
+    each tile being computed by one thread)."""
+    lib = lib or load()
+    f = lib.omp_set_num_threads
+    f.argtypes = [ctypes.c_int]
+    f.restype = None
+    f(int(n))
+
+
 def num_threads(lib=None):
     lib = lib or load()
     return int(lib.oracle_num_threads())

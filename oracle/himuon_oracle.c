@@ -229,8 +229,8 @@ int oracle_ns_tiles(const double* A, int64_t H, int64_t W, int64_t ld_in, int64_
 }
 
 /*
- * One HiMuon optimizer step of one matrix (Sec. 3.4's Muon update with the
- * tiled map substituted, Alg. 1, Sec. 4.3 eq. (scaled_update)), in place on
+ * One HiMuon optimizer step of one matrix (Sec. 2.3's Muon update with the
+ * tiled map substituted: Alg. 1 of Sec. 4.3, eq. (scaled_update) of Sec. 4.2), in place on
  * the H x W weights Wt and momentum Mt (both contiguous), given the gradient
  * G (contiguous):
  *   M   <- beta M + G                                   eq. (muon_momentum)

@@ -49,6 +49,10 @@ def lib():
         i64, vp, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
         L.himuon_ns_tiled_workspace_size.argtypes = [i64]
         L.himuon_ns_tiled_workspace_size.restype = sz
+        L.himuon_ns_tiled_call_workspace_size.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                          ctypes.c_int, ctypes.c_float, ctypes.c_float,
+                                                          ctypes.c_float, sz]
+        L.himuon_ns_tiled_call_workspace_size.restype = sz
         L.himuon_ns_tiled.argtypes = [i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int,
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                       ctypes.c_int, ctypes.c_int, vp, sz, sz, vp]
@@ -106,6 +110,13 @@ def _ptr_array(vals):
 
 def himuon_ns_tiled_workspace_size(n_mats: int) -> int:
     return int(lib().himuon_ns_tiled_workspace_size(int(n_mats)))
+
+
+def himuon_ns_tiled_call_workspace_size(rows, cols, T, dtype, compute, K, a, b, c, chunk_budget_bytes=0) -> int:
+    """Workspace bytes of the himuon_ns_tiled call with these arguments (0 if it would be rejected)."""
+    return int(lib().himuon_ns_tiled_call_workspace_size(
+        len(rows), _i64_array(rows), _i64_array(cols), int(T), int(dtype), int(compute), int(K),
+        float(a), float(b), float(c), int(chunk_budget_bytes)))
 
 
 def himuon_ns_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c,
@@ -252,6 +263,17 @@ def himuon_version() -> int:
 
 # ------------------------------------------------------------ tensor wrapper
 
+def _keep_alive(tensors, stream, dev):
+    """Tensors this module allocated for a call enqueued on ``stream``: when
+    that is not torch's current stream, tell the caching allocator that
+    ``stream`` uses them, so that their memory is not handed out again
+    before the enqueued work has finished."""
+    import torch
+    if stream != torch.cuda.current_stream(dev):
+        for t in tensors:
+            t.record_stream(stream)
+
+
 def _dtype_code(t):
     import torch
     if t.dtype == torch.float32:
@@ -278,8 +300,10 @@ def ns_tiled(inputs, outputs=None, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_D
     for x in inputs:
         if x.dim() != 2 or not x.is_cuda or x.device != dev or _dtype_code(x) != code or x.stride(1) != 1:
             raise ValueError("inputs must be 2-D row-major CUDA tensors of one dtype on one device")
+    fresh = []  # tensors allocated here for the call
     if outputs is None:
         outputs = [torch.empty_like(x, memory_format=torch.contiguous_format) for x in inputs]
+        fresh += outputs
     outputs = list(outputs)
     if len(outputs) != len(inputs):
         raise ValueError("inputs and outputs differ in length")
@@ -287,20 +311,25 @@ def ns_tiled(inputs, outputs=None, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_D
         if y.shape != x.shape or y.dtype != x.dtype or y.device != dev or y.stride(1) != 1:
             raise ValueError("each output must match its input's shape, dtype and device")
     n = len(inputs)
-    need = himuon_ns_tiled_workspace_size(n)
+    a, b, c = coeffs
+    rows = [x.shape[0] for x in inputs]
+    cols = [x.shape[1] for x in inputs]
     if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        need = himuon_ns_tiled_call_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
+        # (a call that would be rejected still gets a table-sized workspace, so
+        # that the library reports the precise error)
+        workspace = torch.empty(max(need, himuon_ns_tiled_workspace_size(n)), dtype=torch.uint8, device=dev)
+        fresh.append(workspace)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
-    a, b, c = coeffs
     st = himuon_ns_tiled(
-        n, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs],
-        [x.shape[0] for x in inputs], [x.shape[1] for x in inputs],
+        n, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs], rows, cols,
         [x.stride(0) for x in inputs], [y.stride(0) for y in outputs],
         T, K, a, b, c, code, compute, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
         chunk_budget_bytes, stream.cuda_stream)
     if st != OK:
         raise HimuonError(st, "himuon_ns_tiled")
+    _keep_alive(fresh, stream, dev)
     return outputs
 
 
@@ -320,8 +349,10 @@ def ns_gemm(inputs, outputs=None, T=0, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFA
     for x in inputs:
         if x.dim() != 2 or not x.is_cuda or x.device != dev or _dtype_code(x) != code or x.stride(1) != 1:
             raise ValueError("inputs must be 2-D row-major CUDA tensors of one dtype on one device")
+    fresh = []  # tensors allocated here for the call
     if outputs is None:
         outputs = [torch.empty_like(x, memory_format=torch.contiguous_format) for x in inputs]
+        fresh += outputs
     outputs = list(outputs)
     if len(outputs) != len(inputs):
         raise ValueError("inputs and outputs differ in length")
@@ -338,6 +369,7 @@ def ns_gemm(inputs, outputs=None, T=0, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFA
         raise HimuonError(ERR_INVALID_ARG, "himuon_ns_gemm_hw_workspace_size")
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        fresh.append(workspace)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
     st = himuon_ns_gemm_hw(
@@ -347,6 +379,7 @@ def ns_gemm(inputs, outputs=None, T=0, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFA
         chunk_budget_bytes, stream.cuda_stream)
     if st != OK:
         raise HimuonError(st, "himuon_ns_gemm_hw")
+    _keep_alive(fresh, stream, dev)
     return outputs
 
 
@@ -375,8 +408,10 @@ def step(weights, grads, moms, T=512, K=5, coeffs=QUINTIC, lr=0.02, momentum=0.9
     need = himuon_step_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
     if need == 0:
         raise HimuonError(ERR_INVALID_ARG, "himuon_step_workspace_size")
+    fresh = []
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        fresh.append(workspace)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
     st = himuon_step(
@@ -386,6 +421,7 @@ def step(weights, grads, moms, T=512, K=5, coeffs=QUINTIC, lr=0.02, momentum=0.9
         stream.cuda_stream)
     if st != OK:
         raise HimuonError(st, "himuon_step")
+    _keep_alive(fresh, stream, dev)
     return weights
 
 
@@ -393,7 +429,7 @@ class HiMuon:
     """Optimizer state around ``himuon_step`` (Alg. 1): one momentum buffer per
     matrix (zero at the start, independent of T) and a device workspace
     cached across steps. ``reconfigure(T)`` changes the tile size at run time
-    (Sec. 4.4.4) and keeps the momentum; T = 0 is the full-matrix branch.
+    (Sec. 4.4.3) and keeps the momentum; T = 0 is the full-matrix branch.
     Every step is one library call over all matrices (cross-layer batching,
     Sec. 4.4.2). With ``tune`` (default), a tile size served by the library
     GEMMs has its GEMM kernels chosen by timing at (re)configuration."""

@@ -61,13 +61,21 @@ def _run(cmd, verbose):
         print(msgs)
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, jobs: int = 0) -> str:
+    """Compile every source (in parallel, `jobs` at a time; 0: up to 8) and
+    link the library."""
+    from concurrent.futures import ThreadPoolExecutor
+
     os.makedirs(BUILD_DIR, exist_ok=True)
-    objs = []
+    cmds, objs = [], []
     for src, extra in SOURCES:
         obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-        _run([hipcc()] + COMMON + extra + ["-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        cmds.append([hipcc()] + COMMON + extra + ["-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
+    jobs = jobs or min(8, len(cmds), os.cpu_count() or 1)
+    with ThreadPoolExecutor(max_workers=jobs) as pool:
+        for f in [pool.submit(_run, c, verbose) for c in cmds]:
+            f.result()
     tmp = LIBRARY + ".tmp"
     _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC"] + objs + LINK_LIBS + ["-o", tmp], verbose)
     os.replace(tmp, LIBRARY)

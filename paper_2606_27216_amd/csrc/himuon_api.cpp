@@ -8,6 +8,7 @@
 // balanced to within one tile. The plan is O(#matrices) integer work and is
 // rebuilt on every call, so changing T between calls costs nothing extra.
 #include "himuon_internal.h"
+#include "ns_gemm_path.h"
 #include "../../include/himuon.h"
 
 #include <math.h>
@@ -90,9 +91,10 @@ int resolve_compute(int dtype, int compute, int K, float a, float b, float c)
     const double M2 = M * M;
     const double fp16_ops = fmax(fmax(Mz, MH + bp), fmax(fabs((double)a) + bp * MH + MH * MH, (MH + bp) * Mz));
     const double bound = fmax(fp16_ops, fmax(M2, fabs((double)b) * M2 + fabs((double)c) * M2 * M2));
-    const bool safe = bound < 16384.0;
-    if (compute == HIMUON_COMPUTE_F16) return safe ? HIMUON_COMPUTE_F16 : HIMUON_ERR_RANGE;
-    return safe ? HIMUON_COMPUTE_F16 : HIMUON_COMPUTE_BF16;
+    // DEFAULT never switches to bf16 operands on its own: one-pass bf16
+    // operands miss the 2e-2 bf16-storage bar at T <= 64 and at K = 8, so a
+    // caller who accepts that accuracy asks for HIMUON_COMPUTE_BF16.
+    return bound < 16384.0 ? HIMUON_COMPUTE_F16 : HIMUON_ERR_RANGE;
 }
 
 }  // namespace
@@ -217,6 +219,20 @@ extern "C" {
 
 size_t himuon_ns_tiled_workspace_size(int64_t n_mats) { return himuon::tiled_workspace(n_mats, false); }
 
+size_t himuon_ns_tiled_call_workspace_size(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
+                                           int compute, int K, float a, float b, float c, size_t chunk_budget_bytes)
+{
+    if (n_mats < 1 || !rows || !cols) return 0;
+    if (T != 32 && T != 64 && T != 128 && T != 256) return 0;
+    const int op = resolve_compute(dtype, compute, K, a, b, c);
+    if (op < 0) return 0;
+    for (int64_t m = 0; m < n_mats; ++m)
+        if (rows[m] < 1 || cols[m] < 1) return 0;
+    const himuon::Storage st = dtype == HIMUON_BF16 ? himuon::Storage::BF16 : himuon::Storage::F32;
+    if (himuon::has_kernel(T, st, (himuon::Operand)op)) return himuon::tiled_workspace(n_mats, false);
+    return himuon::gemm_path_workspace(n_mats, rows, cols, T, T, dtype, op, K, a, b, c, chunk_budget_bytes);
+}
+
 int himuon_plan_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
                        size_t chunk_budget_bytes, int64_t* total_tiles, int64_t* n_chunks,
                        int64_t* chunk_bounds, int64_t max_bounds)
@@ -281,7 +297,14 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
     if (op < 0) return op;
     const himuon::Storage st = dtype == HIMUON_BF16 ? himuon::Storage::BF16 : himuon::Storage::F32;
     const himuon::Operand opnd = (himuon::Operand)op;
-    if (!himuon::has_kernel(T, st, opnd)) return HIMUON_ERR_UNSUPPORTED;
+    if (!himuon::has_kernel(T, st, opnd)) {
+        // 256-tiles without a fused kernel (fp32 storage, bf16 operands): each
+        // tile is a 256 x 256 problem of the library-GEMM path, in the same call
+        if (T == 256 && !opt_host)
+            return run_gemm_path(n_mats, in_ptrs, out_ptrs, nullptr, nullptr, rows, cols, ld_in, ld_out, T, T, K, a,
+                                 b, c, dtype, op, workspace, workspace_bytes, chunk_budget_bytes, stream, nullptr);
+        return HIMUON_ERR_UNSUPPORTED;
+    }
     if (opt_host && !has_step_kernel(T, st, opnd, c)) return HIMUON_ERR_UNSUPPORTED;
     if (!workspace || workspace_bytes < tiled_workspace(n_mats, opt_host != nullptr)) return HIMUON_ERR_WORKSPACE;
 

@@ -3,7 +3,7 @@
 //   U = Phi_K(Ghat) when T = 0 (the branch T = infinity) or T >= max(H, W),
 //       else Phi_{K,T}(Ghat);
 //   W <- (1 - lr lambda) W - lr tau U, tau = c sqrt(max(H, W)) on the full
-//       branch and c sqrt(T) when tiled (Sec. 4.3, eq. scaled_update).
+//       branch and c sqrt(T) when tiled (Sec. 4.2, eq. scaled_update).
 // Three execution routes, chosen from T and the types:
 //   - T in {32, 64, 128} (fp32 storage; bf16 storage with bf16 operands; bf16
 //     storage with fp16 operands when c > 0): the step inside the fused tile

@@ -9,11 +9,12 @@
 //     A = X X^T                       (m x m, one GEMM)
 //     B = (c / s^4) A A + (b / s^2) A (one GEMM, C = A)
 //     X <- B X + a X                  (one GEMM, C = X)
-// X is the rescaled iterate s * X_true: s = sqrt(m) for fp16 operands, which
-// keeps X, A = s^2 A_true and B = b A_true + c A_true^2 inside fp16's range
-// for every m up to 32768 when the scalar iterates stay below the bound
-// checked at planning (himuon_select_compute's argument, on |X|, |A| and
-// |B|); s = 1 for fp32 and bf16 operands. Accumulation is fp32 in every
+// X is the rescaled iterate s * X_true: s^2 = min(m, 4096) for fp16 operands,
+// which lifts the O(1/sqrt(mn)) entries of X off fp16's subnormal range and
+// keeps X, A = s^2 A_true and B = b A_true + c A_true^2 inside its range for
+// every m when the scalar iterates stay below the bound checked at planning
+// (himuon_select_compute's argument, on |X|, |A| and |B|); s = 1 for fp32 and
+// bf16 operands. Accumulation is fp32 in every
 // mode. The GEMMs are hipBLASLt's (column-major: a row-major m x n iterate
 // is an n x m column-major matrix, and A and B are symmetric).
 #include "ns_gemm_path.h"
@@ -146,7 +147,15 @@ int plan_chunks(std::vector<Group>& groups, GemmOperand op, size_t budget, size_
     return HIMUON_OK;
 }
 
+// Square of the fp16 iterate scale for an m x n iterate (see the file comment).
+double fp16_scale2(int m) { return (double)std::min(m, 4096); }
+
+// Scale of the iterate in the GEMM buffers for operand type `op`.
+double iterate_scale(GemmOperand op, int m) { return op == GemmOperand::F16 ? sqrt(fp16_scale2(m)) : 1.0; }
+
 // fp16 operands keep s*X, s^2 A and B inside fp16 (see the file comment).
+// DEFAULT takes them when that holds and otherwise fails with
+// HIMUON_ERR_RANGE; bf16 operands are used only when asked for.
 int resolve_operand(int dtype, int compute, int K, float a, float b, float c, int m_max, GemmOperand* op)
 {
     if (dtype == HIMUON_F32) {
@@ -159,15 +168,14 @@ int resolve_operand(int dtype, int compute, int K, float a, float b, float c, in
         *op = GemmOperand::BF16;
         return HIMUON_OK;
     }
-    // |X| <= M, so |s X| <= M sqrt(m), |s^2 A| <= M^2 m and |B| <= |b| M^2 + |c| M^4
+    // |X| <= M, so |s X| <= M s, |s^2 A| <= M^2 s^2 and |B| <= |b| M^2 + |c| M^4
     // (M from the sampled scalar iterates, K + 1 of them: the output is an
     // operand-typed iterate too; 1.25 covers what falls between samples)
     const double M = 1.25 * himuon::iterate_bound(K + 1, a, b, c);
-    const double s2 = (double)m_max;
+    const double s2 = fp16_scale2(m_max);
     const double bound = fmax(M * sqrt(s2), fmax(M * M * s2, fabs((double)b) * M * M + fabs((double)c) * M * M * M * M));
-    const bool safe = bound < 32768.0;
-    if (compute == HIMUON_COMPUTE_F16 && !safe) return HIMUON_ERR_RANGE;
-    *op = safe ? GemmOperand::F16 : GemmOperand::BF16;
+    if (!(bound < 32768.0)) return HIMUON_ERR_RANGE;
+    *op = GemmOperand::F16;
     return HIMUON_OK;
 }
 
@@ -432,7 +440,7 @@ int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_p
         void* X[2] = {bufs, bufs + xb};
         void* A = bufs + 2 * xb;
         void* B = bufs + 2 * xb + ab;
-        const double s = op == GemmOperand::F16 ? sqrt((double)g.m) : 1.0;
+        const double s = iterate_scale(op, g.m);
         const float alpha2 = (float)((double)c / (s * s * s * s)), beta2 = (float)((double)b / (s * s));
         for (int64_t ci = 0; ci < g.n_chunks && status == HIMUON_OK; ++ci) {
             const int64_t p0 = (int64_t)(((__int128)ci * g.count) / g.n_chunks);
@@ -577,7 +585,7 @@ int himuon_gemm_tune_hw(int64_t n_mats, const int64_t* rows, const int64_t* cols
         uint8_t* const X1 = bufs + xb;
         uint8_t* const A = bufs + 2 * xb;
         uint8_t* const B = bufs + 2 * xb + ab;
-        const double s = op == GemmOperand::F16 ? sqrt((double)g.m) : 1.0;
+        const double s = iterate_scale(op, g.m);
         const float alpha2 = (float)((double)c / (s * s * s * s)), beta2 = (float)((double)b / (s * s));
         const int64_t sizes[2] = {ceil_div(g.count, g.n_chunks), g.count / g.n_chunks};
         for (int k = 0; k < 2 && st == HIMUON_OK; ++k) {

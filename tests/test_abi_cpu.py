@@ -41,6 +41,31 @@ def test_workspace_size():
     assert hm.himuon_ns_tiled_workspace_size(224) == 224 * 64
 
 
+def test_call_workspace_size():
+    """A call served by a fused kernel needs the descriptor table only; a
+    256-tile call without a fused kernel (fp32 storage, bf16 operands) needs
+    the library-GEMM path's workspace for T = 256."""
+    a, b, c = hm.QUINTIC
+    rows, cols = [1024, 2048, 300], [4096, 2048, 500]
+    call = lambda T, dtype, compute=hm.COMPUTE_DEFAULT, budget=0, K=5: hm.himuon_ns_tiled_call_workspace_size(
+        rows, cols, T, dtype, compute, K, a, b, c, budget)
+    gemm = lambda T, dtype, compute=hm.COMPUTE_DEFAULT, budget=0: hm.himuon_ns_gemm_workspace_size(
+        rows, cols, T, dtype, compute, 5, a, b, c, budget)
+    for T in (32, 64, 128):
+        for dtype in (hm.F32, hm.BF16):
+            assert call(T, dtype) == hm.himuon_ns_tiled_workspace_size(3)
+        assert call(T, hm.BF16, hm.COMPUTE_BF16) == hm.himuon_ns_tiled_workspace_size(3)
+    assert call(256, hm.BF16) == hm.himuon_ns_tiled_workspace_size(3)  # fused fp16-operand kernel
+    assert call(256, hm.F32) == gemm(256, hm.F32) > (64 << 20)
+    assert call(256, hm.BF16, hm.COMPUTE_BF16) == gemm(256, hm.BF16, hm.COMPUTE_BF16)
+    budget = 4 * (2 * 256 * 256 + 2 * 256 * 256) * 4  # four fp32 256-problems per chunk
+    assert call(256, hm.F32, budget=budget) == gemm(256, hm.F32, budget=budget) < call(256, hm.F32)
+    # rejected calls: no size
+    assert call(48, hm.BF16) == 0 and call(512, hm.BF16) == 0
+    assert call(128, hm.F32, hm.COMPUTE_F16) == 0
+    assert hm.himuon_ns_tiled_call_workspace_size(rows, cols, 128, hm.BF16, hm.COMPUTE_DEFAULT, 5, 50.0, 0.0, 0.0) == 0
+
+
 def _call(**kw):
     args = dict(n_mats=1, in_ptrs=[FAKE], out_ptrs=[FAKE], rows=[64], cols=[64], ld_in=None, ld_out=None,
                 T=32, K=5, a=3.4445, b=-4.775, c=2.0315, dtype=hm.BF16, compute=hm.COMPUTE_DEFAULT,
@@ -69,6 +94,11 @@ def _call(**kw):
     (dict(workspace_bytes=255), hm.ERR_WORKSPACE),
     (dict(chunk_budget_bytes=100), hm.ERR_WORKSPACE),
     (dict(compute=hm.COMPUTE_F16, a=50.0, b=0.0, c=0.0), hm.ERR_RANGE),
+    # DEFAULT never falls back to bf16 operands on its own
+    (dict(a=50.0, b=0.0, c=0.0), hm.ERR_RANGE),
+    # 256-tiles without a fused kernel run on the GEMM path, whose workspace is larger
+    (dict(T=256, dtype=hm.F32), hm.ERR_WORKSPACE),
+    (dict(T=256, compute=hm.COMPUTE_BF16), hm.ERR_WORKSPACE),
     # 2^32 tiles in one call (the kernels number tiles with 32-bit ids)
     (dict(rows=[1 << 37], cols=[32]), hm.ERR_UNSUPPORTED),
 ])
@@ -90,14 +120,17 @@ def test_select_compute():
     assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 5, a, b, c) == hm.COMPUTE_F16
     assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 8, a, b, c) == hm.COMPUTE_F16
     assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_BF16, 5, a, b, c) == hm.COMPUTE_BF16
-    # iterates that grow without bound fall back to bf16 operands by default
-    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 20, 2.0, 0.0, 0.0) == hm.COMPUTE_BF16
+    # iterates that grow without bound cannot use fp16 operands; DEFAULT
+    # reports that instead of switching to bf16 operands on its own
+    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 20, 2.0, 0.0, 0.0) == hm.ERR_RANGE
     assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_F16, 20, 2.0, 0.0, 0.0) == hm.ERR_RANGE
+    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_BF16, 20, 2.0, 0.0, 0.0) == hm.COMPUTE_BF16
+    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 5, 4.0, -6.0, 3.0) == hm.ERR_RANGE
     # the textbook cubic iteration stays bounded
     assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 60, 1.5, -0.5, 0.0) == hm.COMPUTE_F16
     # one step's operator a I + P carries |a| itself: a large a alone must
     # move the call off fp16 operands
-    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 1, 20000.0, 0.0, 0.0) == hm.COMPUTE_BF16
+    assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_DEFAULT, 1, 20000.0, 0.0, 0.0) == hm.ERR_RANGE
     assert hm.himuon_select_compute(hm.BF16, hm.COMPUTE_F16, 1, 20000.0, 0.0, 0.0) == hm.ERR_RANGE
 
 
@@ -107,8 +140,8 @@ def _qwen(model):
 
 
 def test_planner_reproduces_paper_chunking():
-    """Sec. 6.3: at T = 512 the 1680 tiles of Qwen3-0.6B fit one call, the
-    5376 of Qwen3-1.7B split into two chunks of 2688 (the paper gives no
+    """Sec. 6.4, T = 512: Qwen3-0.6B's 1680 tiles take one call, Qwen3-1.7B's
+    5376 take two chunks of 2688 (the paper gives no
     budget; any budget between 2688 and 5375 one-MiB tiles gives this)."""
     ch = GOLD["cross_layer_chunking"]
     budget = 4 << 30  # 4 GiB; a T=512 bf16 tile stands for 2*512*512*2 B = 1 MiB
@@ -175,6 +208,12 @@ def test_gemm_workspace_size():
     assert ws([64], [64], 0, dtype=7) == 0
     assert ws([64], [64], 0, dtype=hm.F32, compute=hm.COMPUTE_F16) == 0
     assert ws([40000], [40000], 0) == 0  # Gram size above 32768
+    # the fp16 iterate scale is capped (s^2 = min(m, 4096)), so any Gram size
+    # up to the limit keeps fp16 operands by default; growing iterates cannot
+    assert ws([20000], [20000], 0) >= 4 * 20000 * 20000 * 2
+    assert ws([64], [64], 0, K=20) > 0
+    assert hm.himuon_ns_gemm_workspace_size([64], [64], 0, hm.BF16, hm.COMPUTE_DEFAULT, 20, 2.0, 0.0, 0.0, 0) == 0
+    assert hm.himuon_ns_gemm_workspace_size([64], [64], 0, hm.BF16, hm.COMPUTE_BF16, 20, 2.0, 0.0, 0.0, 0) > 0
 
 
 def _gcall(**kw):
@@ -196,6 +235,7 @@ def _gcall(**kw):
     (dict(dtype=hm.F32, compute=hm.COMPUTE_BF16), hm.ERR_UNSUPPORTED),
     (dict(rows=[40000], cols=[40000]), hm.ERR_UNSUPPORTED),
     (dict(compute=hm.COMPUTE_F16, a=50.0, b=0.0, c=0.0), hm.ERR_RANGE),
+    (dict(a=50.0, b=0.0, c=0.0), hm.ERR_RANGE),
     (dict(workspace=0), hm.ERR_WORKSPACE),
     (dict(workspace_bytes=1 << 20), hm.ERR_WORKSPACE),
     (dict(T=512, chunk_budget_bytes=100), hm.ERR_WORKSPACE),

@@ -5,6 +5,8 @@ Bars (written here, from the target): per-tile relative Frobenius error
 for properties that hold exactly in any fixed-order arithmetic (batching,
 chunking, tile permutation, repetition, power-of-two scaling, sign).
 """
+import functools
+
 import numpy as np
 import pytest
 import torch
@@ -12,7 +14,7 @@ import torch
 import oracle
 import paper_2606_27216_amd as hm
 import workloads
-from parity import COEF32, TOL, sampled_tile_errors, tile_errors, to_f64
+from parity import BF16_OPERAND_BAR, COEF32, TOL, sampled_tile_errors, tile_errors, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -30,9 +32,9 @@ def run(mats, T, K=5, coeffs=COEF32, compute=hm.COMPUTE_DEFAULT, budget=0, outpu
 
 
 def tile_sizes(dtype):
-    """Tile sizes with a kernel for this storage type: T = 256 exists for bf16
-    storage (fp16 operands) only."""
-    return (32, 64, 128, 256) if dtype == "bf16" else (32, 64, 128)
+    """Every tile size himuon_ns_tiled serves (for fp32 storage, T = 256 runs
+    each tile as a problem of the library-GEMM path inside the same call)."""
+    return (32, 64, 128, 256)
 
 
 def check_full(x, y, T, K=5, coeffs=COEF32, tol=None):
@@ -65,11 +67,56 @@ def test_config2_bf16(T):
 
 
 def test_config2_bf16_operands_T128():
-    """bf16 MFMA operands (instead of the default fp16) at T=128, K=5."""
+    """bf16 MFMA operands (instead of the default fp16) at T=128, K=5: the
+    one bf16-operand case inside the 2e-2 target."""
     announce("4096x4096 bf16, compute=BF16, T=128")
     x = workloads.lowrank_plus_noise(4096, 4096, 2, "bf16", DEV)
     (y,) = run([x], 128, compute=hm.COMPUTE_BF16)
     check_full(x, y, 128)
+
+
+@pytest.mark.parametrize("T", [32, 64, 128, 256])
+@pytest.mark.parametrize("K", [5, 8])
+def test_bf16_operands_config2_and_config5(T, K):
+    """The opt-in bf16-operand mode (HIMUON_COMPUTE_BF16) on config 2's
+    low-rank-plus-noise matrix and config 5's heavy-tailed shapes, on sampled
+    tiles, against the bar of its own format (BF16_OPERAND_BAR, which is above
+    the 2e-2 default-path bar; the default never selects this mode)."""
+    rng = np.random.default_rng(T * 10 + K)
+    cases = _bf16_operand_cases()
+    worst = 0.0
+    for name, x in cases:
+        announce(f"bf16 operands {name} {tuple(x.shape)} T={T} K={K}")
+        (y,) = run([x], T, K=K, compute=hm.COMPUTE_BF16)
+        S = to_f64(x)
+        n = oracle.tile_count(*S.shape, T)
+        ids = np.sort(rng.choice(n, min(n, 24 if T < 256 else 8), replace=False))
+        ref = oracle.ns_tiles(S, T, K, *COEF32, ids)
+        e = sampled_tile_errors(to_f64(y), ref, ids, T)
+        assert np.all(np.isfinite(e))
+        print(f"[gpu-err] bf16 operands {name} T={T} K={K}: max {e.max():.3e} p50 {np.median(e):.3e}", flush=True)
+        worst = max(worst, e.max())
+    assert worst <= BF16_OPERAND_BAR, worst
+
+
+@functools.lru_cache(maxsize=1)
+def _bf16_operand_cases():
+    cases = [("config 2", workloads.lowrank_plus_noise(4096, 4096, 2, "bf16", DEV))]
+    het = workloads.heterogeneous("bf16", DEV)
+    return cases + [(f"config 5 matrix {i}", het[i]) for i in (0, 9, 17)]
+
+
+def test_default_never_selects_bf16_operands():
+    """Coefficients whose iterates leave the fp16 range: DEFAULT reports
+    HIMUON_ERR_RANGE instead of switching to bf16 operands; asking for them
+    runs."""
+    coeffs = (4.0, -6.0, 3.0)
+    x = workloads.gaussian(256, 256, 15, "bf16", DEV)
+    with pytest.raises(hm.HimuonError) as err:
+        run([x], 128, K=5, coeffs=coeffs)
+    assert err.value.status == hm.ERR_RANGE
+    (y,) = run([x], 128, K=1, coeffs=coeffs, compute=hm.COMPUTE_BF16)
+    assert torch.isfinite(y.float()).all()
 
 
 def test_config3_one_layer_sampled():
@@ -93,9 +140,9 @@ def test_config5_heterogeneous_schedule(dtype, K):
     """24 heavy-tailed matrices, the runtime tile schedule over successive calls."""
     mats = workloads.heterogeneous(dtype, DEV)
     rng = np.random.default_rng(5)
-    # the schedule T = 256 -> 128 -> 64; fp32 storage has no T = 256 kernel
-    # and runs 128 -> 64 -> 32
-    for T in ((256, 128, 64) if dtype == "bf16" else (128, 64, 32)):
+    # the schedule T = 256 -> 128 -> 64 for both storage types (fp32 at T = 256
+    # runs its tiles on the library-GEMM path inside the same call)
+    for T in (256, 128, 64):
         announce(f"heterogeneous batch {dtype} K={K} T={T}")
         outs = run(mats, T, K=K)
         for i in (0, 9, 17):  # one matrix of each shape
@@ -108,7 +155,7 @@ def test_config5_heterogeneous_schedule(dtype, K):
             assert e.max() <= TOL[mats[i].dtype], (T, i, e.max())
 
 
-@pytest.mark.parametrize("T", [128, 64, 32])
+@pytest.mark.parametrize("T", [256, 128, 64, 32])
 def test_config5_fp32_K8_every_tile(T):
     """Every tile of one heavy-tailed 2048x2048 fp32 matrix at K=8, where
     ill-conditioned tiles amplify fp32 rounding the most."""
@@ -141,13 +188,12 @@ def test_single_padded_tile_is_full_map(dtype):
     ref = oracle.phi_k(to_f64(x), 5, *COEF32)
     e = np.linalg.norm(to_f64(y) - ref) / np.linalg.norm(ref)
     assert e <= TOL[x.dtype]
-    if dtype == "bf16":
-        x = workloads.gaussian(200, 256, 12, dtype, DEV)
-        (y,) = run([x], 256)
-        ref = oracle.phi_k(to_f64(x), 5, *COEF32)
-        e = np.linalg.norm(to_f64(y) - ref) / np.linalg.norm(ref)
-        print(f"[gpu-err] 200x256 as one 256-tile: {e:.3e}", flush=True)
-        assert e <= TOL[x.dtype]
+    x = workloads.gaussian(200, 256, 12, dtype, DEV)
+    (y,) = run([x], 256)
+    ref = oracle.phi_k(to_f64(x), 5, *COEF32)
+    e = np.linalg.norm(to_f64(y) - ref) / np.linalg.norm(ref)
+    print(f"[gpu-err] 200x256 as one 256-tile: {e:.3e}", flush=True)
+    assert e <= TOL[x.dtype]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -183,11 +229,18 @@ def test_other_coefficients_bf16(coeffs):
         check_full(x, y, T, K=6, coeffs=coeffs)
 
 
-def test_fp32_storage_has_no_256_kernel():
-    x = workloads.gaussian(256, 256, 14, "f32", DEV)
+def test_fp32_storage_256_tiles_through_the_call():
+    """fp32 storage at T = 256: himuon_ns_tiled serves the call (on the
+    library-GEMM path), with the call's own workspace size; the table-sized
+    workspace of the fused kernels is rejected before anything runs."""
+    announce("fp32 T=256 through himuon_ns_tiled")
+    x = workloads.gaussian(300, 520, 14, "f32", DEV)
+    (y,) = run([x], 256)
+    check_full(x, y, 256)
+    ws = torch.empty(hm.himuon_ns_tiled_workspace_size(1), dtype=torch.uint8, device=DEV)
     with pytest.raises(hm.HimuonError) as err:
-        run([x], 256)
-    assert err.value.status == hm.ERR_UNSUPPORTED
+        hm.ns_tiled([x], T=256, K=5, coeffs=COEF32, workspace=ws)
+    assert err.value.status == hm.ERR_WORKSPACE
 
 
 @pytest.mark.parametrize("dtype,T", [("f32", 64), ("bf16", 64), ("bf16", 256)])
@@ -224,6 +277,28 @@ def test_in_place_and_strided(dtype):
     run([x], 64, outputs=[x])  # in place on the strided view
     assert torch.equal(x, y)
     assert torch.equal(big[:, :10], workloads.gaussian(200, 300, 11, dtype, DEV)[:, :10])
+
+
+@pytest.mark.parametrize("dtype,T", [("bf16", 128), ("bf16", 256), ("f32", 128), ("f32", 256)])
+def test_in_place_equals_out_of_place(dtype, T):
+    """out == in at the tile sizes whose kernels overlap tiles: the 128-tile
+    fp16 kernel issues the loads of a wave's next tile before the stores of
+    its previous one, the 256-tile kernel keeps one tile per CU, and fp32 at
+    T = 256 runs on the GEMM path. In place must equal out of place bit for
+    bit, over several chunks and a ragged edge."""
+    announce(f"in place {dtype} T={T}")
+    mats = [workloads.student_t(5 * T + 17, 3 * T + 40, 90 + i, dtype, DEV) for i in range(3)]
+    elem = 4 if dtype == "f32" else 2
+    if dtype == "f32" and T == 256:  # the GEMM path's budget: X, X', A, B of 7 problems
+        budget = 7 * 4 * T * T * elem
+    else:  # 7 tiles per chunk
+        budget = 7 * 2 * T * T * elem
+    ref = run(mats, T, budget=budget)
+    inplace = [m.clone() for m in mats]
+    run(inplace, T, budget=budget, outputs=inplace)
+    for a, b in zip(ref, inplace):
+        assert torch.equal(a, b)
+    check_full(mats[0], ref[0], T)
 
 
 # ---------------------------------------------------------- exact properties

@@ -43,7 +43,7 @@ LAYER_7B = (
 HETERO_SHAPES = tuple([(1024, 4096)] * 8 + [(4096, 1024)] * 8 + [(2048, 2048)] * 8)
 
 # The seven Muon-eligible matrices of one transformer block of each Qwen3
-# model, output x input (Sec. 6.2, Tab. qwen3_shapes), for the per-layer
+# model, output x input (Sec. 6.3, Tab. qwen3_shapes), for the per-layer
 # tiled/full comparison; the inputs themselves are random Gaussian.
 QWEN3_BLOCK0 = {
     "0.6B": (("q_proj", 2048, 1024), ("k_proj", 1024, 1024), ("v_proj", 1024, 1024), ("o_proj", 1024, 2048),

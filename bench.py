@@ -128,12 +128,15 @@ def cpu_baseline(mats, outs, T, K, coeffs, budget_s, seed=0):
     errs = []
 
     def sample(seconds, batch):
+        # each round: up to `batch` random tiles of one random row of tiles,
+        # so that one oracle call spreads them over its threads
         done, elapsed = 0, 0.0
         while elapsed < seconds:
             i = int(rng.integers(len(mats)))
             x, y = mats[i], outs[i]
-            ids = np.sort(rng.choice(counts[i], batch, replace=False))
             C = -(-x.shape[1] // T)
+            r0 = int(rng.integers(counts[i] // C))
+            ids = r0 * C + np.sort(rng.choice(C, min(batch, C), replace=False))
             # read back only the rows of tiles those ids touch
             rows = sorted({int(t) // C for t in ids})
             sub = {r: x[r * T:(r + 1) * T].float().cpu().double().numpy() for r in rows}
@@ -144,7 +147,7 @@ def cpu_baseline(mats, outs, T, K, coeffs, budget_s, seed=0):
                 loc = [int(t) % C for t in ids if int(t) // C == r]
                 refs[r] = (loc, oracle.ns_tiles(sub[r], T, K, *coeffs, loc))
             elapsed += time.perf_counter() - t0
-            done += batch
+            done += len(ids)
             for r, (loc, ref) in refs.items():
                 for c, tile in zip(loc, ref):
                     g = got[r][:, c * T:(c + 1) * T]
@@ -154,7 +157,7 @@ def cpu_baseline(mats, outs, T, K, coeffs, budget_s, seed=0):
         return done, elapsed
 
     cores = oracle.num_threads()
-    done, elapsed = sample(budget_s, 16)
+    done, elapsed = sample(budget_s, 2 * cores)
     flops = 6.0 * T ** 3 * K
     oracle.set_num_threads(1)
     try:

@@ -22,8 +22,6 @@ using himuon::MatDesc;
 
 constexpr int kVersion = 100;  // 0.1.0
 
-int hip_fail(hipError_t e) { return himuon::set_hip_error(e); }
-
 size_t elem_size(int dtype) { return dtype == HIMUON_BF16 ? 2 : 4; }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -143,16 +141,13 @@ double iterate_bound_uncached(int K, double a, double b, double c)
 {
     constexpr int kPts = 8193;
     double m = 1.0;
-    std::vector<double> s(kPts);
-    for (int i = 0; i < kPts; ++i) s[i] = (double)i / (kPts - 1);
-    for (int k = 1; k < K; ++k) {
-        for (int i = 0; i < kPts; ++i) {
-            const double x = s[i];
-            const double y = a * x + b * x * x * x + c * x * x * x * x * x;
-            s[i] = y;
-            const double ay = fabs(y);
-            if (!(ay < 1e30)) return INFINITY;
-            if (ay > m) m = ay;
+    for (int i = 0; i < kPts; ++i) {
+        double x = (double)i / (kPts - 1);
+        for (int k = 1; k < K; ++k) {
+            x = a * x + b * x * x * x + c * x * x * x * x * x;
+            const double ax = fabs(x);
+            if (!(ax < 1e30)) return INFINITY;
+            if (ax > m) m = ax;
         }
     }
     return m;
@@ -275,12 +270,10 @@ bool has_step_kernel(int T, Storage st, Operand op, float c)
     return has_kernel(T, st, op);                                   // fp32 storage, bf16 operands
 }
 
-int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
-              const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
-              float c, int dtype, int compute, void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
-              void* stream, const OptDesc* opt_host, float beta, float decay, float lr, int nesterov)
+int validate_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+                   const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
+                   float c, int dtype, int compute, int* op)
 {
-    // ---- validation: nothing is enqueued unless every check passes
     if (n_mats < 1 || n_mats > INT32_MAX || !in_ptrs || !out_ptrs || !rows || !cols) return HIMUON_ERR_INVALID_ARG;
     if (K < 0 || !finite3(a, b, c)) return HIMUON_ERR_INVALID_ARG;
     if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
@@ -292,12 +285,115 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
         const int64_t lo = ld_out ? ld_out[m] : cols[m];
         if (li < cols[m] || lo < cols[m]) return HIMUON_ERR_INVALID_ARG;
         if (rows[m] > INT64_MAX / li || rows[m] > INT64_MAX / lo) return HIMUON_ERR_INVALID_ARG;
+        if (ceil_div(cols[m], T) > INT32_MAX) return HIMUON_ERR_INVALID_ARG;
     }
-    const int op = resolve_compute(dtype, compute, K, a, b, c);
-    if (op < 0) return op;
-    const himuon::Storage st = dtype == HIMUON_BF16 ? himuon::Storage::BF16 : himuon::Storage::F32;
-    const himuon::Operand opnd = (himuon::Operand)op;
-    if (!himuon::has_kernel(T, st, opnd)) {
+    const int r = resolve_compute(dtype, compute, K, a, b, c);
+    if (r < 0) return r;
+    *op = r;
+    return HIMUON_OK;
+}
+
+int plan_tiled_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
+                      size_t chunk_budget_bytes, int64_t* total, int64_t* n_chunks)
+{
+    int s = plan_tiles(n_mats, rows, cols, T, nullptr, total);
+    if (s != HIMUON_OK) return s;
+    s = plan_chunk_count(*total, T, elem_size(dtype), chunk_budget_bytes, n_chunks);
+    if (s != HIMUON_OK) return s;
+    // the kernels number the tiles of a call with 32-bit ids
+    if (*total > (int64_t)UINT32_MAX) return HIMUON_ERR_UNSUPPORTED;
+    return HIMUON_OK;
+}
+
+MatDesc make_desc(const void* in, void* out, int64_t rows, int64_t cols, int64_t ld_in, int64_t ld_out,
+                  int64_t tile_begin, int T, int dtype, const void* mom)
+{
+    // 16-byte accesses at every column multiple of 8 (bf16) or 4 (f32)
+    const size_t align = 16;
+    const int64_t ld_mult = dtype == HIMUON_BF16 ? 8 : 4;
+    MatDesc d;
+    d.in = in;
+    d.out = out;
+    d.rows = rows;
+    d.cols = cols;
+    d.ld_in = ld_in;
+    d.ld_out = ld_out;
+    d.tile_begin = tile_begin;
+    d.tiles_c = (int32_t)ceil_div(cols, T);
+    d.flags = 0;
+    // (a step's momentum shares the gradient's layout and alignment flag)
+    if ((uintptr_t)in % align == 0 && ld_in % ld_mult == 0 && (!mom || (uintptr_t)mom % align == 0))
+        d.flags |= MAT_VEC_IN;
+    if ((uintptr_t)out % align == 0 && ld_out % ld_mult == 0) d.flags |= MAT_VEC_OUT;
+    return d;
+}
+
+KernelArgs make_kernel_args(const MatDesc* descs, int64_t n_mats, int K, float a, float b, float c)
+{
+    KernelArgs ka{};
+    ka.descs = descs;
+    ka.odescs = nullptr;
+    ka.beta = 0.f;
+    ka.decay = 1.f;
+    ka.lr = 0.f;
+    ka.nesterov = 0;
+    ka.n_mats = (int32_t)n_mats;
+    ka.K = K;
+    ka.a = a;
+    ka.b = b;
+    ka.c = c;
+    ka.b_over_c = c != 0.f ? b / c : 0.f;
+    if (c != 0.f) {
+        const double ac = fabs((double)c);
+        ka.zscale = (float)pow(ac, 0.25);
+        ka.unscale = (float)(1.0 / pow(ac, 0.25));
+        ka.sigma = c > 0.f ? 1.f : -1.f;
+        ka.bq = (float)((double)ka.sigma * (double)b / sqrt(ac));
+    } else {
+        ka.zscale = 1.f;
+        ka.unscale = 1.f;
+        ka.sigma = 0.f;
+        ka.bq = b;
+    }
+    return ka;
+}
+
+int launch_chunks(int T, Storage st, Operand op, KernelArgs ka, int64_t total, int64_t n_chunks, hipStream_t stream)
+{
+    for (int64_t i = 0; i < n_chunks; ++i) {
+        ka.tile_begin = chunk_bound(i, total, n_chunks);
+        ka.tile_end = chunk_bound(i + 1, total, n_chunks);
+        const hipError_t e = launch_ns_tiled(T, st, op, ka, stream);
+        if (e != hipSuccess) return set_hip_error(e);
+    }
+    return HIMUON_OK;
+}
+
+int stream_device(hipStream_t stream, int* cur, int* dev)
+{
+    hipError_t e = hipGetDevice(cur);
+    if (e != hipSuccess) return set_hip_error(e);
+    *dev = *cur;
+    if (stream) {
+        e = hipStreamGetDevice(stream, dev);
+        if (e != hipSuccess) return set_hip_error(e);
+    }
+    if (*dev != *cur && (e = hipSetDevice(*dev)) != hipSuccess) return set_hip_error(e);
+    return HIMUON_OK;
+}
+
+int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+              const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
+              float c, int dtype, int compute, void* workspace, size_t workspace_bytes, size_t chunk_budget_bytes,
+              void* stream, const OptDesc* opt_host, float beta, float decay, float lr, int nesterov)
+{
+    // ---- validation: nothing is enqueued unless every check passes
+    int op = 0;
+    int s = validate_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c, dtype, compute, &op);
+    if (s != HIMUON_OK) return s;
+    const Storage st = dtype == HIMUON_BF16 ? Storage::BF16 : Storage::F32;
+    const Operand opnd = (Operand)op;
+    if (!has_kernel(T, st, opnd)) {
         // 256-tiles without a fused kernel (fp32 storage, bf16 operands): each
         // tile is a 256 x 256 problem of the library-GEMM path, in the same call
         if (T == 256 && !opt_host)
@@ -307,89 +403,38 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
     }
     if (opt_host && !has_step_kernel(T, st, opnd, c)) return HIMUON_ERR_UNSUPPORTED;
     if (!workspace || workspace_bytes < tiled_workspace(n_mats, opt_host != nullptr)) return HIMUON_ERR_WORKSPACE;
-
-    std::vector<int64_t> begin;
     int64_t total = 0, n_chunks = 0;
-    int s = plan_tiles(n_mats, rows, cols, T, &begin, &total);
+    s = plan_tiled_chunks(n_mats, rows, cols, T, dtype, chunk_budget_bytes, &total, &n_chunks);
     if (s != HIMUON_OK) return s;
-    s = plan_chunk_count(total, T, elem_size(dtype), chunk_budget_bytes, &n_chunks);
-    if (s != HIMUON_OK) return s;
-    // the kernels number the tiles of a call with 32-bit ids
-    if (total > (int64_t)UINT32_MAX) return HIMUON_ERR_UNSUPPORTED;
 
     // ---- descriptor table
-    // 16-byte accesses at every column multiple of 8 (bf16) or 4 (f32)
-    const size_t align = 16;
-    const int64_t ld_mult = dtype == HIMUON_BF16 ? 8 : 4;
     std::vector<MatDesc> descs((size_t)n_mats);
+    int64_t next = 0;
     for (int64_t m = 0; m < n_mats; ++m) {
-        MatDesc& d = descs[(size_t)m];
-        d.in = in_ptrs[m];
-        d.out = out_ptrs[m];
-        d.rows = rows[m];
-        d.cols = cols[m];
-        d.ld_in = ld_in ? ld_in[m] : cols[m];
-        d.ld_out = ld_out ? ld_out[m] : cols[m];
-        d.tile_begin = begin[(size_t)m];
-        d.tiles_c = (int32_t)ceil_div(cols[m], T);
-        d.flags = 0;
-        // (a step's momentum shares the gradient's layout and alignment flag)
-        if ((uintptr_t)d.in % align == 0 && d.ld_in % ld_mult == 0 &&
-            (!opt_host || (uintptr_t)opt_host[m].mom % align == 0))
-            d.flags |= himuon::MAT_VEC_IN;
-        if ((uintptr_t)d.out % align == 0 && d.ld_out % ld_mult == 0) d.flags |= himuon::MAT_VEC_OUT;
-        if (ceil_div(cols[m], T) > INT32_MAX) return HIMUON_ERR_INVALID_ARG;
+        descs[(size_t)m] = make_desc(in_ptrs[m], out_ptrs[m], rows[m], cols[m], ld_in ? ld_in[m] : cols[m],
+                                     ld_out ? ld_out[m] : cols[m], next, T, dtype,
+                                     opt_host ? opt_host[m].mom : nullptr);
+        next += ceil_div(rows[m], T) * ceil_div(cols[m], T);
     }
 
     // ---- run on the stream's device
     hipStream_t hs = static_cast<hipStream_t>(stream);
     int cur = 0, dev = 0;
-    hipError_t e = hipGetDevice(&cur);
-    if (e != hipSuccess) return hip_fail(e);
-    dev = cur;
-    if (hs) {
-        e = hipStreamGetDevice(hs, &dev);
-        if (e != hipSuccess) return hip_fail(e);
-    }
-    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e);
-
+    s = stream_device(hs, &cur, &dev);
+    if (s != HIMUON_OK) return s;
     const size_t dbytes = ((size_t)n_mats * sizeof(MatDesc) + 255) / 256 * 256;
     OptDesc* const otab = opt_host ? reinterpret_cast<OptDesc*>(static_cast<uint8_t*>(workspace) + dbytes) : nullptr;
-    int status = himuon::upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
+    int status = upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
     if (status == HIMUON_OK && opt_host)
-        status = himuon::upload_table(opt_host, (size_t)n_mats * sizeof(OptDesc), otab, hs, dev);
+        status = upload_table(opt_host, (size_t)n_mats * sizeof(OptDesc), otab, hs, dev);
     if (status == HIMUON_OK) {
-        himuon::KernelArgs ka;
-        ka.descs = static_cast<const MatDesc*>(workspace);
+        KernelArgs ka = make_kernel_args(static_cast<const MatDesc*>(workspace), n_mats, K, a, b, c);
         ka.odescs = otab;
         ka.beta = beta;
         ka.decay = decay;
         ka.lr = lr;
         ka.nesterov = nesterov;
-        ka.n_mats = (int32_t)n_mats;
-        ka.K = K;
-        ka.a = a;
-        ka.b = b;
-        ka.c = c;
-        ka.b_over_c = c != 0.f ? b / c : 0.f;
-        if (c != 0.f) {
-            const double ac = fabs((double)c);
-            ka.zscale = (float)pow(ac, 0.25);
-            ka.unscale = (float)(1.0 / pow(ac, 0.25));
-            ka.sigma = c > 0.f ? 1.f : -1.f;
-            ka.bq = (float)((double)ka.sigma * (double)b / sqrt(ac));
-        } else {
-            ka.zscale = 1.f;
-            ka.unscale = 1.f;
-            ka.sigma = 0.f;
-            ka.bq = b;
-        }
-        for (int64_t i = 0; i < n_chunks && status == HIMUON_OK; ++i) {
-            ka.tile_begin = chunk_bound(i, total, n_chunks);
-            ka.tile_end = chunk_bound(i + 1, total, n_chunks);
-            e = himuon::launch_ns_tiled(T, st, opnd, ka, hs);
-            if (e != hipSuccess) status = hip_fail(e);
-        }
+        status = launch_chunks(T, st, opnd, ka, total, n_chunks, hs);
     }
     if (dev != cur) (void)hipSetDevice(cur);
     return status;

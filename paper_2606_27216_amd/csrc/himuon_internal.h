@@ -85,6 +85,25 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
 // Workspace of run_tiled: the MatDesc table, and the OptDesc table for a step.
 size_t tiled_workspace(int64_t n_mats, bool step);
 
+// The pieces of run_tiled, shared with the entry point that allocates
+// nothing. validate_tiled checks every argument of a himuon_ns_tiled call
+// (no HIP call) and resolves its operand type into *op; plan_tiled_chunks
+// gives the call's tile and chunk counts; make_desc builds one matrix's
+// descriptor (tile_begin: its first global tile id; mom: the step's momentum
+// pointer or null); make_kernel_args sets the scalars of a launch;
+// launch_chunks enqueues one launch per chunk; stream_device makes the
+// stream's device current (*cur: the previous one, to restore).
+int validate_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+                   const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
+                   float c, int dtype, int compute, int* op);
+int plan_tiled_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
+                      size_t chunk_budget_bytes, int64_t* total, int64_t* n_chunks);
+MatDesc make_desc(const void* in, void* out, int64_t rows, int64_t cols, int64_t ld_in, int64_t ld_out,
+                  int64_t tile_begin, int T, int dtype, const void* mom);
+KernelArgs make_kernel_args(const MatDesc* descs, int64_t n_mats, int K, float a, float b, float c);
+int launch_chunks(int T, Storage st, Operand op, KernelArgs ka, int64_t total, int64_t n_chunks, hipStream_t stream);
+int stream_device(hipStream_t stream, int* cur, int* dev);
+
 // The fp16-operand kernel family (bf16 storage), T in {32, 64, 128, 256}.
 hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream);
 

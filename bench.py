@@ -242,6 +242,53 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
     print(json.dumps(rec), flush=True)
 
 
+def bench_rect(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, stream, op_name):
+    """The fused rectangular-tile kernels (himuon_ns_tiled_hw): T x Tw tiles,
+    work counted as the GEMM path's rectangular tiles, (4 m^2 n + 2 m^3) K
+    per tile with m = min, n = max of the tile sides (padding included, as
+    the tiles run)."""
+    Th, Tw = args.T, args.Tw
+    m, n = min(Th, Tw), max(Th, Tw)
+    tiles = sum(-(-h // Th) * -(-w // Tw) for h, w in ((x.shape[0], x.shape[1]) for x in mats))
+    flops_step = tiles * (4.0 * m * m * n + 2.0 * m ** 3) * args.K
+    ws = torch.empty(hm.himuon_ns_tiled_workspace_size(len(mats)), dtype=torch.uint8, device=mats[0].device)
+
+    def step():
+        hm.ns_tiled(mats, outputs=outs, T=Th, Tw=Tw, K=args.K, coeffs=coeffs, compute=compute,
+                    chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    peak = PEAK_TFLOPS[op_name]
+    achieved = flops_step / (float(np.mean(step_ms)) * 1e-3) / 1e12
+    rec = {
+        "metric": "tiled-NS TFLOP/s ((4m^2n + 2m^3)K per tile), 7B layer stack %dx%d tiles K=%d (fused kernel)"
+                  % (Th, Tw, args.K),
+        "value": round(flops_step / (wall / args.steps) / 1e12, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": op_name, "data": "synthetic",
+        "config": {"workload": desc, "path": "tiled_hw", "T": Th, "Tw": Tw, "K": args.K, "matrices": len(mats),
+                   "tiles": tiles, "storage": args.dtype, "mfma_operands": op_name, "accumulate": "f32",
+                   "chunk_budget_bytes": int(args.budget)},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None, "flops_per_step": flops_step,
+                     "mean_step_ms": round(float(np.mean(step_ms)), 4)},
+        "step_ms": {"median": round(float(np.median(step_ms)), 4),
+                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4)},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def bench_optstep(args, hm, torch, np, dev):
     """The optimizer-step benchmark of Sec. 6.4 (cross-layer batching): 8
     stacked bias-free Linear(H, H) layers in bf16, fresh Gaussian gradients
@@ -385,7 +432,8 @@ def main():
     ap.add_argument("--T", type=int, default=128)
     ap.add_argument("--K", type=int, default=5)
     ap.add_argument("--Tw", type=int, default=None,
-                    help="--path gemm: tile width (tiles are T x Tw; default square)")
+                    help="tile width (tiles are T x Tw; default square): the fused rectangular kernels "
+                         "(--path tiled) or the library GEMMs (--path gemm)")
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--compute", default="default", choices=["default", "f16", "bf16", "f32"])
     ap.add_argument("--budget", type=float, default=16e9, help="chunk budget in bytes (0: one chunk)")
@@ -453,6 +501,8 @@ def main():
     stream = torch.cuda.current_stream(dev)
     if args.path == "gemm":
         return bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, stream)
+    if args.Tw is not None and args.Tw != args.T:
+        return bench_rect(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, stream, op_name)
     total, bounds = hm.himuon_plan_chunks(rows, cols, args.T, code, int(args.budget))
     launches = len(bounds) - 1
     flops_step = sum(6.0 * h * w * args.T * args.K for h, w in zip(rows, cols))

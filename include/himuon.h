@@ -146,6 +146,33 @@ int himuon_ns_tiled(int64_t n_mats,
                     void* stream);
 
 /*
+ * himuon_ns_tiled with rectangular Th x Tw tiles in the fused kernels: each
+ * matrix is padded to (R Th) x (C Tw), R = ceil(H/Th), C = ceil(W/Tw), every
+ * tile goes through Phi_K on chip (one workgroup per tile, all K steps), and
+ * a tile with Th > Tw is iterated as its transpose (the orientation rule of
+ * Sec. 2.2, Phi_K(S) = Phi_K(S^T)^T), so the Gram matrix is the min(Th, Tw)
+ * square one. This is the fused-kernel region of the tile-shape study
+ * (Sec. 6.3, Th Tw <= 16384). Served shapes: {min(Th, Tw), max(Th, Tw)} in
+ * {32} x {64, 128, 256} for fp32 storage (fp32 operands) and bf16 storage
+ * (fp16 or bf16 operands), and {32} x {512}, {64} x {128, 256} for bf16
+ * storage; both orientations of each;
+ * Th = Tw is himuon_ns_tiled with T = Th. Other shapes return
+ * HIMUON_ERR_UNSUPPORTED (himuon_ns_gemm_hw serves any shape on library
+ * GEMMs). Arguments, workspace (himuon_ns_tiled_workspace_size(n_mats)),
+ * chunk budget (2 Th Tw sizeof(dtype) bytes per tile), aliasing and errors as
+ * himuon_ns_tiled.
+ */
+int himuon_ns_tiled_hw(int64_t n_mats,
+                       const void* const* in_ptrs, void* const* out_ptrs,
+                       const int64_t* rows, const int64_t* cols,
+                       const int64_t* ld_in, const int64_t* ld_out,
+                       int Th, int Tw, int K, float a, float b, float c,
+                       int dtype, int compute,
+                       void* workspace, size_t workspace_bytes,
+                       size_t chunk_budget_bytes,
+                       void* stream);
+
+/*
  * Phi_K through library GEMMs: the full-matrix branch and large tiles.
  *
  * T = 0: Phi_K of every whole matrix (the full-matrix branch, Sec. 4.4.3).

@@ -57,6 +57,10 @@ def lib():
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                       ctypes.c_int, ctypes.c_int, vp, sz, sz, vp]
         L.himuon_ns_tiled.restype = ctypes.c_int
+        L.himuon_ns_tiled_hw.argtypes = [i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                         ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int, ctypes.c_int,
+                                         vp, sz, sz, vp]
+        L.himuon_ns_tiled_hw.restype = ctypes.c_int
         L.himuon_ns_gemm_workspace_size.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                                     ctypes.c_int, ctypes.c_float, ctypes.c_float,
                                                     ctypes.c_float, sz]
@@ -128,6 +132,17 @@ def himuon_ns_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, 
         int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
         None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
         int(T), int(K), float(a), float(b), float(c), int(dtype), int(compute),
+        int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes),
+        int(stream) if stream else None))
+
+
+def himuon_ns_tiled_hw(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, Th, Tw, K, a, b, c,
+                       dtype, compute, workspace, workspace_bytes, chunk_budget_bytes, stream) -> int:
+    """Same arguments as the C function (see himuon_ns_tiled). Returns the status code."""
+    return int(lib().himuon_ns_tiled_hw(
+        int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
+        None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
+        int(Th), int(Tw), int(K), float(a), float(b), float(c), int(dtype), int(compute),
         int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes),
         int(stream) if stream else None))
 
@@ -284,8 +299,9 @@ def _dtype_code(t):
 
 
 def ns_tiled(inputs, outputs=None, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT,
-             chunk_budget_bytes=0, workspace=None, stream=None):
-    """Φ_{K,T} of every 2-D CUDA tensor in ``inputs`` in one library call.
+             chunk_budget_bytes=0, workspace=None, stream=None, Tw=None):
+    """Φ_{K,T} of every 2-D CUDA tensor in ``inputs`` in one library call
+    (with ``Tw``: rectangular T x Tw tiles, himuon_ns_tiled_hw).
 
     ``outputs`` defaults to fresh tensors; passing ``outputs=inputs`` runs in
     place. Rows may be strided (``stride(1) == 1`` is required). The call is
@@ -315,20 +331,23 @@ def ns_tiled(inputs, outputs=None, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_D
     rows = [x.shape[0] for x in inputs]
     cols = [x.shape[1] for x in inputs]
     if workspace is None:
-        need = himuon_ns_tiled_call_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
+        need = 0 if Tw is not None and Tw != T else \
+            himuon_ns_tiled_call_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
         # (a call that would be rejected still gets a table-sized workspace, so
         # that the library reports the precise error)
         workspace = torch.empty(max(need, himuon_ns_tiled_workspace_size(n)), dtype=torch.uint8, device=dev)
         fresh.append(workspace)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
-    st = himuon_ns_tiled(
-        n, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs], rows, cols,
-        [x.stride(0) for x in inputs], [y.stride(0) for y in outputs],
-        T, K, a, b, c, code, compute, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
-        chunk_budget_bytes, stream.cuda_stream)
+    ptrs = ([x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs], rows, cols,
+            [x.stride(0) for x in inputs], [y.stride(0) for y in outputs])
+    ws = (workspace.data_ptr(), workspace.numel() * workspace.element_size(), chunk_budget_bytes, stream.cuda_stream)
+    if Tw is None or Tw == T:
+        st = himuon_ns_tiled(n, *ptrs, T, K, a, b, c, code, compute, *ws)
+    else:
+        st = himuon_ns_tiled_hw(n, *ptrs, T, Tw, K, a, b, c, code, compute, *ws)
     if st != OK:
-        raise HimuonError(st, "himuon_ns_tiled")
+        raise HimuonError(st, "himuon_ns_tiled" if Tw is None or Tw == T else "himuon_ns_tiled_hw")
     _keep_alive(fresh, stream, dev)
     return outputs
 

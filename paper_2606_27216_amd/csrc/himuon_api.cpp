@@ -26,16 +26,17 @@ size_t elem_size(int dtype) { return dtype == HIMUON_BF16 ? 2 : 4; }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Tiles per matrix prefix and total; validates shapes. T >= 1.
-int plan_tiles(int64_t n_mats, const int64_t* rows, const int64_t* cols, int64_t T,
+// Tiles per matrix prefix and total for Th x Tw tiles; validates shapes.
+// Th, Tw >= 1.
+int plan_tiles(int64_t n_mats, const int64_t* rows, const int64_t* cols, int64_t Th, int64_t Tw,
                std::vector<int64_t>* begin, int64_t* total)
 {
-    if (n_mats < 1 || !rows || !cols || T < 1) return HIMUON_ERR_INVALID_ARG;
+    if (n_mats < 1 || !rows || !cols || Th < 1 || Tw < 1) return HIMUON_ERR_INVALID_ARG;
     int64_t acc = 0;
     if (begin) begin->resize((size_t)n_mats);
     for (int64_t m = 0; m < n_mats; ++m) {
         if (rows[m] < 1 || cols[m] < 1) return HIMUON_ERR_INVALID_ARG;
-        const int64_t t = ceil_div(rows[m], T) * ceil_div(cols[m], T);
+        const int64_t t = ceil_div(rows[m], Th) * ceil_div(cols[m], Tw);
         if (begin) (*begin)[(size_t)m] = acc;
         if (acc > INT64_MAX - t) return HIMUON_ERR_INVALID_ARG;
         acc += t;
@@ -44,14 +45,14 @@ int plan_tiles(int64_t n_mats, const int64_t* rows, const int64_t* cols, int64_t
     return HIMUON_OK;
 }
 
-// Fewest chunks whose per-chunk bytes (2*T*T*elem per tile) fit `budget`.
-int plan_chunk_count(int64_t total, int64_t T, size_t elem, size_t budget, int64_t* n_chunks)
+// Fewest chunks whose per-chunk bytes (2*Th*Tw*elem per tile) fit `budget`.
+int plan_chunk_count(int64_t total, int64_t Th, int64_t Tw, size_t elem, size_t budget, int64_t* n_chunks)
 {
     if (budget == 0) {
         *n_chunks = 1;
         return HIMUON_OK;
     }
-    const unsigned __int128 per_tile = (unsigned __int128)2 * (unsigned __int128)T * (unsigned __int128)T * elem;
+    const unsigned __int128 per_tile = (unsigned __int128)2 * (unsigned __int128)Th * (unsigned __int128)Tw * elem;
     const unsigned __int128 fit = (unsigned __int128)budget / per_tile;
     if (fit == 0) return HIMUON_ERR_WORKSPACE;
     const int64_t per_chunk = fit > (unsigned __int128)total ? total : (int64_t)fit;
@@ -235,9 +236,9 @@ int himuon_plan_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols,
     if (!total_tiles || !n_chunks) return HIMUON_ERR_INVALID_ARG;
     if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
     int64_t total = 0, nc = 0;
-    int st = plan_tiles(n_mats, rows, cols, T, nullptr, &total);
+    int st = plan_tiles(n_mats, rows, cols, T, T, nullptr, &total);
     if (st != HIMUON_OK) return st;
-    st = plan_chunk_count(total, T, elem_size(dtype), chunk_budget_bytes, &nc);
+    st = plan_chunk_count(total, T, T, elem_size(dtype), chunk_budget_bytes, &nc);
     if (st != HIMUON_OK) return st;
     *total_tiles = total;
     *n_chunks = nc;
@@ -271,21 +272,21 @@ bool has_step_kernel(int T, Storage st, Operand op, float c)
 }
 
 int validate_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
-                   const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
+                   const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int Tw, int K, float a, float b,
                    float c, int dtype, int compute, int* op)
 {
     if (n_mats < 1 || n_mats > INT32_MAX || !in_ptrs || !out_ptrs || !rows || !cols) return HIMUON_ERR_INVALID_ARG;
     if (K < 0 || !finite3(a, b, c)) return HIMUON_ERR_INVALID_ARG;
     if (dtype != HIMUON_F32 && dtype != HIMUON_BF16) return HIMUON_ERR_INVALID_ARG;
     if (compute < HIMUON_COMPUTE_DEFAULT || compute > HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
-    if (T != 32 && T != 64 && T != 128 && T != 256) return HIMUON_ERR_UNSUPPORTED;
+    if (Tw < 1) return HIMUON_ERR_UNSUPPORTED;
     for (int64_t m = 0; m < n_mats; ++m) {
         if (!in_ptrs[m] || !out_ptrs[m] || rows[m] < 1 || cols[m] < 1) return HIMUON_ERR_INVALID_ARG;
         const int64_t li = ld_in ? ld_in[m] : cols[m];
         const int64_t lo = ld_out ? ld_out[m] : cols[m];
         if (li < cols[m] || lo < cols[m]) return HIMUON_ERR_INVALID_ARG;
         if (rows[m] > INT64_MAX / li || rows[m] > INT64_MAX / lo) return HIMUON_ERR_INVALID_ARG;
-        if (ceil_div(cols[m], T) > INT32_MAX) return HIMUON_ERR_INVALID_ARG;
+        if (ceil_div(cols[m], Tw) > INT32_MAX) return HIMUON_ERR_INVALID_ARG;
     }
     const int r = resolve_compute(dtype, compute, K, a, b, c);
     if (r < 0) return r;
@@ -293,12 +294,12 @@ int validate_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_
     return HIMUON_OK;
 }
 
-int plan_tiled_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
+int plan_tiled_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int Th, int Tw, int dtype,
                       size_t chunk_budget_bytes, int64_t* total, int64_t* n_chunks)
 {
-    int s = plan_tiles(n_mats, rows, cols, T, nullptr, total);
+    int s = plan_tiles(n_mats, rows, cols, Th, Tw, nullptr, total);
     if (s != HIMUON_OK) return s;
-    s = plan_chunk_count(*total, T, elem_size(dtype), chunk_budget_bytes, n_chunks);
+    s = plan_chunk_count(*total, Th, Tw, elem_size(dtype), chunk_budget_bytes, n_chunks);
     if (s != HIMUON_OK) return s;
     // the kernels number the tiles of a call with 32-bit ids
     if (*total > (int64_t)UINT32_MAX) return HIMUON_ERR_UNSUPPORTED;
@@ -306,7 +307,7 @@ int plan_tiled_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, 
 }
 
 MatDesc make_desc(const void* in, void* out, int64_t rows, int64_t cols, int64_t ld_in, int64_t ld_out,
-                  int64_t tile_begin, int T, int dtype, const void* mom)
+                  int64_t tile_begin, int Tw, int dtype, const void* mom)
 {
     // 16-byte accesses at every column multiple of 8 (bf16) or 4 (f32)
     const size_t align = 16;
@@ -319,7 +320,7 @@ MatDesc make_desc(const void* in, void* out, int64_t rows, int64_t cols, int64_t
     d.ld_in = ld_in;
     d.ld_out = ld_out;
     d.tile_begin = tile_begin;
-    d.tiles_c = (int32_t)ceil_div(cols, T);
+    d.tiles_c = (int32_t)ceil_div(cols, Tw);
     d.flags = 0;
     // (a step's momentum shares the gradient's layout and alignment flag)
     if ((uintptr_t)in % align == 0 && ld_in % ld_mult == 0 && (!mom || (uintptr_t)mom % align == 0))
@@ -389,6 +390,11 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
 {
     // ---- validation: nothing is enqueued unless every check passes
     int op = 0;
+    if (T != 32 && T != 64 && T != 128 && T != 256) {
+        const int s = validate_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, 32, K, a, b, c, dtype,
+                                     compute, &op);
+        return s != HIMUON_OK ? s : HIMUON_ERR_UNSUPPORTED;
+    }
     int s = validate_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c, dtype, compute, &op);
     if (s != HIMUON_OK) return s;
     const Storage st = dtype == HIMUON_BF16 ? Storage::BF16 : Storage::F32;
@@ -404,7 +410,7 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
     if (opt_host && !has_step_kernel(T, st, opnd, c)) return HIMUON_ERR_UNSUPPORTED;
     if (!workspace || workspace_bytes < tiled_workspace(n_mats, opt_host != nullptr)) return HIMUON_ERR_WORKSPACE;
     int64_t total = 0, n_chunks = 0;
-    s = plan_tiled_chunks(n_mats, rows, cols, T, dtype, chunk_budget_bytes, &total, &n_chunks);
+    s = plan_tiled_chunks(n_mats, rows, cols, T, T, dtype, chunk_budget_bytes, &total, &n_chunks);
     if (s != HIMUON_OK) return s;
 
     // ---- descriptor table
@@ -440,9 +446,65 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
     return status;
 }
 
+int run_tiled_hw(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+                 const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int Th, int Tw, int K, float a,
+                 float b, float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
+                 size_t chunk_budget_bytes, void* stream)
+{
+    int op = 0;
+    int s = validate_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, Tw < 1 ? 1 : Tw, K, a, b, c,
+                           dtype, compute, &op);
+    if (s != HIMUON_OK) return s;
+    if (Th < 1 || Tw < 1) return HIMUON_ERR_INVALID_ARG;
+    const Storage st = dtype == HIMUON_BF16 ? Storage::BF16 : Storage::F32;
+    const Operand opnd = (Operand)op;
+    if (!has_rect_kernel(Th, Tw, st, opnd)) return HIMUON_ERR_UNSUPPORTED;
+    if (!workspace || workspace_bytes < tiled_workspace(n_mats, false)) return HIMUON_ERR_WORKSPACE;
+    int64_t total = 0, n_chunks = 0;
+    s = plan_tiled_chunks(n_mats, rows, cols, Th, Tw, dtype, chunk_budget_bytes, &total, &n_chunks);
+    if (s != HIMUON_OK) return s;
+
+    std::vector<MatDesc> descs((size_t)n_mats);
+    int64_t next = 0;
+    for (int64_t m = 0; m < n_mats; ++m) {
+        descs[(size_t)m] = make_desc(in_ptrs[m], out_ptrs[m], rows[m], cols[m], ld_in ? ld_in[m] : cols[m],
+                                     ld_out ? ld_out[m] : cols[m], next, Tw, dtype, nullptr);
+        next += ceil_div(rows[m], Th) * ceil_div(cols[m], Tw);
+    }
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    int cur = 0, dev = 0;
+    s = stream_device(hs, &cur, &dev);
+    if (s != HIMUON_OK) return s;
+    int status = upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
+    if (status == HIMUON_OK) {
+        KernelArgs ka = make_kernel_args(static_cast<const MatDesc*>(workspace), n_mats, K, a, b, c);
+        for (int64_t i = 0; i < n_chunks && status == HIMUON_OK; ++i) {
+            ka.tile_begin = chunk_bound(i, total, n_chunks);
+            ka.tile_end = chunk_bound(i + 1, total, n_chunks);
+            const hipError_t e = launch_ns_rect(Th, Tw, st, opnd, ka, hs);
+            if (e != hipSuccess) status = set_hip_error(e);
+        }
+    }
+    if (dev != cur) (void)hipSetDevice(cur);
+    return status;
+}
+
 }  // namespace himuon
 
 extern "C" {
+
+int himuon_ns_tiled_hw(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
+                       const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int Th, int Tw, int K,
+                       float a, float b, float c, int dtype, int compute, void* workspace, size_t workspace_bytes,
+                       size_t chunk_budget_bytes, void* stream)
+{
+    if (Th == Tw)
+        return himuon::run_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, Th, K, a, b, c, dtype,
+                                 compute, workspace, workspace_bytes, chunk_budget_bytes, stream, nullptr, 0.f, 1.f,
+                                 0.f, 0);
+    return himuon::run_tiled_hw(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, Th, Tw, K, a, b, c, dtype,
+                                compute, workspace, workspace_bytes, chunk_budget_bytes, stream);
+}
 
 int himuon_ns_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
                     const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a,

@@ -93,19 +93,28 @@ size_t tiled_workspace(int64_t n_mats, bool step);
 // pointer or null); make_kernel_args sets the scalars of a launch;
 // launch_chunks enqueues one launch per chunk; stream_device makes the
 // stream's device current (*cur: the previous one, to restore).
+// Tile shapes are Th x Tw (square: Th = Tw = T); validate_tiled checks
+// argument values only (the caller checks that a kernel serves the shape).
 int validate_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, const int64_t* rows,
-                   const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T, int K, float a, float b,
+                   const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int Tw, int K, float a, float b,
                    float c, int dtype, int compute, int* op);
-int plan_tiled_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int T, int dtype,
+int plan_tiled_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, int Th, int Tw, int dtype,
                       size_t chunk_budget_bytes, int64_t* total, int64_t* n_chunks);
 MatDesc make_desc(const void* in, void* out, int64_t rows, int64_t cols, int64_t ld_in, int64_t ld_out,
-                  int64_t tile_begin, int T, int dtype, const void* mom);
+                  int64_t tile_begin, int Tw, int dtype, const void* mom);
 KernelArgs make_kernel_args(const MatDesc* descs, int64_t n_mats, int K, float a, float b, float c);
 int launch_chunks(int T, Storage st, Operand op, KernelArgs ka, int64_t total, int64_t n_chunks, hipStream_t stream);
 int stream_device(hipStream_t stream, int* cur, int* dev);
 
 // The fp16-operand kernel family (bf16 storage), T in {32, 64, 128, 256}.
 hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream);
+
+// The fused rectangular-tile family (ns_rect.hip): Th x Tw tiles with
+// {min, max} in {32} x {64, 128, 256} (fp32 storage with fp32 operands,
+// bf16 storage with fp16 or bf16 operands) or {32} x {512}, {64} x {128,
+// 256} (bf16 storage only).
+bool has_rect_kernel(int Th, int Tw, Storage st, Operand op);
+hipError_t launch_ns_rect(int Th, int Tw, Storage st, Operand op, const KernelArgs& args, hipStream_t stream);
 
 // Host helpers shared by the entry points (himuon_api.cpp).
 extern thread_local int g_last_hip_error;

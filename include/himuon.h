@@ -172,6 +172,37 @@ int himuon_ns_tiled_hw(int64_t n_mats,
                        size_t chunk_budget_bytes,
                        void* stream);
 
+/* Most matrices one himuon_ns_tiled_noalloc call takes. */
+#define HIMUON_NOALLOC_MAX_MATS 1024
+
+/*
+ * himuon_ns_tiled for callers that cannot allocate memory or own a workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation. Same arguments, kernels, results (bit for bit) and errors as
+ * himuon_ns_tiled, without workspace and workspace_bytes:
+ *   - the per-matrix descriptor table lives in a 64 KiB device array that the
+ *     library holds on each GPU it runs on until the process ends, so a call
+ *     takes at most HIMUON_NOALLOC_MAX_MATS (1024) matrices; more is
+ *     HIMUON_ERR_WORKSPACE, returned before anything is enqueued;
+ *   - every call on a GPU rewrites that array through small upload kernels
+ *     enqueued on `stream` ahead of the tile kernels, so calls on one stream
+ *     follow each other safely, but calls that overlap on one GPU (on
+ *     different streams, or from several threads) race and must not be made;
+ *   - the call allocates nothing, on the host or the device: no hipMalloc,
+ *     no pinned staging; the descriptors travel in kernel arguments;
+ *   - only calls a fused kernel serves: T = 256 with fp32 storage or bf16
+ *     operands (the library-GEMM route, which needs a workspace) is
+ *     HIMUON_ERR_UNSUPPORTED.
+ */
+int himuon_ns_tiled_noalloc(int64_t n_mats,
+                            const void* const* in_ptrs, void* const* out_ptrs,
+                            const int64_t* rows, const int64_t* cols,
+                            const int64_t* ld_in, const int64_t* ld_out,
+                            int T, int K, float a, float b, float c,
+                            int dtype, int compute,
+                            size_t chunk_budget_bytes,
+                            void* stream);
+
 /*
  * Phi_K through library GEMMs: the full-matrix branch and large tiles.
  *

@@ -61,6 +61,10 @@ def lib():
                                          ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int, ctypes.c_int,
                                          vp, sz, sz, vp]
         L.himuon_ns_tiled_hw.restype = ctypes.c_int
+        L.himuon_ns_tiled_noalloc.argtypes = [i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int,
+                                              ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                              ctypes.c_int, ctypes.c_int, sz, vp]
+        L.himuon_ns_tiled_noalloc.restype = ctypes.c_int
         L.himuon_ns_gemm_workspace_size.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                                     ctypes.c_int, ctypes.c_float, ctypes.c_float,
                                                     ctypes.c_float, sz]
@@ -144,6 +148,20 @@ def himuon_ns_tiled_hw(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, Th,
         None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
         int(Th), int(Tw), int(K), float(a), float(b), float(c), int(dtype), int(compute),
         int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes),
+        int(stream) if stream else None))
+
+
+NOALLOC_MAX_MATS = 1024  # HIMUON_NOALLOC_MAX_MATS
+
+
+def himuon_ns_tiled_noalloc(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c,
+                            dtype, compute, chunk_budget_bytes, stream) -> int:
+    """Same arguments as the C function (himuon_ns_tiled without the
+    workspace). Returns the status code."""
+    return int(lib().himuon_ns_tiled_noalloc(
+        int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
+        None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
+        int(T), int(K), float(a), float(b), float(c), int(dtype), int(compute), int(chunk_budget_bytes),
         int(stream) if stream else None))
 
 

@@ -32,6 +32,7 @@ COMMON = [
 SOURCES = [
     ("ns_tiled_kernels.hip", []),
     ("ns_tiled_f16.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form"]),
+    ("ns_tiled_noalloc.hip", []),
     ("ns_rect.hip", []),
     ("ns_gemm_kernels.hip", []),
     ("optim_kernels.hip", []),

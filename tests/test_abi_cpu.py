@@ -106,6 +106,21 @@ def test_validation_rejects_before_any_hip_call(kw, status):
     assert _call(**kw) == status
 
 
+def test_noalloc_validation_rejects_before_any_hip_call():
+    """The entry point that allocates nothing validates as himuon_ns_tiled,
+    and rejects more matrices than its device table holds."""
+    kw = dict(n_mats=1, in_ptrs=[FAKE], out_ptrs=[FAKE], rows=[64], cols=[64], ld_in=None, ld_out=None, T=32, K=5,
+              a=3.4445, b=-4.775, c=2.0315, dtype=hm.BF16, compute=hm.COMPUTE_DEFAULT, chunk_budget_bytes=0,
+              stream=None)
+    for over, status in ((dict(rows=[0]), hm.ERR_INVALID_ARG), (dict(T=48), hm.ERR_UNSUPPORTED),
+                         (dict(a=50.0, b=0.0, c=0.0), hm.ERR_RANGE), (dict(chunk_budget_bytes=100), hm.ERR_WORKSPACE),
+                         (dict(T=256, dtype=hm.F32), hm.ERR_UNSUPPORTED)):
+        assert hm.himuon_ns_tiled_noalloc(**{**kw, **over}) == status, over
+    n = hm.NOALLOC_MAX_MATS + 1
+    assert hm.himuon_ns_tiled_noalloc(**{**kw, "n_mats": n, "in_ptrs": [FAKE] * n, "out_ptrs": [FAKE] * n,
+                                         "rows": [64] * n, "cols": [64] * n}) == hm.ERR_WORKSPACE
+
+
 def test_null_arrays_rejected():
     L = hm.lib()
     assert L.himuon_ns_tiled(1, None, None, None, None, None, None, 32, 5, 1.0, 0.0, 0.0, 1, 0,

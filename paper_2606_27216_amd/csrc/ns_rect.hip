@@ -19,7 +19,7 @@
 //   - every wave forms B = bA + cA^2 (M x M, small) and its slab of
 //     aX + BX, the column pieces of its own slab coming from LDS (written by
 //     the same wave, in its own region).
-// The only cross-wave traffic is the M x M partials. Operands are rounded
+// The only cross-wave traffic is the M x M partials and their sum. Operands are rounded
 // once to fp16/bf16 (round to nearest even) or stay fp32; accumulation and
 // the epilogues are fp32 with an fp32 master iterate, as in the square
 // generic kernel.
@@ -74,7 +74,9 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
     constexpr int PART = NBR * NBR * 16 * 64;        // floats
     constexpr int XC = NBR * NBC * S * 64;           // 16-byte slots
     constexpr int REGION = PART * 4 > XC * 16 ? PART * 4 : XC * 16;  // bytes
+    constexpr int NV = NBR * NBR * 4;                // 16-byte vectors of the Gram per lane
     __shared__ __attribute__((aligned(16))) unsigned char s_reg[W * REGION];
+    __shared__ f32x4 s_total[NV * 64];               // the summed Gram
     __shared__ float s_red[2][W];
 
     const int lane = threadIdx.x & 63;
@@ -82,8 +84,8 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
     const int li = lane & 31, lh = lane >> 5;
     const int t4 = li & 3, quad = li >> 2;
     const int xg = quad >> 1, xh = quad & 1;
-    float* const part_all = reinterpret_cast<float*>(s_reg);
-    float* const part = reinterpret_cast<float*>(s_reg + wave * REGION);
+    f32x4* const part4 = reinterpret_cast<f32x4*>(s_reg + wave * REGION);
+    f32x4* const total4 = s_total;
     u32x4* const xc = reinterpret_cast<u32x4*>(s_reg + wave * REGION);
     const int slab0 = wave * NBC * 32;  // first iterate column of the wave's slab
 
@@ -196,30 +198,42 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
                     for (int J = 0; J < NBR; ++J) G[I][J] = chain_sum<NC>(Gc[I][J]);
             }
 
-            // sum of the partials, in wave order 0 .. W-1 (the same in every
-            // wave). A wave's region holds only its own column pieces between
-            // the last barrier of a step and here, so it overwrites them
-            // without waiting for the others.
+            // sum of the partials. Wave w sums the 16-byte vectors v = w, w + W, ...
+            // of the partials in wave order 0 .. W-1 and stores them to the
+            // total; every wave then reads the whole total, so all hold the
+            // same fp32 A. A wave's region holds only its own column pieces
+            // between the last barrier of a step and here, so it overwrites
+            // them without waiting for the others.
 #pragma unroll
             for (int I = 0; I < NBR; ++I)
 #pragma unroll
                 for (int J = 0; J < NBR; ++J)
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) part[((I * NBR + J) * 16 + v) * 64 + lane] = G[I][J][v];
+                    for (int v4 = 0; v4 < 4; ++v4)
+                        part4[((I * NBR + J) * 4 + v4) * 64 + lane] =
+                            f32x4{G[I][J][4 * v4], G[I][J][4 * v4 + 1], G[I][J][4 * v4 + 2], G[I][J][4 * v4 + 3]};
             __syncthreads();
 #pragma unroll
+            for (int vi = 0; vi < NV; vi += W) {
+                if (vi + wave < NV) {
+                    const int idx = (vi + wave) * 64 + lane;
+                    f32x4 acc = reinterpret_cast<const f32x4*>(s_reg)[idx];
+#pragma unroll
+                    for (int w = 1; w < W; ++w) acc += reinterpret_cast<const f32x4*>(s_reg + w * REGION)[idx];
+                    total4[idx] = acc;
+                }
+            }
+            __syncthreads();  // every partial is summed; every wave reads the total
+#pragma unroll
             for (int I = 0; I < NBR; ++I)
 #pragma unroll
                 for (int J = 0; J < NBR; ++J)
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        float acc = part_all[((I * NBR + J) * 16 + v) * 64 + lane];
+                    for (int v4 = 0; v4 < 4; ++v4) {
+                        const f32x4 t = total4[((I * NBR + J) * 4 + v4) * 64 + lane];
 #pragma unroll
-                        for (int w = 1; w < W; ++w)
-                            acc += part_all[w * (REGION / 4) + ((I * NBR + J) * 16 + v) * 64 + lane];
-                        G[I][J][v] = acc;
+                        for (int e = 0; e < 4; ++e) G[I][J][4 * v4 + e] = t[e];
                     }
-            __syncthreads();  // every wave has read every partial
 
             // column pieces of the slab for the B X product (own region)
 #pragma unroll

@@ -37,28 +37,6 @@ template <int N> struct RectShape {
     static constexpr int NBC = N / 32 / W;              // 32-column blocks per wave slab
 };
 
-// Element (i, j) of the iterate, widened to fp32: S[r0 + i][c0 + j] for a
-// wide tile, S[r0 + j][c0 + i] for a tall one; zero outside the matrix.
-template <Storage ST>
-HM_DEV float load1(const void* base, int64_t gr, int64_t gc, int64_t ld, int64_t rows, int64_t cols)
-{
-    if (gr >= rows || gc >= cols) return 0.f;
-    if constexpr (ST == Storage::BF16)
-        return __uint_as_float(((uint32_t) static_cast<const uint16_t*>(base)[gr * ld + gc]) << 16);
-    else
-        return static_cast<const float*>(base)[gr * ld + gc];
-}
-
-template <Storage ST>
-HM_DEV void store1(void* base, int64_t gr, int64_t gc, int64_t ld, int64_t rows, int64_t cols, float v)
-{
-    if (gr >= rows || gc >= cols) return;
-    if constexpr (ST == Storage::BF16)
-        static_cast<uint16_t*>(base)[gr * ld + gc] = (uint16_t)(pack2<Operand::BF16>(v, 0.f) & 0xffffu);
-    else
-        static_cast<float*>(base)[gr * ld + gc] = v;
-}
-
 template <int M, int N, Storage ST, Operand OP, bool TALL>
 __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const KernelArgs args)
 {
@@ -89,6 +67,74 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
     u32x4* const xc = reinterpret_cast<u32x4*>(s_reg + wave * REGION);
     const int slab0 = wave * NBC * 32;  // first iterate column of the wave's slab
 
+    // Tall tiles: a row-major copy of the TH x TW tile in the storage type,
+    // over the wave regions (they are free outside the K loop).
+    constexpr int ES = ST == Storage::BF16 ? 2 : 4;  // bytes per element
+    constexpr int EPC = 16 / ES;                      // elements per 16-byte chunk
+    constexpr int CPR = TW / EPC;                     // chunks per tile row
+    static_assert(!TALL || TH * TW * ES <= W * REGION, "a tall tile's copy fits the wave regions");
+    auto stage_rows = [&](const void* base, int64_t ld, int64_t rows, int64_t cols, int64_t r0, int64_t c0,
+                          bool vec) {
+        for (int ch = threadIdx.x; ch < TH * CPR; ch += W * 64) {
+            const int r = ch / CPR, cc = ch % CPR;
+            const int64_t gr = r0 + r, gc = c0 + cc * EPC;
+            u32x4 v;
+            if (vec) {
+                v = *(const gbl_u32x4*)(static_cast<const unsigned char*>(base) + (gr * ld + gc) * ES);
+            } else {
+                uint32_t h[4] = {0u, 0u, 0u, 0u};
+                if constexpr (ST == Storage::BF16) {
+                    const uint16_t* p = static_cast<const uint16_t*>(base) + gr * ld + gc;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (gr < rows && gc + e < cols) h[e >> 1] |= (uint32_t)p[e] << (16 * (e & 1));
+                } else {
+                    const uint32_t* p = static_cast<const uint32_t*>(base) + gr * ld + gc;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (gr < rows && gc + e < cols) h[e] = p[e];
+                }
+                v = u32x4{h[0], h[1], h[2], h[3]};
+            }
+            *reinterpret_cast<u32x4*>(s_reg + (r * TW + cc * EPC) * ES) = v;
+        }
+    };
+    auto unstage_rows = [&](void* base, int64_t ld, int64_t rows, int64_t cols, int64_t r0, int64_t c0, bool vec) {
+        for (int ch = threadIdx.x; ch < TH * CPR; ch += W * 64) {
+            const int r = ch / CPR, cc = ch % CPR;
+            const int64_t gr = r0 + r, gc = c0 + cc * EPC;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(s_reg + (r * TW + cc * EPC) * ES);
+            if (vec) {
+                *(gbl_u32x4*)(static_cast<unsigned char*>(base) + (gr * ld + gc) * ES) = v;
+            } else if (gr < rows) {
+                if constexpr (ST == Storage::BF16) {
+                    uint16_t* p = static_cast<uint16_t*>(base) + gr * ld + gc;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (gc + e < cols) p[e] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+                } else {
+                    uint32_t* p = static_cast<uint32_t*>(base) + gr * ld + gc;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (gc + e < cols) p[e] = v[e];
+                }
+            }
+        }
+    };
+    // element (r, c) of the copy (tile row r, column c), widened to fp32, and its store
+    auto stage_get = [&](int r, int c) -> float {
+        if constexpr (ST == Storage::BF16)
+            return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(s_reg)[r * TW + c] << 16);
+        else
+            return reinterpret_cast<const float*>(s_reg)[r * TW + c];
+    };
+    auto stage_put = [&](int r, int c, float v) {
+        if constexpr (ST == Storage::BF16)
+            reinterpret_cast<uint16_t*>(s_reg)[r * TW + c] = (uint16_t)(pack2<Operand::BF16>(v, 0.f) & 0xffffu);
+        else
+            reinterpret_cast<float*>(s_reg)[r * TW + c] = v;
+    };
+
     const int64_t n_tiles = args.tile_end - args.tile_begin;
     int mhint = 0;
     for (int64_t local = blockIdx.x; local < n_tiles; local += gridDim.x) {
@@ -103,25 +149,38 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
         const bool vin = !TALL && full && (d.flags & MAT_VEC_IN);
         const bool vout = !TALL && full && (d.flags & MAT_VEC_OUT);
 
-        // ---- gather the wave's slab of the iterate (zero padded) as fp32 row pieces
+        // ---- gather the wave's slab of the iterate (zero padded) as fp32 row pieces.
+        //      A tall tile goes through LDS: the workgroup moves its rows in
+        //      16-byte chunks into a row-major copy, and each wave reads the
+        //      columns of that copy as the rows of X = S^T.
         f32x16 X[NBR][NBC];
+        if constexpr (TALL) {
+            const bool vin_t = full && (d.flags & MAT_VEC_IN);
+            stage_rows(d.in, d.ld_in, d.rows, d.cols, row0, col0, vin_t);
+            __syncthreads();
 #pragma unroll
-        for (int I = 0; I < NBR; ++I)
+            for (int I = 0; I < NBR; ++I)
 #pragma unroll
-            for (int q = 0; q < NBC; ++q)
+                for (int q = 0; q < NBC; ++q)
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int64_t i = 32 * I + li, j = slab0 + 32 * q + 8 * g + 4 * lh;
-                    if constexpr (TALL) {
+                    for (int g = 0; g < 4; ++g)
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            X[I][q][4 * g + e] = load1<ST>(d.in, row0 + j + e, col0 + i, d.ld_in, d.rows, d.cols);
-                    } else {
+                            X[I][q][4 * g + e] = stage_get(slab0 + 32 * q + 8 * g + 4 * lh + e, 32 * I + li);
+            __syncthreads();  // the K loop reuses the staging area
+        } else {
+#pragma unroll
+            for (int I = 0; I < NBR; ++I)
+#pragma unroll
+                for (int q = 0; q < NBC; ++q)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int64_t i = 32 * I + li, j = slab0 + 32 * q + 8 * g + 4 * lh;
                         const f32x4 v = load4<ST>(d.in, row0 + i, col0 + j, d.ld_in, d.rows, d.cols, vin);
 #pragma unroll
                         for (int e = 0; e < 4; ++e) X[I][q][4 * g + e] = v[e];
                     }
-                }
+        }
 
         // ---- X_0 = S / ||S||_F after an exact power-of-two pre-scale (the
         //      fp32 sum of squares neither overflows nor underflows)
@@ -350,25 +409,35 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
             }
         }
 
-        // ---- write back the unpadded part
+        // ---- write back the unpadded part (a tall tile through the LDS copy)
+        if constexpr (TALL) {
+            __syncthreads();  // every wave is done with its region of the staging area
 #pragma unroll
-        for (int I = 0; I < NBR; ++I)
+            for (int I = 0; I < NBR; ++I)
 #pragma unroll
-            for (int q = 0; q < NBC; ++q)
+                for (int q = 0; q < NBC; ++q)
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int64_t i = 32 * I + li, j = slab0 + 32 * q + 8 * g + 4 * lh;
-                    if constexpr (TALL) {
+                    for (int g = 0; g < 4; ++g)
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            store1<ST>(d.out, row0 + j + e, col0 + i, d.ld_out, d.rows, d.cols, X[I][q][4 * g + e]);
-                    } else {
+                            stage_put(slab0 + 32 * q + 8 * g + 4 * lh + e, 32 * I + li, X[I][q][4 * g + e]);
+            __syncthreads();
+            const bool vout_t = full && (d.flags & MAT_VEC_OUT);
+            unstage_rows(d.out, d.ld_out, d.rows, d.cols, row0, col0, vout_t);
+        } else {
+#pragma unroll
+            for (int I = 0; I < NBR; ++I)
+#pragma unroll
+                for (int q = 0; q < NBC; ++q)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int64_t i = 32 * I + li, j = slab0 + 32 * q + 8 * g + 4 * lh;
                         const f32x4 v = {X[I][q][4 * g + 0], X[I][q][4 * g + 1], X[I][q][4 * g + 2],
                                          X[I][q][4 * g + 3]};
                         store4<ST>(d.out, row0 + i, col0 + j, d.ld_out, d.rows, d.cols, vout, v);
                     }
-                }
-        __syncthreads();  // the next tile's normalisation reuses s_red
+        }
+        __syncthreads();  // the next tile's normalisation reuses s_red (and a tall tile's staging area)
     }
 }
 

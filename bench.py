@@ -295,9 +295,12 @@ def bench_optstep(args, hm, torch, np, dev):
     before every step (outside the timed region), HiMuon with T = 512, K = 5
     against full-matrix Muon (T = 0: the same Alg. 1 step with Phi_K of the
     whole matrix), each as one call per layer and as one batched call over
-    all layers. Per-step time is the median of the HIP-event times of
-    `--steps` steps after `--warmup` (the paper: 50 after 20); peak memory
-    is torch's peak allocation over the variant's run, workspace included."""
+    all layers; for HiMuon also the batched call recorded once into a plan (a
+    HIP graph) and replayed each step, the study's graph-captured variant.
+    Per-step time is the median of the HIP-event times of
+    `--steps` steps after `--warmup` (the paper: 50 after 20), beside the
+    median host time the step's calls take to enqueue; peak memory is
+    torch's peak allocation over the variant's run, workspace included."""
     coeffs = tuple(float(np.float32(v)) for v in hm.QUINTIC)
     hs = [int(h) for h in args.hidden.split(",")]
     stream = torch.cuda.current_stream(dev)
@@ -308,19 +311,21 @@ def bench_optstep(args, hm, torch, np, dev):
         Ws = [(torch.randn(H, H, device=dev, generator=gen) * 0.02).to(torch.bfloat16) for _ in range(8)]
         Gs = [torch.empty(H, H, dtype=torch.bfloat16, device=dev) for _ in range(8)]
         res = {}
-        variants = [("muon_full_per_layer", 0, False), ("muon_full_batched", 0, True)]
+        variants = [("muon_full_per_layer", 0, False, False), ("muon_full_batched", 0, True, False)]
         for t in (int(v) for v in args.optstep_T.split(",")):
-            variants += [(f"himuon_T{t}_per_layer", t, False), (f"himuon_T{t}_batched", t, True)]
+            variants += [(f"himuon_T{t}_per_layer", t, False, False), (f"himuon_T{t}_batched", t, True, False),
+                         (f"himuon_T{t}_batched_graph", t, True, True)]
         if args.variants != "all":
             keep = args.variants.split(",")
             variants = [v for v in variants if v[0] in keep]
-        for name, T, batched in variants:
+        for name, T, batched, graph in variants:
             Ms = [torch.zeros_like(w) for w in Ws]
             torch.cuda.synchronize()
             torch.cuda.reset_peak_memory_stats(dev)
             groups = [list(range(8))] if batched else [[i] for i in range(8)]
             opts = [hm.HiMuon([Ws[i] for i in g], T=T, K=5, coeffs=coeffs, lr=0.02, momentum=0.95,
-                              weight_decay=0.0, nesterov=True, scale_c=0.2, tune=args.tune) for g in groups]
+                              weight_decay=0.0, nesterov=True, scale_c=0.2, tune=args.tune, capture=graph)
+                    for g in groups]
             for o, g in zip(opts, groups):
                 o.moms = [Ms[i] for i in g]
             ws_bytes = sum(o._workspace.numel() for o in opts)
@@ -329,20 +334,24 @@ def bench_optstep(args, hm, torch, np, dev):
                 for o, g in zip(opts, groups):
                     o.step([Gs[i] for i in g], stream=stream)
 
-            times = []
+            times, host = [], []
             for it in range(args.warmup + args.steps):
                 for g in Gs:
                     g.normal_(generator=gen)
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a.record(stream)
+                h0 = time.perf_counter()
                 one_step()
+                h1 = time.perf_counter()
                 b.record(stream)
                 if it >= args.warmup:
                     times.append((a, b))
+                    host.append(h1 - h0)
             torch.cuda.synchronize()
             ms = np.array([a.elapsed_time(b) for a, b in times])
             flops = 8 * (6.0 * H * H * min(T, H) * 5 if T else 6.0 * H ** 3 * 5)
             res[name] = {"median_ms": round(float(np.median(ms)), 4),
+                         "host_us_per_step": round(float(np.median(host)) * 1e6, 1),
                          "iqr_ms": round(float(np.percentile(ms, 75) - np.percentile(ms, 25)), 4),
                          "ns_tflops": round(flops / (float(np.median(ms)) * 1e-3) / 1e12, 2),
                          "peak_mem_MiB": round(torch.cuda.max_memory_allocated(dev) / 2 ** 20, 1),

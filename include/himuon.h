@@ -360,6 +360,57 @@ int himuon_step(int64_t n_mats,
                 void* stream);
 
 /*
+ * Plans: a himuon_ns_tiled or himuon_step call recorded once, on the current
+ * device, into a HIP graph and replayed by himuon_plan_launch, whose only
+ * host work is one graph launch (no validation, planning or table staging
+ * per call). This is the graph-captured cross-layer optimizer step of the
+ * optimizer-step study (Sec. 6.4) and the graph-capture state that the
+ * runtime tile-size reconfiguration rebuilds when T changes (Sec. 4.4.3).
+ *
+ * himuon_plan_ns_tiled / himuon_plan_step take the arguments of
+ * himuon_ns_tiled / himuon_step without the stream, validate them as those
+ * do (returning the same errors, with *plan = NULL), and record the call:
+ * every device pointer and every scalar is fixed in the plan. Each launch
+ * then performs the recorded call again on the current contents of those
+ * buffers, in `stream` order: it first copies the call's descriptor tables
+ * from pinned host buffers that the plan owns into `workspace`, so the
+ * workspace and every matrix must stay allocated, and the workspace must not
+ * be used by other work that overlaps a launch, until the plan is destroyed.
+ * A launch's results equal those of the recorded call bit for bit.
+ * Recording synchronises nothing and enqueues nothing on the caller's
+ * streams; it allocates the plan's host memory, a private stream and the
+ * graph (configuration-time calls, like himuon_gemm_tune).
+ *
+ * himuon_plan_launch returns HIMUON_ERR_INVALID_ARG for a NULL plan or a
+ * stream on another device than the plan's; himuon_plan_destroy frees the
+ * plan (NULL is a no-op) and must not be called while a launch of it may
+ * still run.
+ */
+typedef struct himuon_plan himuon_plan_t;
+
+int himuon_plan_ns_tiled(himuon_plan_t** plan, int64_t n_mats,
+                         const void* const* in_ptrs, void* const* out_ptrs,
+                         const int64_t* rows, const int64_t* cols,
+                         const int64_t* ld_in, const int64_t* ld_out,
+                         int T, int K, float a, float b, float c,
+                         int dtype, int compute,
+                         void* workspace, size_t workspace_bytes,
+                         size_t chunk_budget_bytes);
+
+int himuon_plan_step(himuon_plan_t** plan, int64_t n_mats,
+                     void* const* weights, const void* const* grads, void* const* moms,
+                     const int64_t* rows, const int64_t* cols, const int64_t* ld,
+                     int T, int K, float a, float b, float c,
+                     float lr, float momentum, float weight_decay, int nesterov, float scale_c,
+                     int dtype, int compute,
+                     void* workspace, size_t workspace_bytes,
+                     size_t chunk_budget_bytes);
+
+int himuon_plan_launch(const himuon_plan_t* plan, void* stream);
+
+void himuon_plan_destroy(himuon_plan_t* plan);
+
+/*
  * Host-only planner (no HIP call): the tiles and chunks himuon_ns_tiled
  * would use, i.e. the memory-bounded chunking of cross-layer batches of
  * Sec. 4.4.2 (a batch larger than the memory budget is split into the

@@ -89,6 +89,16 @@ def lib():
         L.himuon_ns_gemm_hw.argtypes = [i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                         f, f, f, ctypes.c_int, ctypes.c_int, vp, sz, sz, vp]
         L.himuon_ns_gemm_hw.restype = ctypes.c_int
+        L.himuon_plan_ns_tiled.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int,
+                                           f, f, f, ctypes.c_int, ctypes.c_int, vp, sz, sz]
+        L.himuon_plan_ns_tiled.restype = ctypes.c_int
+        L.himuon_plan_step.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, f, f, f,
+                                       f, f, f, ctypes.c_int, f, ctypes.c_int, ctypes.c_int, vp, sz, sz]
+        L.himuon_plan_step.restype = ctypes.c_int
+        L.himuon_plan_launch.argtypes = [vp, vp]
+        L.himuon_plan_launch.restype = ctypes.c_int
+        L.himuon_plan_destroy.argtypes = [vp]
+        L.himuon_plan_destroy.restype = None
         L.himuon_plan_chunks.argtypes = [i64, vp, vp, ctypes.c_int, ctypes.c_int, sz, vp, vp, vp, i64]
         L.himuon_plan_chunks.restype = ctypes.c_int
         L.himuon_select_compute.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -258,6 +268,94 @@ def gemm_tune(shapes, T, dtype, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT, ch
                              workspace.numel() * workspace.element_size(), chunk_budget_bytes, stream.cuda_stream)
     if st != OK:
         raise HimuonError(st, "himuon_gemm_tune_hw")
+
+
+def himuon_plan_ns_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c, dtype, compute,
+                         workspace, workspace_bytes, chunk_budget_bytes):
+    """Records a himuon_ns_tiled call into a plan. Returns (status, plan handle or None)."""
+    h = ctypes.c_void_p()
+    st = int(lib().himuon_plan_ns_tiled(
+        ctypes.byref(h), int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
+        None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
+        int(T), int(K), float(a), float(b), float(c), int(dtype), int(compute),
+        int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes)))
+    return st, (h.value if st == OK else None)
+
+
+def himuon_plan_step(n_mats, weights, grads, moms, rows, cols, ld, T, K, a, b, c, lr, momentum, weight_decay,
+                     nesterov, scale_c, dtype, compute, workspace, workspace_bytes, chunk_budget_bytes):
+    """Records a himuon_step call into a plan. Returns (status, plan handle or None)."""
+    h = ctypes.c_void_p()
+    st = int(lib().himuon_plan_step(
+        ctypes.byref(h), int(n_mats), _ptr_array(weights), _ptr_array(grads), _ptr_array(moms), _i64_array(rows),
+        _i64_array(cols), None if ld is None else _i64_array(ld), int(T), int(K), float(a), float(b), float(c),
+        float(lr), float(momentum), float(weight_decay), int(bool(nesterov)), float(scale_c), int(dtype),
+        int(compute), int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes)))
+    return st, (h.value if st == OK else None)
+
+
+def himuon_plan_launch(plan, stream) -> int:
+    return int(lib().himuon_plan_launch(plan, int(stream) if stream else None))
+
+
+def himuon_plan_destroy(plan) -> None:
+    lib().himuon_plan_destroy(plan)
+
+
+class Plan:
+    """A recorded call (``himuon_plan_*``): ``launch(stream)`` replays it.
+    Keeps the tensors it was recorded on (and its workspace) alive."""
+
+    def __init__(self, handle, keep):
+        self.handle = handle
+        self._keep = keep
+
+    def launch(self, stream=None):
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        st = himuon_plan_launch(self.handle, stream.cuda_stream)
+        if st != OK:
+            raise HimuonError(st, "himuon_plan_launch")
+
+    def close(self):
+        if self.handle:
+            import torch
+            torch.cuda.synchronize()
+            himuon_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def plan_ns_tiled(inputs, outputs, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0,
+                  workspace=None):
+    """Records ``ns_tiled(inputs, outputs, ...)`` into a Plan (on the inputs'
+    device); every launch recomputes the outputs from the inputs' current
+    contents."""
+    import torch
+    inputs, outputs = list(inputs), list(outputs)
+    code = _dtype_code(inputs[0])
+    dev = inputs[0].device
+    a, b, c = coeffs
+    rows = [x.shape[0] for x in inputs]
+    cols = [x.shape[1] for x in inputs]
+    if workspace is None:
+        need = himuon_ns_tiled_call_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
+        workspace = torch.empty(max(need, himuon_ns_tiled_workspace_size(len(inputs))), dtype=torch.uint8,
+                                device=dev)
+    with torch.cuda.device(dev):
+        st, h = himuon_plan_ns_tiled(
+            len(inputs), [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs], rows, cols,
+            [x.stride(0) for x in inputs], [y.stride(0) for y in outputs], T, K, a, b, c, code, compute,
+            workspace.data_ptr(), workspace.numel() * workspace.element_size(), chunk_budget_bytes)
+    if st != OK:
+        raise HimuonError(st, "himuon_plan_ns_tiled")
+    return Plan(h, (inputs, outputs, workspace))
 
 
 def himuon_plan_chunks(rows, cols, T, dtype=BF16, chunk_budget_bytes=0):
@@ -469,10 +567,14 @@ class HiMuon:
     (Sec. 4.4.3) and keeps the momentum; T = 0 is the full-matrix branch.
     Every step is one library call over all matrices (cross-layer batching,
     Sec. 4.4.2). With ``tune`` (default), a tile size served by the library
-    GEMMs has its GEMM kernels chosen by timing at (re)configuration."""
+    GEMMs has its GEMM kernels chosen by timing at (re)configuration. With
+    ``capture``, the step is recorded once into a plan (a HIP graph, rebuilt
+    by ``reconfigure`` and when the gradient buffers change) and each step is
+    one graph launch."""
 
     def __init__(self, params, T=512, K=5, coeffs=QUINTIC, lr=0.02, momentum=0.95, weight_decay=0.0,
-                 nesterov=True, scale_c=0.2, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0, tune=True):
+                 nesterov=True, scale_c=0.2, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0, tune=True,
+                 capture=False):
         import torch
         self.params = list(params)
         if not self.params:
@@ -485,7 +587,10 @@ class HiMuon:
         self.weight_decay, self.nesterov, self.scale_c = weight_decay, nesterov, scale_c
         self.compute, self.chunk_budget_bytes = compute, chunk_budget_bytes
         self.tune = tune
+        self.capture = capture
         self._workspace = None
+        self._plan = None
+        self._plan_key = None
         self.reconfigure(T)
 
     def reconfigure(self, T):
@@ -504,8 +609,40 @@ class HiMuon:
             gemm_tune([tuple(p.shape) for p in self.params], T, code, K=self.K, coeffs=self.coeffs,
                       compute=self.compute, chunk_budget_bytes=self.chunk_budget_bytes, workspace=self._workspace)
         self.T = T
+        if self._plan is not None:  # the recorded step belongs to the previous tile size
+            self._plan.close()
+            self._plan = None
+
+    def _step_plan(self, grads):
+        """The recorded step for these gradient buffers (re-recorded when they change)."""
+        import torch
+        key = tuple(g.data_ptr() for g in grads)
+        if self._plan is None or self._plan_key != key:
+            if self._plan is not None:
+                self._plan.close()
+            a, b, c = self.coeffs
+            code = _dtype_code(self.params[0])
+            with torch.cuda.device(self.params[0].device):
+                st, h = himuon_plan_step(
+                    len(self.params), [p.data_ptr() for p in self.params], [g.data_ptr() for g in grads],
+                    [m.data_ptr() for m in self.moms], [p.shape[0] for p in self.params],
+                    [p.shape[1] for p in self.params], [p.stride(0) for p in self.params], self.T, self.K, a, b, c,
+                    self.lr, self.momentum, self.weight_decay, self.nesterov, self.scale_c, code, self.compute,
+                    self._workspace.data_ptr(), self._workspace.numel(), self.chunk_budget_bytes)
+            if st != OK:
+                raise HimuonError(st, "himuon_plan_step")
+            self._plan = Plan(h, (list(grads),))
+            self._plan_key = key
+        return self._plan
 
     def step(self, grads, stream=None):
+        if self.capture:
+            # one graph launch per step: the gradient buffers must keep their storage between steps
+            for g, p in zip(grads, self.params):
+                if g.shape != p.shape or g.dtype != p.dtype or g.stride(0) != p.stride(0):
+                    raise ValueError("each gradient must match its parameter's shape, dtype and row stride")
+            self._step_plan(list(grads)).launch(stream)
+            return self.params
         return step(self.params, grads, self.moms, T=self.T, K=self.K, coeffs=self.coeffs, lr=self.lr,
                     momentum=self.momentum, weight_decay=self.weight_decay, nesterov=self.nesterov,
                     scale_c=self.scale_c, compute=self.compute, chunk_budget_bytes=self.chunk_budget_bytes,

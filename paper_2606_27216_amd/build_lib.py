@@ -39,6 +39,7 @@ SOURCES = [
     ("himuon_api.cpp", []),
     ("ns_gemm_path.cpp", []),
     ("himuon_step.cpp", []),
+    ("himuon_plan.cpp", []),
 ]
 # The whole-matrix and large-tile path runs its Newton-Schulz GEMMs on hipBLASLt.
 LINK_LIBS = ["-lhipblaslt"]

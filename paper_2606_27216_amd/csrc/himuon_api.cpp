@@ -170,8 +170,21 @@ std::mutex g_staging_mu;
 StagingSlot g_slots[kSlots];
 unsigned g_next_slot = 0;
 
+thread_local PlanRecording* g_recording = nullptr;
+
 int upload_table(const void* data, size_t bytes, void* workspace, hipStream_t stream, int dev)
 {
+    if (g_recording) {
+        // A plan being recorded: the table goes into a pinned buffer that the
+        // plan owns, so the captured copy reads the same bytes at every replay.
+        void* host = nullptr;
+        hipError_t e = hipHostMalloc(&host, bytes, hipHostMallocDefault);
+        if (e != hipSuccess) return set_hip_error(e);
+        g_recording->host_buffers.push_back(host);
+        memcpy(host, data, bytes);
+        e = hipMemcpyAsync(workspace, host, bytes, hipMemcpyHostToDevice, stream);
+        return e == hipSuccess ? HIMUON_OK : set_hip_error(e);
+    }
     std::lock_guard<std::mutex> lock(g_staging_mu);
     StagingSlot& sl = g_slots[g_next_slot++ % kSlots];
     hipError_t e;

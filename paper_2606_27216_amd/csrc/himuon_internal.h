@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 namespace himuon {
 
 // One entry per matrix in a call; the table lives in the caller's workspace.
@@ -122,8 +124,20 @@ extern thread_local int g_last_hip_error;
 int set_hip_error(hipError_t e);
 // Copies `bytes` of host data to device memory `dst` on `stream` through a
 // ring of pinned staging slots (asynchronous; a slot is reused once its
-// copy has completed). Returns a himuon status.
+// copy has completed). Returns a himuon status. While a plan is recorded on
+// the calling thread (g_recording), each table gets a pinned buffer of the
+// plan's own instead, which the recorded copy reads at every replay.
 int upload_table(const void* data, size_t bytes, void* dst, hipStream_t stream, int dev);
+
+// The host side of a plan being recorded (himuon_plan.cpp).
+struct PlanRecording {
+    std::vector<void*> host_buffers;  // pinned, freed with the plan
+};
+extern thread_local PlanRecording* g_recording;
+
+// Creates the GEMM library's handle on device `dev` if it does not exist yet
+// (plans create it before recording). Returns a himuon status.
+int gemm_handle_ready(int dev);
 // Largest |p^k(s)| over s in [0, 1], k < K, p(s) = a s + b s^3 + c s^5.
 double iterate_bound(int K, double a, double b, double c);
 

@@ -319,6 +319,17 @@ int tune_gemm(hipblasLtHandle_t h, Gemm& g, float alpha, const void* A, const vo
 
 namespace himuon {
 
+int gemm_handle_ready(int dev)
+{
+    std::lock_guard<std::mutex> lock(g_lt_mu);
+    if (dev < 0 || dev >= kMaxDevices) return set_hip_error(hipErrorInvalidDevice);
+    if (!g_lt[dev] && hipblasLtCreate(&g_lt[dev]) != HIPBLAS_STATUS_SUCCESS) {
+        g_lt[dev] = nullptr;
+        return set_hip_error(hipErrorInitializationError);
+    }
+    return HIMUON_OK;
+}
+
 int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs, void* const* mom_ptrs,
                   const float* tau, const int64_t* rows, const int64_t* cols, const int64_t* ld_in,
                   const int64_t* ld_out, int Th, int Tw, int K, float a, float b, float c, int dtype, int compute,

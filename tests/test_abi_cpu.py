@@ -121,6 +121,11 @@ def test_noalloc_validation_rejects_before_any_hip_call():
                                          "rows": [64] * n, "cols": [64] * n}) == hm.ERR_WORKSPACE
 
 
+def test_plan_null_handles():
+    assert hm.himuon_plan_launch(None, None) == hm.ERR_INVALID_ARG
+    hm.himuon_plan_destroy(None)  # a no-op
+
+
 def test_null_arrays_rejected():
     L = hm.lib()
     assert L.himuon_ns_tiled(1, None, None, None, None, None, None, 32, 5, 1.0, 0.0, 0.0, 1, 0,

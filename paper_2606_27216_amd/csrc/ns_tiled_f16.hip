@@ -45,18 +45,25 @@ using namespace dev;
 // issued before the current tile is written back.
 
 // Sum over the 64 lanes in a fixed order: butterflies inside each 16-lane
-// row (quad swaps, half-row and row mirrors), then the four row sums.
+// row (quad swaps, half-row and row mirrors) leave every lane of a row with
+// the row's sum; row broadcasts then add row 0 into row 1 and row 2 into row
+// 3, and lane 31 into rows 2 and 3, so lane 63 holds (r2 + r3) + (r0 + r1).
+// (DPP reads from lanes that exist only; rows a broadcast does not write get
+// 0, the identity of the sum, so each step folds into one DPP add.)
+template <int CTRL, int ROW_MASK> HM_DEV float dpp_add(float v)
+{
+    return v + __uint_as_float((uint32_t)__builtin_amdgcn_update_dpp(0, (int)__float_as_uint(v), CTRL, ROW_MASK, 0xF, false));
+}
+
 HM_DEV float wave_sum_f32(float v)
 {
-    v += __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(v), 0xB1, 0xF, 0xF, false));
-    v += __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(v), 0x4E, 0xF, 0xF, false));
-    v += __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(v), 0x141, 0xF, 0xF, false));
-    v += __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(v), 0x140, 0xF, 0xF, false));
-    const float r0 = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 0));
-    const float r1 = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 16));
-    const float r2 = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 32));
-    const float r3 = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 48));
-    return (r0 + r1) + (r2 + r3);
+    v = dpp_add<0xB1, 0xF>(v);  // quad_perm [1, 0, 3, 2]
+    v = dpp_add<0x4E, 0xF>(v);  // quad_perm [2, 3, 0, 1]
+    v = dpp_add<0x141, 0xF>(v);  // row_half_mirror
+    v = dpp_add<0x140, 0xF>(v);  // row_mirror
+    v = dpp_add<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+    v = dpp_add<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+    return __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), 63));
 }
 
 HM_DEV uint32_t wave_max_u32(uint32_t v)
@@ -188,6 +195,15 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     int rp_off[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) rp_off[g] = li * RS + 8 * ((2 * g + lh) ^ rm_swz(li));
+    // The staged input and the packed output use the swizzle with its lowest
+    // bit cleared (chunk c at c ^ (rm_swz(r) & 6)), in which the two 8-byte
+    // halves of every aligned 16-byte pair keep their order: whole 16-byte
+    // row chunks then move between HBM and LDS with no exchange in
+    // registers, at the price of two-way bank conflicts on the four
+    // row-piece accesses of each end of a tile.
+    int io_rp[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) io_rp[g] = li * RS + 8 * ((2 * g + lh) ^ (rm_swz(li) & 6));
     // Transposing reads: supplier lane 4q' + m of 16-lane group G addresses
     // row 16s + 4(G/2) + m (+ 8x) and logical chunk 4(G%2) + q' of a block
     // segment, for the k half s of the block.
@@ -324,14 +340,10 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         load_rows(L, L.in, L.ld_in, L.vin, raw);
         if constexpr (OPT) load_rows(L, L.mom, L.ld_in, L.vin, rawm);
     };
-    // byte offset of the 16-byte chunk io_cc of tile row `row` in the row-major
-    // copy: its two 8-byte halves sit in one aligned 16-byte pair, swapped
-    // when rm_swz(row) is odd (io_swap exchanges them in registers)
+    // byte offset of the 16-byte chunk io_cc of tile row `row` in the staging
+    // layout of the row-major copy (io_rp)
     auto io_lds = [&](int row) -> int {
         return row * RS + 64 * (io_cc >> 2) + 16 * ((io_cc & 3) ^ (rm_swz(row) >> 1));
-    };
-    auto io_swap = [&](const u32x4& v, int row) -> u32x4 {
-        return (rm_swz(row) & 1) ? u32x4{v[2], v[3], v[0], v[1]} : v;
     };
     // The symmetric 128-tile step keeps its Z copy in a layout of aligned
     // 16-byte operand pairs (described at ns_steps_sym); its tiles are
@@ -469,7 +481,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                 *reinterpret_cast<u32x2*>(rm + io_half(row, 0)) = u32x2{raw[i][0], raw[i][1]};
                 *reinterpret_cast<u32x2*>(rm + io_half(row, 1)) = u32x2{raw[i][2], raw[i][3]};
             } else {
-                *reinterpret_cast<u32x4*>(rm + io_lds(row)) = io_swap(raw[i], row);
+                *reinterpret_cast<u32x4*>(rm + io_lds(row)) = raw[i];
             }
         }
         if (pending) store_rows(prv, outv);
@@ -490,7 +502,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                             for (int x = 0; x < 4; ++x) W[rb][q][2 * g + x] = w[x];
                         }
                     } else {
-                        const u32x2 w = *reinterpret_cast<const u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q);
+                        const u32x2 w = *reinterpret_cast<const u32x2*>(rm + 32 * (p0 + rb) * RS + io_rp[g] + 64 * q);
                         W[rb][q][2 * g] = w[0];
                         W[rb][q][2 * g + 1] = w[1];
                     }
@@ -533,7 +545,15 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                         }
                 ss = tile_sumsq(W, 3 * parity + 2);
             }
-            sc = args.zscale / sqrtf(ss);
+            // ss = m 4^e with m in [1, 4): sc = |c|^(1/4) rsq(m) 2^-e. The
+            // tile's scale reaches sc only through the exact factor 2^-e, which
+            // keeps Phi(2^e S) = Phi(S) bit for bit; the hardware reciprocal
+            // square root (about one ulp) is far inside the fp16 rounding of
+            // the iterate.
+            const uint32_t sb = __float_as_uint(ss);
+            const int e = ((int)(sb >> 23) - 127) >> 1;
+            const float m = __uint_as_float(sb - ((uint32_t)(2 * e) << 23));
+            sc = ldexpf(args.zscale * __builtin_amdgcn_rsqf(m), -e);
         }
         parity ^= 1;
         f32x16 Z[RB][NB];
@@ -1392,7 +1412,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                             *reinterpret_cast<u32x4*>(rm + 32 * (p0 + rb) * RS + 64 * q + rpB[g / 2]) =
                                 u32x4{OB[rb][q][2 * g], OB[rb][q][2 * g + 1], OB[rb][q][2 * g + 2], OB[rb][q][2 * g + 3]};
                     } else {
-                        *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + rp_off[g] + 64 * q) =
+                        *reinterpret_cast<u32x2*>(rm + 32 * (p0 + rb) * RS + io_rp[g] + 64 * q) =
                             u32x2{OB[rb][q][2 * g], OB[rb][q][2 * g + 1]};
                     }
                 }
@@ -1404,15 +1424,16 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                 const u32x2 hi = *reinterpret_cast<const u32x2*>(rm + io_half(row, 1));
                 outv[i] = u32x4{lo[0], lo[1], hi[0], hi[1]};
             } else {
-                outv[i] = io_swap(*reinterpret_cast<const u32x4*>(rm + io_lds(row)), row);
+                outv[i] = *reinterpret_cast<const u32x4*>(rm + io_lds(row));
             }
         }
         prv = cur;
         pending = true;
         // (raw is defined on both paths, so the values staged at the top of
-        // this round are dead across its steps)
+        // this round are dead across its steps; the hint keeps the zeroing,
+        // once per wave, off the path of every other round)
         if constexpr (!EARLY) {
-            if (has_next) {
+            if (__builtin_expect(has_next, 1)) {
                 issue_loads(nxt);
             } else {
 #pragma unroll

@@ -363,11 +363,15 @@ KernelArgs make_kernel_args(const MatDesc* descs, int64_t n_mats, int K, float a
         ka.unscale = (float)(1.0 / pow(ac, 0.25));
         ka.sigma = c > 0.f ? 1.f : -1.f;
         ka.bq = (float)((double)ka.sigma * (double)b / sqrt(ac));
+        ka.hshift = (float)(0.5 * (double)ka.sigma * (double)b / sqrt(ac));
+        ka.am = (float)((double)a - (double)b * (double)b / (4.0 * (double)c));
     } else {
         ka.zscale = 1.f;
         ka.unscale = 1.f;
         ka.sigma = 0.f;
         ka.bq = b;
+        ka.hshift = 0.f;
+        ka.am = a;
     }
     return ka;
 }

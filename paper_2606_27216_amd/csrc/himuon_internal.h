@@ -64,6 +64,11 @@ struct KernelArgs {
     float unscale;   // 1 / zscale
     float bq;        // sigma * b' (c != 0) or b (c == 0)
     float sigma;     // sign(c), 0 when c == 0
+    // The same step with the square completed (c != 0): with the shifted
+    // Gram matrix M = H + (sigma b' / 2) I, a I + P = sigma M^2 + a' I and
+    // a' = a - b^2 / (4c).
+    float hshift;    // sigma b' / 2 (0 when c == 0)
+    float am;        // a' (a when c == 0)
 };
 
 // Enqueue one chunk on `stream`. Returns hipErrorInvalidValue for a

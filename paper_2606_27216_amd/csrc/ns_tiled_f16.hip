@@ -21,14 +21,17 @@ using namespace dev;
 // Same tile map, restructured so that no vector-ALU work but the fp16
 // conversions is left in the K loop. The state is Z = X |c|^(1/4) (exact
 // rescaling of the iterate), for which one step of eq. (ns_iteration) reads
-//     Z <- (a I + P) Z,   P = sigma H (H + sigma b' I),   H = Z Z^T,
-// with b' = b / sqrt|c| and sigma = sign(c): the c-coefficient becomes +-1,
-// b' moves onto the diagonal of an MFMA operand, and a I seeds the diagonal
-// blocks of the P accumulator, so a step is three MFMA products. Between
-// steps the iterate is held as fp16 operands only (near convergence a I + P
-// has eigenvalues of order one, so rounding its product does not amplify).
-// The normalisation multiplies by |c|^(1/4) and the store by |c|^(-1/4).
-// c = 0 takes a I + b H.
+//     Z <- (a I + sigma H^2 + b' H) Z,   H = Z Z^T,
+// with b' = b / sqrt|c| and sigma = sign(c): the c-coefficient becomes +-1.
+// Completing the square, with M = H + (sigma b' / 2) I,
+//     a I + sigma H^2 + b' H = sigma M^2 + a' I,   a' = a - b^2 / (4c),
+// so the Gram product, seeded with the shift on its diagonal blocks, yields M
+// directly, the polynomial is the single product M M seeded with sigma a' I,
+// and a step is three MFMA products with nothing between them but the fp16
+// conversions of their results. Between steps the iterate is held as fp16
+// operands only (near convergence a I + P has eigenvalues of order one, so
+// rounding its product does not amplify). The normalisation multiplies by
+// |c|^(1/4) and the store by |c|^(-1/4). c = 0 takes a I + b H.
 //
 // Z is shared through one row-major fp16 copy of the tile (see kRowStride).
 // Gram operands of the other waves' rows are read from it as row pieces; the
@@ -86,16 +89,6 @@ HM_DEV u32x2 load_bf16x4(const void* base, int64_t gr, int64_t gc, int64_t ld, i
             if (gc + e < cols) h[e] = p[e];
     }
     return u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
-}
-
-// Two packed fp16 additions (v_pk_add_f16), written out: for f16x2 adds on
-// the four words of a u32x4 operand slot the compiler emitted four
-// v_pk_add_f16 that all read the slot's first word.
-HM_DEV uint32_t pk_add_f16(uint32_t a, uint32_t b)
-{
-    uint32_t r;
-    asm("v_pk_add_f16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
 }
 
 HM_DEV u32x2 tr_read(const uint8_t* ptr)
@@ -220,21 +213,18 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
     // A diagonal block holds row li's column 8g + 4lh + e in register 4g + e,
     // so the diagonal entry of this lane (if any) is register vdiag.
     const int vdiag = (lh == ((li >> 2) & 1)) ? 4 * (li >> 3) + (li & 3) : -1;
-    // sigma b' in the packed fp16 operand word of that diagonal entry (word x of
-    // slot s holds registers 8s + 2x and 8s + 2x + 1), zero elsewhere
-    uint32_t dq[2][4];
+    // Diagonal blocks that seed accumulators: sigma a' I for the polynomial
+    // product (sigma a I for c = 0), and the shift (sigma b' / 2) I that turns
+    // a diagonal Gram block into the same block of M (zero for c = 0).
+    f32x16 diag_a = {}, diag_m = {};
     {
-        const uint32_t bq16 = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)args.bq);
+        const float sa = CMODE == 2 ? args.a : args.am;
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-            for (int x = 0; x < 4; ++x)
-                dq[s][x] = (vdiag >= 0 && (vdiag >> 3) == s && ((vdiag & 7) >> 1) == x) ? (bq16 << (16 * (vdiag & 1))) : 0u;
+        for (int v = 0; v < 16; ++v) {
+            diag_a[v] = v == vdiag ? (CMODE == 1 ? -sa : sa) : 0.f;
+            diag_m[v] = (CMODE != 2 && v == vdiag) ? args.hshift : 0.f;
+        }
     }
-    // sigma a I as a diagonal block (the seed of the aI + P accumulators)
-    f32x16 diag_a = {};
-#pragma unroll
-    for (int v = 0; v < 16; ++v) diag_a[v] = v == vdiag ? (CMODE == 1 ? -args.a : args.a) : 0.f;
     // the row blocks owned by the other waves, in rotated order: H slots and
     // the rows of the row-major copy
     u32x4* sl_row[NOA];
@@ -574,7 +564,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                 }
 
         // The K steps of a 128-tile split over two waves, using the symmetry
-        // of H = Z Z^T and of aI + P (a polynomial in H): of the 16 blocks
+        // of M and of aI + P (polynomials in H = Z Z^T): of the 16 blocks
         // of each, only the ten on and above the block diagonal are
         // computed, five per wave. Wave w owns row blocks r0 = 2w, r1 = r0+1
         // and computes blocks (r0,r0), (r0,r1), (r1,r1), (r0,o_w) and
@@ -583,8 +573,8 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         // so each upper block is computed exactly once. Blocks are stored in
         // LDS as 32x32 fp16 arrays (64-byte rows, the Z copy's chunk
         // swizzle); a block needed in the other orientation is read with
-        // ds_read_b64_tr_b16. Diagonal H blocks are stored with the shift
-        // sigma b' I, the form in which the other wave uses them. Per step:
+        // ds_read_b64_tr_b16. The Gram blocks are those of M (the diagonal
+        // ones carry the shift from the seed of their accumulators). Per step:
         //   Gram (r0,r0), part of (r0,r1), with the conversion of Z into
         //   operands | barrier | own Z rows to LDS + rest of the own Gram
         //   blocks | barrier | Gram cross blocks (+ own H conversions and
@@ -655,9 +645,9 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                 // of the Z copy (no wave reads the copy after the previous
                 // step's last barrier, see below).
                 u32x4 Zop[RB][NB][S];
-                f32x16 g[5];
+                f32x16 g[5];  // the diagonal blocks (r0, r0), (r1, r1) of M from the shift
 #pragma unroll
-                for (int e = 0; e < 5; ++e) g[e] = f32x16{};
+                for (int e = 0; e < 5; ++e) g[e] = (e == 0 || e == 2) ? diag_m : f32x16{};
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -693,7 +683,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
                     for (int s = 0; s < S; ++s) g[2] = mma1<OP>(Zop[1][q][s], Zop[1][q][s], g[2]);
                 __builtin_amdgcn_sched_barrier(0);
-                u32x4 hs[5][S], qs[2][S], la1[S];  // la1: H[r1, r0]
+                u32x4 hs[5][S], la1[S];  // hs[0], hs[2]: diagonal blocks of M; la1: H[r1, r0]
 #pragma unroll
                 for (int it = 0; it < IT; ++it) {
                     const int q = it / S, s = it % S;
@@ -710,27 +700,17 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
                             for (int x = 0; x < S; ++x) hs[0][x] = make_slot<OP>(g[0], x);
                         } else if (it == 1) {
-                            // H + sigma b' I: one packed fp16 add on the operand
-                            // word that holds this lane's diagonal entry
-#pragma unroll
-                            for (int x = 0; x < S; ++x)
-#pragma unroll
-                                for (int y = 0; y < 4; ++y) qs[0][x][y] = pk_add_f16(hs[0][x][y], dq[x][y]);
+                            blk_put(hblk(w, 0), hs[0]);
                         } else if (it == 2) {
 #pragma unroll
                             for (int x = 0; x < S; ++x) hs[1][x] = make_slot<OP>(g[1], x);
-                            blk_put(hblk(w, 0), qs[0]);
                         } else if (it == 3) {
                             blk_put(hblk(w, 1), hs[1]);
 #pragma unroll
                             for (int x = 0; x < S; ++x) hs[2][x] = make_slot<OP>(g[2], x);
                         } else if (it == 4) {
-#pragma unroll
-                            for (int x = 0; x < S; ++x)
-#pragma unroll
-                                for (int y = 0; y < 4; ++y) qs[1][x][y] = pk_add_f16(hs[2][x][y], dq[x][y]);
+                            blk_put(hblk(w, 2), hs[2]);
                         } else if (it == 5) {
-                            blk_put(hblk(w, 2), qs[1]);
 #pragma unroll
                             for (int x = 0; x < S; ++x) la1[x] = blk_tr(hblk(w, 1), x);
                         }
@@ -748,10 +728,10 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     }
                 };
                 if constexpr (CMODE != 2) {
-                    // ---- P (as acc = H (H + sigma b' I) + sigma a I): block (i, j)
-                    // accumulates H'[j, k] x H[i, k] over the k-blocks. Terms on
-                    // this wave's blocks first; the cross blocks' conversions and
-                    // stores ride along.
+                    // ---- P (as acc = M M + sigma a' I): block (i, j) accumulates
+                    // M[j, k] x M[i, k] over the k-blocks (M and H share their
+                    // off-diagonal blocks). Terms on this wave's blocks first;
+                    // the cross blocks' conversions and stores ride along.
                     pa[0] = diag_a;
                     pa[1] = f32x16{};
                     pa[2] = diag_a;
@@ -760,9 +740,9 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                     u32x4 lb1[S], lb6[S];  // H[o_t, r0], H[o_{1-t}, r1]
 #pragma unroll
                     for (int s = 0; s < S; ++s) {
-                        pa[0] = mma1<OP>(qs[0][s], hs[0][s], pa[0]);  // k = r0
-                        pa[1] = mma1<OP>(qs[1][s], hs[1][s], pa[1]);  // k = r1
-                        pa[2] = mma1<OP>(qs[1][s], hs[2][s], pa[2]);  // k = r1
+                        pa[0] = mma1<OP>(hs[0][s], hs[0][s], pa[0]);  // k = r0
+                        pa[1] = mma1<OP>(hs[2][s], hs[1][s], pa[1]);  // k = r1
+                        pa[2] = mma1<OP>(hs[2][s], hs[2][s], pa[2]);  // k = r1
                         pa[0] = mma1<OP>(hs[1][s], hs[1][s], pa[0]);  // k = r1
                         pa[1] = mma1<OP>(la1[s], hs[0][s], pa[1]);    // k = r0
                         pa[2] = mma1<OP>(la1[s], la1[s], pa[2]);      // k = r0
@@ -800,11 +780,11 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
                     for (int s = 0; s < S; ++s) {
                         lb2[s] = blk_rows(hblk(wo, 3 + w), s);      // H[o_t, r1]
-                        lb3[s] = blk_rows(hblk(wo, 2 * w), s);      // H'[o_t, o_t]
+                        lb3[s] = blk_rows(hblk(wo, 2 * w), s);      // M[o_t, o_t]
                         lb4[s] = blk_rows(hblk(wo, w ? 5 : 1), s);  // H[o_t, o_{1-t}]
                         lb7[s] = blk_rows(hblk(wo, w ? 1 : 5), s);  // H[o_{1-t}, o_t]
                         lb5[s] = blk_rows(hblk(wo, 4 - w), s);      // H[o_{1-t}, r0]
-                        lb8[s] = blk_rows(hblk(wo, 2 - 2 * w), s);  // H'[o_{1-t}, o_{1-t}]
+                        lb8[s] = blk_rows(hblk(wo, 2 - 2 * w), s);  // M[o_{1-t}, o_{1-t}]
                     }
                     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -950,8 +930,8 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         // The K steps of a 256-tile (one tile per CU, four waves of two row
         // blocks each). Its fp16 copy fills the LDS, so H is never exchanged:
         // each step is evaluated in the equivalent chain form
-        //     Y = sigma (H + sigma b' I) Z,   Z <- a Z + H Y,
-        // with H's own rows kept in registers. Column block N of Y depends
+        //     Y = sigma M Z,   Z <- a' Z + M Y,
+        // with M's own rows kept in registers. Column block N of Y depends
         // only on column block N of Z, so Y replaces Z in the row-major copy
         // one column half at a time:
         //   Z own rows to LDS | barrier | Gram | Y, first half | barrier |
@@ -1021,16 +1001,17 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                 put_rows(Zop, 0, NB);
                 __syncthreads();
 
-                // ---- H = Z Z^T by groups of NG rotated column blocks;
-                // G[rb][jj] is block (p0 + rb, (p0 + NG gq + jj) mod NB)
-                u32x4 Hop[RB][NB][S], Q0[RB][S];
+                // ---- M = Z Z^T + (sigma b' / 2) I by groups of NG rotated column
+                // blocks (b H for c = 0); G[rb][jj] is block (p0 + rb, (p0 + NG gq
+                // + jj) mod NB), diagonal for NG gq + jj = rb
+                u32x4 Hop[RB][NB][S];
 #pragma unroll
                 for (int gq = 0; gq < NGR; ++gq) {
                     f32x16 G[RB][NG];
 #pragma unroll
                     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-                        for (int jj = 0; jj < NG; ++jj) G[rb][jj] = f32x16{};
+                        for (int jj = 0; jj < NG; ++jj) G[rb][jj] = NG * gq + jj == rb ? diag_m : f32x16{};
                     auto opa = [&](int j, int q, int s) -> u32x4 {
                         return j < RB ? Zop[j < RB ? j : 0][q][s] : rowpiece(rm_row[j < RB ? 0 : j - RB], q, s);
                     };
@@ -1062,19 +1043,13 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                             const f32x16 gj = CMODE == 2 ? G[rb][jj] * args.bq : G[rb][jj];
 #pragma unroll
                             for (int s = 0; s < S; ++s) Hop[rb][j][s] = make_slot<OP>(gj, s);
-                            if (CMODE != 2 && j == rb) {
-                                f32x16 gd = G[rb][jj];
-#pragma unroll
-                                for (int v = 0; v < 16; ++v) gd[v] += v == vdiag ? args.bq : 0.f;
-#pragma unroll
-                                for (int s = 0; s < S; ++s) Q0[rb][s] = make_slot<OP>(gd, s);
-                            }
                         }
                 }
                 auto hb = [&](int rb, int jk, int s) -> u32x4 { return Hop[rb][jk][s]; };
-                auto hqb = [&](int rb, int jk, int s) -> u32x4 { return jk == rb ? Q0[rb][s] : Hop[rb][jk][s]; };
-                // a Z (fp16 state, exact products) as the seed of the last product
+                // a' Z (a Z for c = 0; fp16 state, exact products) as the seed of
+                // the last product
                 auto seed = [&](f32x16 (&acc)[RB][NG], int n0) {
+                    const float sa = CMODE == 2 ? args.a : args.am;
 #pragma unroll
                     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -1087,8 +1062,8 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                                     // would read the vector's first element)
                                     const uint32_t wv = Zop[rb][n0 + n][s][w];
                                     const f16x2 pr = __builtin_bit_cast(f16x2, wv);
-                                    acc[rb][n][8 * s + 2 * w] = args.a * (float)pr[0];
-                                    acc[rb][n][8 * s + 2 * w + 1] = args.a * (float)pr[1];
+                                    acc[rb][n][8 * s + 2 * w] = sa * (float)pr[0];
+                                    acc[rb][n][8 * s + 2 * w + 1] = sa * (float)pr[1];
                                 }
                 };
                 // a finished group of Z becomes next step's operands (after the
@@ -1122,7 +1097,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                             for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
                                 for (int n = 0; n < NG; ++n) acc[rb][n] = f32x16{};
-                            col_product(acc, NG * gq, hqb);
+                            col_product(acc, NG * gq, hb);
 #pragma unroll
                             for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -1202,7 +1177,8 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                             u32x2{Zop[rb][N][g >> 1][(g & 1) * 2], Zop[rb][N][g >> 1][(g & 1) * 2 + 1]};
             if constexpr (SHARED) __syncthreads();
 
-            // H = Z Z^T; G[rb][j] is the row piece of block (p0 + rb, (p0 + j) mod NB).
+            // M = Z Z^T + (sigma b' / 2) I (H itself for c = 0): G[rb][j] is the
+            // row piece of block (p0 + rb, (p0 + j) mod NB), diagonal for j = rb.
             // Iteration it = (q, s) reads the other waves' row pieces (q, s) from
             // the row-major copy; those of iteration it + 1 are requested before
             // its MFMAs issue.
@@ -1210,7 +1186,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-                for (int j = 0; j < NB; ++j) G[rb][j] = f32x16{};
+                for (int j = 0; j < NB; ++j) G[rb][j] = j == rb ? diag_m : f32x16{};
             {
                 u32x4 nxt_op[NOA];
                 if constexpr (NO > 0) {
@@ -1245,30 +1221,22 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 
             u32x4 Pop[RB][NB][S];  // own rows of P (rotated k-blocks), fp16
             if constexpr (CMODE != 2) {
-                u32x4 Hop[RB][NB][S], Q0[RB][S];
+                u32x4 Hop[RB][NB][S];
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb) {
+                for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
                     for (int j = 0; j < NB; ++j)
 #pragma unroll
                         for (int s = 0; s < S; ++s)
                             if (!(SYM64 && rb == 1 && j == 0)) Hop[rb][j][s] = make_slot<OP>(G[rb][j], s);
-                    // H + sigma b' I on the diagonal block (p0 + rb, p0 + rb): the
-                    // shift is added to the fp16 operand word that holds this
-                    // lane's diagonal entry (one packed add per word)
-#pragma unroll
-                    for (int s = 0; s < S; ++s)
-#pragma unroll
-                        for (int x = 0; x < 4; ++x) Q0[rb][s][x] = pk_add_f16(Hop[rb][rb][s][x], dq[s][x]);
-                }
                 if constexpr (SYM64) {
-                    // H(1, 0) = H(0, 1)^T
+                    // M(1, 0) = M(0, 1)^T
                     sym_put(sblk, Hop[0][1]);
 #pragma unroll
                     for (int s = 0; s < S; ++s) Hop[1][0][s] = sym_tr(sblk, s);
                 }
                 if constexpr (SHARED) {
-                    // the H slots were last read before the previous step's final barrier
+                    // the M slots were last read before the previous step's final barrier
 #pragma unroll
                     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -1278,10 +1246,10 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                                 slots[(((p0 + rb) * NB + (p0 + j) % NB) * S + s) * 64 + lane] = Hop[rb][j][s];
                     __syncthreads();
                 }
-                // acc = H (H + sigma b' I) + sigma a I, so that sigma acc = a I + P:
-                // acc[rb][j] is block (p0 + rb, (p0 + j) mod NB), the diagonal
-                // blocks (j = rb) start from sigma a I; iteration it = (jk, s)
-                // runs over the rotated k-blocks (p0 + jk) mod NB.
+                // acc = M M + sigma a' I, so that sigma acc = a I + P: acc[rb][j]
+                // is block (p0 + rb, (p0 + j) mod NB), the diagonal blocks (j = rb)
+                // start from sigma a' I; iteration it = (jk, s) runs over the
+                // rotated k-blocks (p0 + jk) mod NB.
                 f32x16 acc[RB][NB];
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
@@ -1315,8 +1283,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
 #pragma unroll
                         for (int rb = 0; rb < RB; ++rb) {
                             if (SYM64 && rb == 1 && j == 0) continue;  // aI + P is symmetric too
-                            const u32x4 opb = jk == rb ? Q0[rb][s] : Hop[rb][jk][s];
-                            acc[rb][j] = mma1<OP>(opa, opb, acc[rb][j]);
+                            acc[rb][j] = mma1<OP>(opa, Hop[rb][jk][s], acc[rb][j]);
                         }
                     }
                     __builtin_amdgcn_sched_barrier(0);

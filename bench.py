@@ -1,6 +1,6 @@
 """Throughput of the tiled Newton–Schulz map on one MI355X.
 
-    python bench.py [--steps 20] [--warmup 5] [--T 128] [--K 5] [--workload stack7b]
+    python bench.py [--steps 60] [--warmup 10] [--T 128] [--K 5] [--workload stack7b]
 
 One step is one ``himuon_ns_tiled`` call over the whole workload (every tile
 of every matrix: gather, normalise, K Newton–Schulz steps, write back), with
@@ -24,7 +24,15 @@ The JSON also carries:
   cpu_baseline  the fp64 oracle timed on the host cores (and on one core) on a
                 bounded random sample of the same workload's tiles (read back
                 from the GPU), with the CPU model; its `parity` field compares
-                those oracle tiles with the GPU's outputs of the last timed step.
+                those oracle tiles with the GPU's outputs of the last timed step;
+  power         socket power and graphics clock sampled from the driver's sysfs
+                files during the timed region (null where they cannot be read):
+                the fused kernels run at the board's power cap, below the clock
+                on which the published peak is quoted.
+
+`--calib-gemm N` times the GEMM library's N x N x N fp16 product instead (the
+same power and clock fields), as a reference for what dense MFMA work
+sustains under the same power cap.
 """
 from __future__ import annotations
 
@@ -34,6 +42,7 @@ import json
 import os
 import re
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -49,6 +58,101 @@ METRIC = "tiled-NS TFLOP/s (6·H·W·T·K) + % bf16 MFMA peak, 7B layer stack T=
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class PowerSampler:
+    """Samples the GPU's socket power (hwmon power1_input, microwatts) and
+    current graphics clock (the marked line of pp_dpm_sclk) every `period`
+    seconds in a thread, while used as a context manager. Only a machine with
+    exactly one GPU card in sysfs is sampled (no mapping from device to card
+    is needed then); elsewhere summary() is None."""
+
+    def __init__(self, period: float = 0.05):
+        import glob
+        self.period = period
+        self.power_w, self.mhz = [], []
+        self._stop = threading.Event()
+        self._thread = None
+        self.power_file = self.sclk_file = None
+        cards = [d for d in sorted(glob.glob("/sys/class/drm/card*/device"))
+                 if glob.glob(os.path.join(d, "hwmon", "hwmon*", "power1_input"))]
+        if len(cards) == 1:
+            self.power_file = glob.glob(os.path.join(cards[0], "hwmon", "hwmon*", "power1_input"))[0]
+            sclk = os.path.join(cards[0], "pp_dpm_sclk")
+            self.sclk_file = sclk if os.path.exists(sclk) else None
+
+    def _read(self):
+        try:
+            with open(self.power_file) as f:
+                self.power_w.append(int(f.read().strip()) / 1e6)
+        except (OSError, ValueError):
+            pass
+        if self.sclk_file:
+            try:
+                with open(self.sclk_file) as f:
+                    for line in f:
+                        if "*" in line:
+                            m = re.search(r"(\d+)\s*[Mm]hz", line)
+                            if m:
+                                self.mhz.append(int(m.group(1)))
+            except OSError:
+                pass
+
+    def _run(self):
+        while not self._stop.wait(self.period):
+            self._read()
+
+    def __enter__(self):
+        if self.power_file:
+            self._thread = threading.Thread(target=self._run, daemon=True)
+            self._thread.start()
+        return self
+
+    def restart(self):
+        """Drops the samples taken so far (those of a warm-up)."""
+        self.power_w.clear()
+        self.mhz.clear()
+
+    def __exit__(self, *exc):
+        if self._thread:
+            self._stop.set()
+            self._thread.join()
+        return False
+
+    def summary(self):
+        if not self.power_w:
+            return None
+        import statistics
+        return {"socket_w_median": round(statistics.median(self.power_w), 1),
+                "gfx_mhz_median": statistics.median(self.mhz) if self.mhz else None,
+                "samples": len(self.power_w), "period_s": self.period,
+                "source": "sysfs hwmon power1_input, pp_dpm_sclk"}
+
+
+def bench_calib_gemm(args, torch, np, dev):
+    """The GEMM library's N x N x N fp16 product, timed like a bench step."""
+    n = args.calib_gemm
+    a = torch.randn(n, n, device=dev, dtype=torch.float16)
+    b = torch.randn(n, n, device=dev, dtype=torch.float16)
+    c = torch.empty(n, n, device=dev, dtype=torch.float16)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    with PowerSampler() as ps:
+        for _ in range(args.warmup):
+            torch.matmul(a, b, out=c)
+        torch.cuda.synchronize()
+        ps.restart()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            ev[i][0].record()
+            torch.matmul(a, b, out=c)
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    ms = np.array([x.elapsed_time(y) for x, y in ev])
+    rec = {"metric": "library GEMM fp16 TFLOP/s (2N^3)", "value": round(2.0 * n ** 3 / (wall / args.steps) / 1e12, 1),
+           "unit": "TFLOP/s", "n": n, "steps": args.steps, "warmup": args.warmup,
+           "median_ms": round(float(np.median(ms)), 4), "peak": PEAK_TFLOPS["f16"], "power": ps.summary()}
+    print(json.dumps(rec), flush=True)
 
 
 def kernel_source_hash() -> str:
@@ -435,8 +539,8 @@ def bench_layershapes(args, hm, torch, np, dev):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=60)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="stack7b", choices=["stack7b", "layer7b", "square4096", "hetero"])
     ap.add_argument("--T", type=int, default=128)
     ap.add_argument("--K", type=int, default=5)
@@ -463,6 +567,8 @@ def main():
                     help="--optstep variants to run (comma-separated names, or all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB per launch (counter calibration)")
+    ap.add_argument("--calib-gemm", type=int, default=0,
+                    help="only time the GEMM library's N x N x N fp16 product (power-cap reference)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -487,6 +593,8 @@ def main():
         log(f"copied {args.calib_copy_mib} MiB x {args.warmup + args.steps}")
         return
 
+    if args.calib_gemm:
+        return bench_calib_gemm(args, torch, np, dev)
     if args.optstep:
         return bench_optstep(args, hm, torch, np, dev)
     if args.layershapes:
@@ -527,22 +635,26 @@ def main():
         hm.ns_tiled(mats, outputs=outs, T=args.T, K=args.K, coeffs=coeffs, compute=compute,
                     chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    log(f"warmup {args.warmup} steps done")
-
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for i in range(args.steps):
-        ev[i][0].record(stream)
-        step()
-        ev[i][1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_start
+    with PowerSampler() as ps:
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        log(f"warmup {args.warmup} steps done")
+        ps.restart()
+        t_start = time.perf_counter()
+        for i in range(args.steps):
+            ev[i][0].record(stream)
+            step()
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t_start
     step_ms = np.array([a.elapsed_time(b) for a, b in ev])
     log(f"timed {args.steps} steps: wall {wall * 1e3:.2f} ms, event median {np.median(step_ms):.3f} ms/step")
+    power = ps.summary()
+    if power:
+        log(f"socket power {power['socket_w_median']} W, graphics clock {power['gfx_mhz_median']} MHz "
+            f"({power['samples']} samples)")
 
     ms_per_step = wall * 1e3 / args.steps
     value = flops_step / (wall / args.steps) / 1e12
@@ -584,6 +696,7 @@ def main():
         },
         "step_ms": {"median": round(float(np.median(step_ms)), 4),
                     "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4)},
+        "power": power,
     }
     if args.cpu_seconds > 0:
         log(f"cpu baseline: oracle on sampled tiles for ~{args.cpu_seconds:.0f} s")

@@ -491,7 +491,8 @@ def bench_layershapes(args, hm, torch, np, dev):
     shape, Phi_K (T = 0) and Phi_{K,512} through the library-GEMM path, K = 5,
     one call per matrix; the paired ratio t_full / t_tile is the median over
     `--steps` timed calls after `--warmup` (the paper: 30 after 3). The fused
-    T = 128 kernel is timed beside them."""
+    T = 128 kernel is timed beside them, and every call again as a recorded
+    plan (one HIP graph launch per call, field `graph`)."""
     import workloads
     coeffs = tuple(float(np.float32(v)) for v in hm.QUINTIC)
     stream = torch.cuda.current_stream(dev)
@@ -518,11 +519,23 @@ def bench_layershapes(args, hm, torch, np, dev):
             t_full = timed(lambda: hm.ns_gemm([x], outputs=[y], T=0, K=5, coeffs=coeffs, stream=stream))
             t_tile = timed(lambda: hm.ns_gemm([x], outputs=[y], T=512, K=5, coeffs=coeffs, stream=stream))
             t_128 = timed(lambda: hm.ns_tiled([x], outputs=[y], T=128, K=5, coeffs=coeffs, stream=stream))
+            # the same calls recorded once into HIP graphs (plans), one graph launch per call
+            plans = {"full": hm.plan_ns_gemm([x], [y], T=0, K=5, coeffs=coeffs),
+                     "512": hm.plan_ns_gemm([x], [y], T=512, K=5, coeffs=coeffs),
+                     "128": hm.plan_ns_tiled([x], [y], T=128, K=5, coeffs=coeffs)}
+            g = {k: timed(lambda p=p: p.launch(stream)) for k, p in plans.items()}
+            for p in plans.values():
+                p.close()
             res[name] = {"shape": [H, W], "full_ms": round(float(np.median(t_full)), 4),
                          "tiled512_ms": round(float(np.median(t_tile)), 4),
                          "speedup_512": round(float(np.median(t_full / t_tile)), 3),
                          "fused128_ms": round(float(np.median(t_128)), 4),
-                         "speedup_128": round(float(np.median(t_full / t_128)), 3)}
+                         "speedup_128": round(float(np.median(t_full / t_128)), 3),
+                         "graph": {"full_ms": round(float(np.median(g["full"])), 4),
+                                   "tiled512_ms": round(float(np.median(g["512"])), 4),
+                                   "fused128_ms": round(float(np.median(g["128"])), 4),
+                                   "speedup_512": round(float(np.median(g["full"] / g["512"])), 3),
+                                   "speedup_128": round(float(np.median(g["full"] / g["128"])), 3)}}
             log(f"{model} {name} {H}x{W}: {res[name]}")
         out[model] = res
     sp = [r["speedup_512"] for m in out.values() for r in m.values()]

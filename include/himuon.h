@@ -360,16 +360,19 @@ int himuon_step(int64_t n_mats,
                 void* stream);
 
 /*
- * Plans: a himuon_ns_tiled or himuon_step call recorded once, on the current
- * device, into a HIP graph and replayed by himuon_plan_launch, whose only
- * host work is one graph launch (no validation, planning or table staging
- * per call). This is the graph-captured cross-layer optimizer step of the
- * optimizer-step study (Sec. 6.4) and the graph-capture state that the
- * runtime tile-size reconfiguration rebuilds when T changes (Sec. 4.4.3).
+ * Plans: a himuon_ns_tiled, himuon_ns_gemm or himuon_step call recorded
+ * once, on the current device, into a HIP graph and replayed by
+ * himuon_plan_launch, whose only host work is one graph launch (no
+ * validation, planning or table staging per call, and one launch for the
+ * whole chain of kernels of a library-GEMM call). This is the graph-captured
+ * cross-layer optimizer step of the optimizer-step study (Sec. 6.4) and the
+ * graph-capture state that the runtime tile-size reconfiguration rebuilds
+ * when T changes (Sec. 4.4.3).
  *
- * himuon_plan_ns_tiled / himuon_plan_step take the arguments of
- * himuon_ns_tiled / himuon_step without the stream, validate them as those
- * do (returning the same errors, with *plan = NULL), and record the call:
+ * himuon_plan_ns_tiled / himuon_plan_ns_gemm / himuon_plan_step take the
+ * arguments of himuon_ns_tiled / himuon_ns_gemm / himuon_step without the
+ * stream, validate them as those do (returning the same errors, with
+ * *plan = NULL), and record the call:
  * every device pointer and every scalar is fixed in the plan. Each launch
  * then performs the recorded call again on the current contents of those
  * buffers, in `stream` order: it first copies the call's descriptor tables
@@ -396,6 +399,15 @@ int himuon_plan_ns_tiled(himuon_plan_t** plan, int64_t n_mats,
                          int dtype, int compute,
                          void* workspace, size_t workspace_bytes,
                          size_t chunk_budget_bytes);
+
+int himuon_plan_ns_gemm(himuon_plan_t** plan, int64_t n_mats,
+                        const void* const* in_ptrs, void* const* out_ptrs,
+                        const int64_t* rows, const int64_t* cols,
+                        const int64_t* ld_in, const int64_t* ld_out,
+                        int T, int K, float a, float b, float c,
+                        int dtype, int compute,
+                        void* workspace, size_t workspace_bytes,
+                        size_t chunk_budget_bytes);
 
 int himuon_plan_step(himuon_plan_t** plan, int64_t n_mats,
                      void* const* weights, const void* const* grads, void* const* moms,

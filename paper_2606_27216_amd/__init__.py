@@ -92,6 +92,9 @@ def lib():
         L.himuon_plan_ns_tiled.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int,
                                            f, f, f, ctypes.c_int, ctypes.c_int, vp, sz, sz]
         L.himuon_plan_ns_tiled.restype = ctypes.c_int
+        L.himuon_plan_ns_gemm.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int,
+                                          f, f, f, ctypes.c_int, ctypes.c_int, vp, sz, sz]
+        L.himuon_plan_ns_gemm.restype = ctypes.c_int
         L.himuon_plan_step.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, f, f, f,
                                        f, f, f, ctypes.c_int, f, ctypes.c_int, ctypes.c_int, vp, sz, sz]
         L.himuon_plan_step.restype = ctypes.c_int
@@ -282,6 +285,18 @@ def himuon_plan_ns_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T
     return st, (h.value if st == OK else None)
 
 
+def himuon_plan_ns_gemm(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c, dtype, compute,
+                        workspace, workspace_bytes, chunk_budget_bytes):
+    """Records a himuon_ns_gemm call into a plan. Returns (status, plan handle or None)."""
+    h = ctypes.c_void_p()
+    st = int(lib().himuon_plan_ns_gemm(
+        ctypes.byref(h), int(n_mats), _ptr_array(in_ptrs), _ptr_array(out_ptrs), _i64_array(rows), _i64_array(cols),
+        None if ld_in is None else _i64_array(ld_in), None if ld_out is None else _i64_array(ld_out),
+        int(T), int(K), float(a), float(b), float(c), int(dtype), int(compute),
+        int(workspace) if workspace else None, int(workspace_bytes), int(chunk_budget_bytes)))
+    return st, (h.value if st == OK else None)
+
+
 def himuon_plan_step(n_mats, weights, grads, moms, rows, cols, ld, T, K, a, b, c, lr, momentum, weight_decay,
                      nesterov, scale_c, dtype, compute, workspace, workspace_bytes, chunk_budget_bytes):
     """Records a himuon_step call into a plan. Returns (status, plan handle or None)."""
@@ -355,6 +370,33 @@ def plan_ns_tiled(inputs, outputs, T=128, K=5, coeffs=QUINTIC, compute=COMPUTE_D
             workspace.data_ptr(), workspace.numel() * workspace.element_size(), chunk_budget_bytes)
     if st != OK:
         raise HimuonError(st, "himuon_plan_ns_tiled")
+    return Plan(h, (inputs, outputs, workspace))
+
+
+def plan_ns_gemm(inputs, outputs, T=0, K=5, coeffs=QUINTIC, compute=COMPUTE_DEFAULT, chunk_budget_bytes=0,
+                 workspace=None):
+    """Records ``ns_gemm(inputs, outputs, ...)`` (square T x T tiles, or whole
+    matrices for T = 0) into a Plan on the inputs' device; every launch
+    recomputes the outputs from the inputs' current contents."""
+    import torch
+    inputs, outputs = list(inputs), list(outputs)
+    code = _dtype_code(inputs[0])
+    dev = inputs[0].device
+    a, b, c = coeffs
+    rows = [x.shape[0] for x in inputs]
+    cols = [x.shape[1] for x in inputs]
+    if workspace is None:
+        need = himuon_ns_gemm_workspace_size(rows, cols, T, code, compute, K, a, b, c, chunk_budget_bytes)
+        if need == 0:
+            raise HimuonError(ERR_INVALID_ARG, "himuon_ns_gemm_workspace_size")
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    with torch.cuda.device(dev):
+        st, h = himuon_plan_ns_gemm(
+            len(inputs), [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs], rows, cols,
+            [x.stride(0) for x in inputs], [y.stride(0) for y in outputs], T, K, a, b, c, code, compute,
+            workspace.data_ptr(), workspace.numel() * workspace.element_size(), chunk_budget_bytes)
+    if st != OK:
+        raise HimuonError(st, "himuon_plan_ns_gemm")
     return Plan(h, (inputs, outputs, workspace))
 
 

@@ -1,6 +1,6 @@
-// Plans: a himuon_ns_tiled call or a himuon_step call recorded once into a
-// HIP graph, replayed by himuon_plan_launch with no host work but one graph
-// launch. This is the graph-captured cross-layer step of the optimizer-step
+// Plans: a himuon_ns_tiled, himuon_ns_gemm or himuon_step call recorded once
+// into a HIP graph, replayed by himuon_plan_launch with no host work but one
+// graph launch. This is the graph-captured cross-layer step of the optimizer-step
 // study (Sec. 6.4) and the graph-capture state that the runtime tile-size
 // reconfiguration rebuilds when T changes (Sec. 4.4.3).
 //
@@ -84,6 +84,17 @@ int himuon_plan_ns_tiled(himuon_plan_t** plan, int64_t n_mats, const void* const
     return record(plan, [&](hipStream_t s) {
         return himuon_ns_tiled(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c, dtype, compute,
                                workspace, workspace_bytes, chunk_budget_bytes, s);
+    });
+}
+
+int himuon_plan_ns_gemm(himuon_plan_t** plan, int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
+                        const int64_t* rows, const int64_t* cols, const int64_t* ld_in, const int64_t* ld_out, int T,
+                        int K, float a, float b, float c, int dtype, int compute, void* workspace,
+                        size_t workspace_bytes, size_t chunk_budget_bytes)
+{
+    return record(plan, [&](hipStream_t s) {
+        return himuon_ns_gemm(n_mats, in_ptrs, out_ptrs, rows, cols, ld_in, ld_out, T, K, a, b, c, dtype, compute,
+                              workspace, workspace_bytes, chunk_budget_bytes, s);
     });
 }
 

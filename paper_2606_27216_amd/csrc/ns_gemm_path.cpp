@@ -184,7 +184,7 @@ int resolve_operand(int dtype, int compute, int K, float a, float b, float c, in
 std::mutex g_lt_mu;
 hipblasLtHandle_t g_lt[kMaxDevices] = {};
 
-constexpr int kCandidates = 8;  // heuristic results kept per GEMM for himuon_gemm_tune
+constexpr int kCandidates = 32;  // heuristic results kept per GEMM for himuon_gemm_tune
 
 struct Gemm {
     hipblasLtMatmulDesc_t desc = nullptr;

@@ -100,6 +100,36 @@ def test_ns_tiled_plan_replays(T, dtype):
     plan.close()
 
 
+@pytest.mark.parametrize("T,dtype", [(512, "bf16"), (0, "f32"), (0, "bf16")])
+def test_ns_gemm_plan_replays(T, dtype):
+    """The recorded library-GEMM call (large tiles, or whole matrices for
+    T = 0): every replay on new input contents equals the eager call, and
+    stays within the oracle's bar."""
+    announce(f"ns_gemm plan T={T} {dtype}, 3 replays")
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(T + 3)
+    shapes = [(600, 1100), (1024, 512), (100, 60)]
+    X = [torch.zeros(s, dtype=tdt, device=DEV) for s in shapes]
+    Y = [torch.empty_like(x) for x in X]
+    plan = hm.plan_ns_gemm(X, Y, T=T, K=5, coeffs=COEF32)
+    for it in range(3):
+        fill(X, gen, 1.0)
+        plan.launch()
+        ref = hm.ns_gemm(X, T=T, K=5, coeffs=COEF32)
+        torch.cuda.synchronize()
+        for y, r in zip(Y, ref):
+            assert torch.equal(y, r), f"replay {it}: output differs from the eager call"
+        x0, y0 = to_f64(X[0]), to_f64(Y[0])
+        if T == 0:
+            R = oracle.phi_k(x0, 5, *COEF32)
+            e = np.array([np.linalg.norm(y0 - R) / np.linalg.norm(R)])
+        else:
+            e = tile_errors(y0, oracle.ns_tiled(x0, T, 5, *COEF32), T)
+        assert e.max() <= TOL[tdt], e.max()
+    plan.close()
+
+
 def test_plan_rejects_bad_arguments_and_foreign_streams():
     x = workloads.gaussian(64, 64, 1, "bf16", DEV)
     ws = torch.empty(256, dtype=torch.uint8, device=DEV)

@@ -20,10 +20,13 @@
  * arrays, device pointers for matrix data and workspace, and a HIP stream
  * passed as void* (a hipStream_t; NULL is the null stream). No entry point
  * allocates device memory or synchronises the device on the compute path.
- * Each call copies its descriptor table to the workspace from a ring of
- * pinned host slots (allocated on first use, reused once the copy that last
- * used a slot has completed), so calls are not meant for stream capture into
- * a HIP graph: a captured copy would read whatever a slot holds at replay.
+ * A fused-kernel call over at most 32 matrices carries its descriptor table
+ * in the kernels' own launch arguments. Other calls copy their descriptor
+ * tables to the workspace from a ring of pinned host slots (allocated on
+ * first use, reused once the copy that last used a slot has completed), so
+ * calls are not meant for stream capture into a HIP graph: a captured copy
+ * would read whatever a slot holds at replay (plans, below, record such
+ * calls safely).
  *
  * Matrices are row-major: element (i, j) of matrix l sits at
  * ptr_l + i*ld_l + j (in elements). One call uses one storage dtype for all
@@ -184,10 +187,12 @@ int himuon_ns_tiled_hw(int64_t n_mats,
  *     library holds on each GPU it runs on until the process ends, so a call
  *     takes at most HIMUON_NOALLOC_MAX_MATS (1024) matrices; more is
  *     HIMUON_ERR_WORKSPACE, returned before anything is enqueued;
- *   - every call on a GPU rewrites that array through small upload kernels
- *     enqueued on `stream` ahead of the tile kernels, so calls on one stream
- *     follow each other safely, but calls that overlap on one GPU (on
- *     different streams, or from several threads) race and must not be made;
+ *   - every call on a GPU of more than 32 matrices rewrites that array
+ *     through small upload kernels enqueued on `stream` ahead of the tile
+ *     kernels (smaller calls carry the table in the tile kernels' own
+ *     arguments), so calls on one stream follow each other safely, but calls
+ *     that overlap on one GPU (on different streams, or from several
+ *     threads) race and must not be made;
  *   - the call allocates nothing, on the host or the device: no hipMalloc,
  *     no pinned staging; the descriptors travel in kernel arguments;
  *   - only calls a fused kernel serves: T = 256 with fp32 storage or bf16

@@ -347,6 +347,7 @@ KernelArgs make_kernel_args(const MatDesc* descs, int64_t n_mats, int K, float a
     KernelArgs ka{};
     ka.descs = descs;
     ka.odescs = nullptr;
+    ka.step = 0;
     ka.beta = 0.f;
     ka.decay = 1.f;
     ka.lr = 0.f;
@@ -374,6 +375,16 @@ KernelArgs make_kernel_args(const MatDesc* descs, int64_t n_mats, int K, float a
         ka.am = a;
     }
     return ka;
+}
+
+void set_inline_tables(KernelArgs& ka, const MatDesc* descs, const OptDesc* opt, int64_t n_mats)
+{
+    ka.descs = nullptr;
+    ka.odescs = nullptr;
+    for (int64_t m = 0; m < n_mats; ++m) {
+        ka.inline_descs[m] = descs[m];
+        if (opt) ka.inline_odescs[m] = opt[m];
+    }
 }
 
 int launch_chunks(int T, Storage st, Operand op, KernelArgs ka, int64_t total, int64_t n_chunks, hipStream_t stream)
@@ -447,12 +458,20 @@ int run_tiled(int64_t n_mats, const void* const* in_ptrs, void* const* out_ptrs,
     if (s != HIMUON_OK) return s;
     const size_t dbytes = ((size_t)n_mats * sizeof(MatDesc) + 255) / 256 * 256;
     OptDesc* const otab = opt_host ? reinterpret_cast<OptDesc*>(static_cast<uint8_t*>(workspace) + dbytes) : nullptr;
-    int status = upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
-    if (status == HIMUON_OK && opt_host)
-        status = upload_table(opt_host, (size_t)n_mats * sizeof(OptDesc), otab, hs, dev);
+    // A call of few matrices carries its tables in the launch arguments;
+    // larger ones copy them into the workspace ahead of the kernels.
+    const bool inl = n_mats <= kInlineMats;
+    int status = HIMUON_OK;
+    if (!inl) {
+        status = upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
+        if (status == HIMUON_OK && opt_host)
+            status = upload_table(opt_host, (size_t)n_mats * sizeof(OptDesc), otab, hs, dev);
+    }
     if (status == HIMUON_OK) {
         KernelArgs ka = make_kernel_args(static_cast<const MatDesc*>(workspace), n_mats, K, a, b, c);
         ka.odescs = otab;
+        ka.step = opt_host ? 1 : 0;
+        if (inl) set_inline_tables(ka, descs.data(), opt_host, n_mats);
         ka.beta = beta;
         ka.decay = decay;
         ka.lr = lr;
@@ -492,9 +511,11 @@ int run_tiled_hw(int64_t n_mats, const void* const* in_ptrs, void* const* out_pt
     int cur = 0, dev = 0;
     s = stream_device(hs, &cur, &dev);
     if (s != HIMUON_OK) return s;
-    int status = upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
+    const bool inl = n_mats <= kInlineMats;
+    int status = inl ? HIMUON_OK : upload_table(descs.data(), descs.size() * sizeof(MatDesc), workspace, hs, dev);
     if (status == HIMUON_OK) {
         KernelArgs ka = make_kernel_args(static_cast<const MatDesc*>(workspace), n_mats, K, a, b, c);
+        if (inl) set_inline_tables(ka, descs.data(), nullptr, n_mats);
         for (int64_t i = 0; i < n_chunks && status == HIMUON_OK; ++i) {
             ka.tile_begin = chunk_bound(i, total, n_chunks);
             ka.tile_end = chunk_bound(i + 1, total, n_chunks);

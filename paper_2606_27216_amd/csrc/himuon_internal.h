@@ -42,14 +42,22 @@ struct alignas(16) OptDesc {
 };
 static_assert(sizeof(OptDesc) == 16, "optimizer descriptor layout");
 
+// Descriptors a launch carries in its own arguments: a call of at most this
+// many matrices copies no table to the device before its kernels (2.5 KiB of
+// kernel arguments).
+constexpr int kInlineMats = 32;
+
 // Kernel arguments of one chunk launch: tiles [tile_begin, tile_end).
 struct KernelArgs {
+    // The descriptor tables in device memory, or null: then they are
+    // inline_descs / inline_odescs below.
     const MatDesc* descs;
-    // non-null: the launch is an optimizer step (OptDesc per matrix). The
-    // tile staging forms M <- beta M + G (stored, rounded to bf16) and the
+    const OptDesc* odescs;
+    // 1: the launch is an optimizer step (OptDesc per matrix). The tile
+    // staging forms M <- beta M + G (stored, rounded to bf16) and the
     // lookahead G + beta M (nesterov) or M as the tile's input; the
     // write-back stores W <- decay W - lr tau U.
-    const OptDesc* odescs;
+    int32_t step;
     float beta, decay, lr;
     int32_t nesterov;
     int64_t tile_begin;
@@ -69,6 +77,8 @@ struct KernelArgs {
     // a' = a - b^2 / (4c).
     float hshift;    // sigma b' / 2 (0 when c == 0)
     float am;        // a' (a when c == 0)
+    MatDesc inline_descs[kInlineMats];
+    OptDesc inline_odescs[kInlineMats];
 };
 
 // Enqueue one chunk on `stream`. Returns hipErrorInvalidValue for a
@@ -110,6 +120,9 @@ int plan_tiled_chunks(int64_t n_mats, const int64_t* rows, const int64_t* cols, 
 MatDesc make_desc(const void* in, void* out, int64_t rows, int64_t cols, int64_t ld_in, int64_t ld_out,
                   int64_t tile_begin, int Tw, int dtype, const void* mom);
 KernelArgs make_kernel_args(const MatDesc* descs, int64_t n_mats, int K, float a, float b, float c);
+// Copies the tables of a call of at most kInlineMats matrices into the
+// arguments (descs, odescs become null; `opt` may be null).
+void set_inline_tables(KernelArgs& ka, const MatDesc* descs, const OptDesc* opt, int64_t n_mats);
 int launch_chunks(int T, Storage st, Operand op, KernelArgs ka, int64_t total, int64_t n_chunks, hipStream_t stream);
 int stream_device(hipStream_t stream, int* cur, int* dev);
 

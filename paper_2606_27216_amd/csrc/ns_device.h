@@ -5,6 +5,8 @@
 
 #include "himuon_internal.h"
 
+#include <stddef.h>
+
 #include <math.h>
 
 namespace himuon {
@@ -29,7 +31,24 @@ typedef __attribute__((address_space(1))) u32x4 gbl_u32x4;
 // descriptor loads become scalar loads, which do not wait on the vector
 // memory counter that the tile loads and stores share.
 typedef __attribute__((address_space(4))) const MatDesc ConstDesc;
-HM_DEV const ConstDesc* desc_table(const KernelArgs& a) { return (const ConstDesc*)(uintptr_t)a.descs; }
+typedef __attribute__((address_space(4))) const OptDesc ConstOpt;
+// A table carried in the arguments is read where the launch placed them:
+// every kernel that reads these tables takes its KernelArgs as its first
+// argument, at offset 0 of the kernel-argument segment. (Addressing the
+// argument itself instead would make the compiler copy the whole structure
+// into per-lane scratch memory.)
+typedef __attribute__((address_space(4))) const uint8_t ConstByte;
+HM_DEV ConstByte* kernarg_base() { return (ConstByte*)__builtin_amdgcn_kernarg_segment_ptr(); }
+HM_DEV const ConstDesc* desc_table(const KernelArgs& a)
+{
+    if (a.descs) return (const ConstDesc*)(uintptr_t)a.descs;
+    return (const ConstDesc*)(kernarg_base() + offsetof(KernelArgs, inline_descs));
+}
+HM_DEV const ConstOpt* opt_table(const KernelArgs& a)
+{
+    if (a.odescs) return (const ConstOpt*)(uintptr_t)a.odescs;
+    return (const ConstOpt*)(kernarg_base() + offsetof(KernelArgs, inline_odescs));
+}
 
 // Matrix owning `tile`, searching from `hint` (the tiles one wave visits only
 // grow, so the owner of an earlier tile is a lower bound). Tile ids of one

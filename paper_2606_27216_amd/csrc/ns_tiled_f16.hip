@@ -275,8 +275,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         L.vin = full & ((fl & MAT_VEC_IN) != 0);
         L.vout = full & ((fl & MAT_VEC_OUT) != 0);
         if constexpr (OPT) {
-            typedef __attribute__((address_space(4))) const OptDesc ConstOpt;
-            const ConstOpt& O = ((const ConstOpt*)(uintptr_t)args.odescs)[mhint];
+            const ConstOpt& O = opt_table(args)[mhint];
             L.mom = O.mom;
             L.tau = O.tau;
         } else {
@@ -1455,7 +1454,7 @@ hipError_t launch_f16(const KernelArgs& args, hipStream_t stream)
 
 hipError_t launch_ns_tiled_f16(int T, const KernelArgs& args, hipStream_t stream)
 {
-    if (args.odescs) {  // the optimizer step (c > 0, T <= 128; has_step_kernel)
+    if (args.step) {  // the optimizer step (c > 0, T <= 128; has_step_kernel)
         if (!(args.c > 0.f)) return hipErrorInvalidValue;
         switch (T) {
         case 32: return launch_f16<32, 1, 0, true>(args, stream);

@@ -118,8 +118,7 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
         void* mom = nullptr;
         float tau = 0.f;
         if constexpr (OPT) {
-            typedef __attribute__((address_space(4))) const OptDesc ConstOpt;
-            const ConstOpt& O = ((const ConstOpt*)(uintptr_t)args.odescs)[lo];
+            const ConstOpt& O = opt_table(args)[lo];
             mom = O.mom;
             tau = O.tau;
         }
@@ -445,7 +444,7 @@ hipError_t launch_one(const KernelArgs& args, hipStream_t stream)
 template <Storage ST, Operand OP>
 hipError_t launch_T(int T, const KernelArgs& args, hipStream_t stream)
 {
-    if (args.odescs) {
+    if (args.step) {
         switch (T) {
         case 32: return launch_one<32, 1, ST, OP, true>(args, stream);
         case 64: return launch_one<64, 2, ST, OP, true>(args, stream);

@@ -90,10 +90,22 @@ extern "C" int himuon_ns_tiled_noalloc(int64_t n_mats, const void* const* in_ptr
     void* table = nullptr;
     int status = table_address(dev, &table);
 
-    // ---- descriptor table, in batches carried by kernel arguments
+    // ---- descriptor table: carried by the tile kernels' own arguments for a
+    // call of at most himuon::kInlineMats matrices, else written to `scratch`
+    // in batches carried by the arguments of upload kernels
+    const bool inl = n_mats <= himuon::kInlineMats;
+    MatDesc inline_descs[himuon::kInlineMats];
     DescWords words;
     int64_t next = 0;
-    for (int64_t m0 = 0; m0 < n_mats && status == HIMUON_OK; m0 += kPerUpload) {
+    if (inl) {
+        for (int64_t m = 0; m < n_mats; ++m) {
+            inline_descs[m] = himuon::make_desc(in_ptrs[m], out_ptrs[m], rows[m], cols[m],
+                                                ld_in ? ld_in[m] : cols[m], ld_out ? ld_out[m] : cols[m], next, T,
+                                                dtype, nullptr);
+            next += ceil_div(rows[m], T) * ceil_div(cols[m], T);
+        }
+    }
+    for (int64_t m0 = 0; !inl && m0 < n_mats && status == HIMUON_OK; m0 += kPerUpload) {
         const int n = (int)(n_mats - m0 < kPerUpload ? n_mats - m0 : kPerUpload);
         memset(&words, 0, sizeof(words));
         for (int j = 0; j < n; ++j) {
@@ -110,7 +122,8 @@ extern "C" int himuon_ns_tiled_noalloc(int64_t n_mats, const void* const* in_ptr
         if (e != hipSuccess) status = himuon::set_hip_error(e);
     }
     if (status == HIMUON_OK) {
-        const himuon::KernelArgs ka = himuon::make_kernel_args(static_cast<const MatDesc*>(table), n_mats, K, a, b, c);
+        himuon::KernelArgs ka = himuon::make_kernel_args(static_cast<const MatDesc*>(table), n_mats, K, a, b, c);
+        if (inl) himuon::set_inline_tables(ka, inline_descs, nullptr, n_mats);
         status = himuon::launch_chunks(T, st, opnd, ka, total, n_chunks, hs);
     }
     if (dev != cur) (void)hipSetDevice(cur);

@@ -196,6 +196,41 @@ HM_DEV float wave_sum(float v)
     return v;
 }
 
+// Normalisation of an fp32-operand tile without rounding it. The step is
+// homogeneous: with X = Y / rho, one step X <- aX + (bA + cA^2)X is
+// Y <- aY + ((b / rho^2) A_Y + (c / rho^4) A_Y^2) Y with A_Y = Y Y^T, and
+// Y_K / rho = X_K. So the tile is scaled by a power of two only (exact), to
+// Y with ||Y||_F^2 = m in [1, 4), and rho^2 = m goes into the coefficients
+// and the output factor; the normalised tile itself is never rounded. The
+// coefficients b / m and c / m^2 are carried as unevaluated sums hi + lo of
+// two fp32 numbers (formed in fp64), so that they are exact to about 2^-48
+// and the polynomial is the one the caller asked for.
+// `ss` is the tile's sum of squares (a normal fp32 number, or 0: then
+// Phi_K = 0 and everything here is 0).
+struct ExactNorm {
+    float scale;   // 2^-e, with ss = m 4^e
+    float bh, bl;  // b / m = bh + bl
+    float ch, cl;  // c / m^2 = ch + cl
+    float out;     // 1 / sqrt(m)
+};
+HM_DEV ExactNorm exact_norm(float ss, float b, float c)
+{
+    if (!(ss > 0.f)) return ExactNorm{0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const uint32_t sb = __float_as_uint(ss);
+    const int e = ((int)(sb >> 23) - 127) >> 1;
+    const double m = (double)__uint_as_float(sb - ((uint32_t)(2 * e) << 23));
+    const double bd = (double)b / m, cd = (double)c / (m * m);
+    const float bh = (float)bd, ch = (float)cd;
+    return ExactNorm{ldexpf(1.f, -e), bh, (float)(bd - (double)bh), ch, (float)(cd - (double)ch),
+                     (float)(1.0 / sqrt(m))};
+}
+
+// b' G + c' Q with b' = bh + bl and c' = ch + cl (the correction terms first)
+HM_DEV float poly2(const ExactNorm& n, float g, float q)
+{
+    return fmaf(n.ch, q, fmaf(n.bh, g, fmaf(n.bl, g, n.cl * q)));
+}
+
 // Four consecutive elements of row `gr`, columns gc..gc+3, widened to fp32;
 // zero outside the matrix (the zero padding of the tiling operator).
 template <Storage ST>

@@ -217,7 +217,13 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
         ss = s_red[1][0];
 #pragma unroll
         for (int w = 1; w < W; ++w) ss += s_red[1][w];
-        const float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;  // Phi_K(0) = 0
+        // fp32 operands: the exact power-of-two normalisation (exact_norm)
+        float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;  // Phi_K(0) = 0
+        ExactNorm en{};
+        if constexpr (OP == Operand::F32) {
+            en = exact_norm(ss, args.b, args.c);
+            inv = en.scale;
+        }
 #pragma unroll
         for (int I = 0; I < NBR; ++I)
 #pragma unroll
@@ -353,7 +359,7 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
                         const f32x16 sq = chain_sum<NC>(Gc[I][J]);
                         if constexpr (OP == Operand::F32) {
 #pragma unroll
-                            for (int v = 0; v < 16; ++v) G[I][J][v] = fmaf(args.c, sq[v], args.b * G[I][J][v]);
+                            for (int v = 0; v < 16; ++v) G[I][J][v] = poly2(en, G[I][J][v], sq[v]);
                         } else {
                             G[I][J] = sq * args.c;
                         }
@@ -362,7 +368,14 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
 #pragma unroll
                 for (int I = 0; I < NBR; ++I)
 #pragma unroll
-                    for (int J = 0; J < NBR; ++J) G[I][J] *= args.b;
+                    for (int J = 0; J < NBR; ++J) {
+                        if constexpr (OP == Operand::F32) {
+#pragma unroll
+                            for (int v = 0; v < 16; ++v) G[I][J][v] = fmaf(en.bh, G[I][J][v], en.bl * G[I][J][v]);
+                        } else {
+                            G[I][J] *= args.b;
+                        }
+                    }
             }
 
             // X <- aX + B X on the slab
@@ -410,6 +423,12 @@ __global__ void __launch_bounds__(RectShape<N>::W * 64) ns_rect_kernel(const Ker
         }
 
         // ---- write back the unpadded part (a tall tile through the LDS copy)
+        if constexpr (OP == Operand::F32) {
+#pragma unroll
+            for (int I = 0; I < NBR; ++I)
+#pragma unroll
+                for (int q = 0; q < NBC; ++q) X[I][q] *= en.out;
+        }
         if constexpr (TALL) {
             __syncthreads();  // every wave is done with its region of the staging area
 #pragma unroll

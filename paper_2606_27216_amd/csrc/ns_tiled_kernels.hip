@@ -193,7 +193,15 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
 #pragma unroll
             for (int w = 1; w < WT; ++w) ss += s_red[1][tslot * WT + w];
         }
-        const float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;  // Phi_K(0) = 0
+        // 16-bit operands round the tile anyway: X_0 = S / ||S||_F. fp32
+        // operands: the exact power-of-two normalisation (exact_norm), the
+        // rest of ||S||_F in the step's coefficients and the output factor.
+        float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;  // Phi_K(0) = 0
+        ExactNorm en{};
+        if constexpr (OP == Operand::F32) {
+            en = exact_norm(ss, args.b, args.c);
+            inv = en.scale;
+        }
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -323,7 +331,7 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
                         const f32x16 sq = chain_sum<NC>(Gc[rb][J]);
                         if constexpr (OP == Operand::F32) {
 #pragma unroll
-                            for (int v = 0; v < 16; ++v) G[rb][J][v] = fmaf(args.c, sq[v], args.b * G[rb][J][v]);
+                            for (int v = 0; v < 16; ++v) G[rb][J][v] = poly2(en, G[rb][J][v], sq[v]);
                         } else {
                             G[rb][J] = sq * args.c;
                         }
@@ -332,7 +340,14 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
 #pragma unroll
                 for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-                    for (int J = 0; J < NB; ++J) G[rb][J] *= args.b;
+                    for (int J = 0; J < NB; ++J) {
+                        if constexpr (OP == Operand::F32) {
+#pragma unroll
+                            for (int v = 0; v < 16; ++v) G[rb][J][v] = fmaf(en.bh, G[rb][J][v], en.bl * G[rb][J][v]);
+                        } else {
+                            G[rb][J] *= args.b;
+                        }
+                    }
             }
 
             // X <- aX + B X
@@ -381,6 +396,12 @@ __global__ void __launch_bounds__(kThreads) ns_tiled_kernel(const KernelArgs arg
         }
 
         // ---- write back the unpadded part
+        if constexpr (OP == Operand::F32) {
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int q = 0; q < NB; ++q) X[rb][q] *= en.out;
+        }
         if (valid) {
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) {

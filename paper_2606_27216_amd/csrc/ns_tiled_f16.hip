@@ -1059,10 +1059,12 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                                 for (int w = 0; w < 4; ++w) {
                                     // (copied out first: a bit cast of a vector element
                                     // would read the vector's first element)
+                                    // (fma with a zero addend: one mixed-precision
+                                    // instruction per value, the same rounding)
                                     const uint32_t wv = Zop[rb][n0 + n][s][w];
                                     const f16x2 pr = __builtin_bit_cast(f16x2, wv);
-                                    acc[rb][n][8 * s + 2 * w] = sa * (float)pr[0];
-                                    acc[rb][n][8 * s + 2 * w + 1] = sa * (float)pr[1];
+                                    acc[rb][n][8 * s + 2 * w] = __builtin_fmaf(sa, (float)pr[0], 0.f);
+                                    acc[rb][n][8 * s + 2 * w + 1] = __builtin_fmaf(sa, (float)pr[1], 0.f);
                                 }
                 };
                 // a finished group of Z becomes next step's operands (after the
@@ -1130,8 +1132,8 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                             for (int w = 0; w < 4; ++w) {
                                 const uint32_t wv = Zop[rb][q][s][w];
                                 const f16x2 pr = __builtin_bit_cast(f16x2, wv);
-                                OB[rb][q][4 * s + w] = pack2<Operand::BF16>((float)pr[0] * args.unscale,
-                                                                            (float)pr[1] * args.unscale);
+                                OB[rb][q][4 * s + w] = pack2<Operand::BF16>(__builtin_fmaf((float)pr[0], args.unscale, 0.f),
+                                                                            __builtin_fmaf((float)pr[1], args.unscale, 0.f));
                             }
             }
           }

@@ -32,7 +32,9 @@ The JSON also carries:
 
 `--calib-gemm N` times the GEMM library's N x N x N fp16 product instead (the
 same power and clock fields), as a reference for what dense MFMA work
-sustains under the same power cap.
+sustains under the same power cap; `--calib-mfma f16|bf16` times a launch of
+nothing but 32x32x16 MFMA products (himuon_calib_mfma), the device's ceiling
+for the tile kernels' own instruction.
 """
 from __future__ import annotations
 
@@ -152,6 +154,49 @@ def bench_calib_gemm(args, torch, np, dev):
     rec = {"metric": "library GEMM fp16 TFLOP/s (2N^3)", "value": round(2.0 * n ** 3 / (wall / args.steps) / 1e12, 1),
            "unit": "TFLOP/s", "n": n, "steps": args.steps, "warmup": args.warmup,
            "median_ms": round(float(np.median(ms)), 4), "peak": PEAK_TFLOPS["f16"], "power": ps.summary()}
+    print(json.dumps(rec), flush=True)
+
+
+def bench_calib_mfma(args, torch, np, dev, hm):
+    """Dense 32x32x16 MFMA products and nothing else (himuon_calib_mfma):
+    the rate the device sustains for the tile kernels' own instruction,
+    timed like a bench step, with the power sampler."""
+    compute = hm.COMPUTE_BF16 if args.calib_mfma == "bf16" else hm.COMPUTE_F16
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    grid, iters = 8 * cus, 20000  # eight waves per SIMD
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    x = torch.randn(4096 * 8, device=dev, generator=g, dtype=torch.float32)
+    ops = (x.to(torch.bfloat16) if args.calib_mfma == "bf16" else x.to(torch.float16)).contiguous()
+    out = torch.empty(grid * 256, device=dev, dtype=torch.float32)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def launch():
+        st = hm.himuon_calib_mfma(compute, ops.data_ptr(), out.data_ptr(), grid, iters, stream)
+        if st != hm.OK:
+            raise RuntimeError(f"himuon_calib_mfma: {hm.himuon_status_string(st)}")
+
+    flops = grid * 4 * 4 * iters * 32 * 32 * 16 * 2.0
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    with PowerSampler() as ps:
+        for _ in range(args.warmup):
+            launch()
+        torch.cuda.synchronize()
+        ps.restart()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            ev[i][0].record()
+            launch()
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    assert torch.isfinite(out).all().item()
+    rec = {"metric": f"MFMA-only 32x32x16 {args.calib_mfma} TFLOP/s", "value": round(flops / (wall / args.steps) / 1e12, 1),
+           "unit": "TFLOP/s", "steps": args.steps, "warmup": args.warmup, "grid": grid, "iters": iters,
+           "median_launch_ms": round(float(np.median(ms)), 4),
+           "median_launch_tflops": round(flops / float(np.median(ms)) / 1e9, 1),
+           "peak": PEAK_TFLOPS["f16"], "power": ps.summary()}
     print(json.dumps(rec), flush=True)
 
 
@@ -580,6 +625,8 @@ def main():
                     help="--optstep variants to run (comma-separated names, or all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB per launch (counter calibration)")
+    ap.add_argument("--calib-mfma", choices=["f16", "bf16"], default=None,
+                    help="only run dense MFMA products (himuon_calib_mfma): the device's MFMA ceiling")
     ap.add_argument("--calib-gemm", type=int, default=0,
                     help="only time the GEMM library's N x N x N fp16 product (power-cap reference)")
     args = ap.parse_args()
@@ -608,6 +655,8 @@ def main():
 
     if args.calib_gemm:
         return bench_calib_gemm(args, torch, np, dev)
+    if args.calib_mfma:
+        return bench_calib_mfma(args, torch, np, dev, hm)
     if args.optstep:
         return bench_optstep(args, hm, torch, np, dev)
     if args.layershapes:

@@ -466,6 +466,23 @@ int himuon_last_hip_error(void);
 /* Library version, major*10000 + minor*100 + patch. */
 int himuon_version(void);
 
+/*
+ * Measurement aid, not part of the map: a launch that runs nothing but dense
+ * 32x32x16 MFMA products (fp16 operands for compute = HIMUON_COMPUTE_F16,
+ * bf16 for HIMUON_COMPUTE_BF16, fp32 accumulation), the ceiling against which
+ * the roofline of the tile kernels' issued MFMA work is read. `grid`
+ * workgroups of 256 threads; every wave issues 4 * iters products with four
+ * independent accumulators, so one launch performs
+ *     grid * 4 * 4 * iters * 32 * 32 * 16 * 2   flops.
+ * ops: device memory of 4096 16-byte words (64 KiB) of operand bits, read
+ * only (read once per lane). out: device memory of grid * 256 floats,
+ * written (the lanes' sums, so that nothing is optimised away). Enqueue only,
+ * on `stream` (NULL: the default stream). Errors: HIMUON_ERR_INVALID_ARG
+ * (null pointer, grid or iters below 1, another compute value),
+ * HIMUON_ERR_HIP.
+ */
+int himuon_calib_mfma(int compute, const void* ops, float* out, int grid, int iters, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

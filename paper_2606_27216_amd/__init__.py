@@ -113,6 +113,8 @@ def lib():
         L.himuon_last_hip_error.restype = ctypes.c_int
         L.himuon_version.argtypes = []
         L.himuon_version.restype = ctypes.c_int
+        L.himuon_calib_mfma.argtypes = [ctypes.c_int, vp, vp, ctypes.c_int, ctypes.c_int, vp]
+        L.himuon_calib_mfma.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -432,6 +434,10 @@ def himuon_last_hip_error() -> int:
 
 def himuon_version() -> int:
     return int(lib().himuon_version())
+
+
+def himuon_calib_mfma(compute: int, ops: int, out: int, grid: int, iters: int, stream: int = 0) -> int:
+    return int(lib().himuon_calib_mfma(compute, ops, out, grid, iters, stream))
 
 
 # ------------------------------------------------------------ tensor wrapper

@@ -40,6 +40,7 @@ SOURCES = [
     ("ns_gemm_path.cpp", []),
     ("himuon_step.cpp", []),
     ("himuon_plan.cpp", []),
+    ("calib_mfma.hip", []),
 ]
 # The whole-matrix and large-tile path runs its Newton-Schulz GEMMs on hipBLASLt.
 LINK_LIBS = ["-lhipblaslt"]

@@ -362,3 +362,15 @@ def test_gemm_hw_workspace_and_validation():
     assert hm.himuon_ns_gemm_hw(**args) == hm.ERR_INVALID_ARG
     args.update(Th=32, Tw=64)
     assert hm.himuon_ns_gemm_hw(**args) == hm.ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("args", [
+    (hm.COMPUTE_F16, 0, FAKE, 1, 1),        # no operands
+    (hm.COMPUTE_F16, FAKE, 0, 1, 1),        # no output
+    (hm.COMPUTE_F16, FAKE, FAKE, 0, 1),     # empty grid
+    (hm.COMPUTE_BF16, FAKE, FAKE, 1, 0),    # no products
+    (hm.COMPUTE_F32, FAKE, FAKE, 1, 1),     # fp32 operands: no such calibration
+    (hm.COMPUTE_DEFAULT, FAKE, FAKE, 1, 1),
+])
+def test_calib_mfma_rejects_bad_arguments_before_any_launch(args):
+    assert hm.himuon_calib_mfma(*args) == hm.ERR_INVALID_ARG

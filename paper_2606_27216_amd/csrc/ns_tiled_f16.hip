@@ -935,9 +935,9 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
         // one column half at a time:
         //   Z own rows to LDS | barrier | Gram | Y, first half | barrier |
         //   Y first half to LDS | Y, second half | barrier | Y second half to
-        //   LDS | HY, first half | barrier | HY, second half.
+        //   LDS | MY, first half | barrier | MY, second half.
         // Products run on groups of NG column blocks, which bounds the
-        // accumulators to 64 registers; each HY group is converted at once
+        // accumulators to 64 registers; each MY group is converted at once
         // into the next step's fp16 operands, from which the bf16 output is
         // rounded after the last step (for K = 0 too, so that no fp32 copy of
         // the tile stays live across the steps). The barrier at the top of each later step keeps
@@ -1110,7 +1110,7 @@ __global__ void __launch_bounds__((F16Shape<T, RB>::kThreads), (F16Shape<T, RB>:
                         __syncthreads();  // every wave is done reading this column half of Z
                         put_rows(Yop, NH * h, NH * (h + 1));
                     }
-                    // Z <- a Z + H Y, by column halves
+                    // Z <- a' Z + M Y, by column halves
 #pragma unroll
                     for (int gq = 0; gq < NGR / 2; ++gq) hy_group(gq);
                     __syncthreads();  // the second half of Y is visible

@@ -13,7 +13,10 @@ Throughput counts 6·H·W·T·K flops per matrix (three T³ products per tile pe
 step). Rank 0 prints one JSON line on stdout; progress goes to stderr.
 The JSON also carries:
   roofline      the fused kernel's algorithmic flops per launch over its mean
-                launch duration (HIP events on the launch stream), against the
+                launch duration (one pair of HIP events on the launch stream
+                around the timed region, whose launches run back to back; the
+                per-step spread in `step_ms` comes from a second, untimed pass
+                with an event pair around each step), against the
                 published dense fp16/bf16 MFMA peak (2.5 PFLOP/s); the MFMA
                 work actually issued (less than 6T^3 per tile-step where a
                 kernel exploits the symmetry of H and aI + P) is reported
@@ -24,7 +27,7 @@ The JSON also carries:
   cpu_baseline  the fp64 oracle timed on the host cores (and on one core) on a
                 bounded random sample of the same workload's tiles (read back
                 from the GPU), with the CPU model; its `parity` field compares
-                those oracle tiles with the GPU's outputs of the last timed step;
+                those oracle tiles with the GPU's outputs of the last step;
   power         socket power and graphics clock sampled from the driver's sysfs
                 files during the timed region (null where they cannot be read):
                 the fused kernels run at the board's power cap, below the clock
@@ -115,10 +118,15 @@ class PowerSampler:
         self.power_w.clear()
         self.mhz.clear()
 
-    def __exit__(self, *exc):
+    def stop(self):
+        """Ends the sampling; summary() then covers what was sampled so far."""
         if self._thread:
             self._stop.set()
             self._thread.join()
+            self._thread = None
+
+    def __exit__(self, *exc):
+        self.stop()
         return False
 
     def summary(self):
@@ -131,26 +139,54 @@ class PowerSampler:
                 "source": "sysfs hwmon power1_input, pp_dpm_sclk"}
 
 
+def timed_steps(torch, np, step, stream, steps, warmup, ps=None, jitter_steps=30):
+    """Runs `warmup` untimed steps, then times exactly `steps` steps back to back.
+
+    The timed region holds one pair of HIP events on the launch stream (start
+    and end) and nothing else: an event recorded between two launches costs
+    the GPU 10-25 us (the event's release fence), which a call of a few
+    hundred microseconds would otherwise carry. Step-to-step spread comes from
+    a second, untimed pass of up to `jitter_steps` steps with an event pair
+    around each. `ps` (a PowerSampler) is restarted with the timed region and
+    stopped at its end.
+
+    Returns (wall seconds, event-timed ms of the timed region, per-step ms of
+    the second pass)."""
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if ps is not None:
+        ps.restart()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    if ps is not None:
+        ps.stop()
+    region_ms = e0.elapsed_time(e1)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(min(steps, jitter_steps))]
+    for a, b in ev:
+        a.record(stream)
+        step()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return wall, region_ms, np.array([a.elapsed_time(b) for a, b in ev])
+
+
 def bench_calib_gemm(args, torch, np, dev):
     """The GEMM library's N x N x N fp16 product, timed like a bench step."""
     n = args.calib_gemm
     a = torch.randn(n, n, device=dev, dtype=torch.float16)
     b = torch.randn(n, n, device=dev, dtype=torch.float16)
     c = torch.empty(n, n, device=dev, dtype=torch.float16)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     with PowerSampler() as ps:
-        for _ in range(args.warmup):
-            torch.matmul(a, b, out=c)
-        torch.cuda.synchronize()
-        ps.restart()
-        t0 = time.perf_counter()
-        for i in range(args.steps):
-            ev[i][0].record()
-            torch.matmul(a, b, out=c)
-            ev[i][1].record()
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-    ms = np.array([x.elapsed_time(y) for x, y in ev])
+        wall, _, ms = timed_steps(torch, np, lambda: torch.matmul(a, b, out=c), torch.cuda.current_stream(dev),
+                                  args.steps, args.warmup, ps)
     rec = {"metric": "library GEMM fp16 TFLOP/s (2N^3)", "value": round(2.0 * n ** 3 / (wall / args.steps) / 1e12, 1),
            "unit": "TFLOP/s", "n": n, "steps": args.steps, "warmup": args.warmup,
            "median_ms": round(float(np.median(ms)), 4), "peak": PEAK_TFLOPS["f16"], "power": ps.summary()}
@@ -177,20 +213,8 @@ def bench_calib_mfma(args, torch, np, dev, hm):
             raise RuntimeError(f"himuon_calib_mfma: {hm.himuon_status_string(st)}")
 
     flops = grid * 4 * 4 * iters * 32 * 32 * 16 * 2.0
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     with PowerSampler() as ps:
-        for _ in range(args.warmup):
-            launch()
-        torch.cuda.synchronize()
-        ps.restart()
-        t0 = time.perf_counter()
-        for i in range(args.steps):
-            ev[i][0].record()
-            launch()
-            ev[i][1].record()
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-    ms = np.array([a.elapsed_time(b) for a, b in ev])
+        wall, _, ms = timed_steps(torch, np, launch, torch.cuda.current_stream(dev), args.steps, args.warmup, ps)
     assert torch.isfinite(out).all().item()
     rec = {"metric": f"MFMA-only 32x32x16 {args.calib_mfma} TFLOP/s", "value": round(flops / (wall / args.steps) / 1e12, 1),
            "unit": "TFLOP/s", "steps": args.steps, "warmup": args.warmup, "grid": grid, "iters": iters,
@@ -267,7 +291,7 @@ def cpu_model() -> str:
 def cpu_baseline(mats, outs, T, K, coeffs, budget_s, seed=0):
     """The fp64 oracle on a random sample of tiles of the workload (host
     cores), timed; its tiles are also compared with the GPU's outputs of the
-    last timed step (per-tile relative Frobenius error). A second, smaller
+    last step (per-tile relative Frobenius error). A second, smaller
     sample runs on one core."""
     import numpy as np
     import oracle
@@ -320,7 +344,7 @@ def cpu_baseline(mats, outs, T, K, coeffs, budget_s, seed=0):
             "one_core_value": flops * done1 / elapsed1 / 1e12, "cpu_model": cpu_model(),
             "parity": {"tiles": int(e.size), "max": float(e.max()), "p50": float(np.median(e)),
                        "bar": 2e-2 if mats[0].dtype.itemsize == 2 else 1e-5,
-                       "what": "per-tile relative Frobenius error of the last timed step's output against these "
+                       "what": "per-tile relative Frobenius error of the last step's output against these "
                                "oracle tiles"}}
 
 
@@ -360,21 +384,10 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
         hm.ns_gemm(mats, outputs=outs, T=Th, K=args.K, coeffs=coeffs, compute=compute,
                    chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream, Tw=Tw)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        ev[i][0].record(stream)
-        step()
-        ev[i][1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    wall, region_ms, step_ms = timed_steps(torch, np, step, stream, args.steps, args.warmup)
     op_name = "f32" if code == hm.F32 else ("bf16" if compute == hm.COMPUTE_BF16 else "f16")
     peak = PEAK_TFLOPS[op_name]
-    achieved = flops_step / (float(np.mean(step_ms)) * 1e-3) / 1e12
+    achieved = flops_step / (region_ms / args.steps * 1e-3) / 1e12
     rec = {
         "metric": metric, "value": round(flops_step / (wall / args.steps) / 1e12, 3), "unit": "TFLOP/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 4),
@@ -384,9 +397,10 @@ def bench_gemm(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
                    "chunk_budget_bytes": int(args.budget), "workspace_bytes": need, "gemm_tuned": bool(args.tune)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": None, "flops_per_step": flops_step,
-                     "mean_step_ms": round(float(np.mean(step_ms)), 4)},
+                     "mean_step_ms": round(region_ms / args.steps, 4)},
         "step_ms": {"median": round(float(np.median(step_ms)), 4),
-                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4)},
+                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4),
+                    "steps": len(step_ms)},
     }
     print(json.dumps(rec), flush=True)
 
@@ -406,20 +420,9 @@ def bench_rect(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
         hm.ns_tiled(mats, outputs=outs, T=Th, Tw=Tw, K=args.K, coeffs=coeffs, compute=compute,
                     chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        ev[i][0].record(stream)
-        step()
-        ev[i][1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    wall, region_ms, step_ms = timed_steps(torch, np, step, stream, args.steps, args.warmup)
     peak = PEAK_TFLOPS[op_name]
-    achieved = flops_step / (float(np.mean(step_ms)) * 1e-3) / 1e12
+    achieved = flops_step / (region_ms / args.steps * 1e-3) / 1e12
     rec = {
         "metric": "tiled-NS TFLOP/s ((4m^2n + 2m^3)K per tile), 7B layer stack %dx%d tiles K=%d (fused kernel)"
                   % (Th, Tw, args.K),
@@ -431,9 +434,10 @@ def bench_rect(args, hm, torch, np, mats, outs, desc, coeffs, compute, code, str
                    "chunk_budget_bytes": int(args.budget)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": None, "flops_per_step": flops_step,
-                     "mean_step_ms": round(float(np.mean(step_ms)), 4)},
+                     "mean_step_ms": round(region_ms / args.steps, 4)},
         "step_ms": {"median": round(float(np.median(step_ms)), 4),
-                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4)},
+                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4),
+                    "steps": len(step_ms)},
     }
     print(json.dumps(rec), flush=True)
 
@@ -697,22 +701,10 @@ def main():
         hm.ns_tiled(mats, outputs=outs, T=args.T, K=args.K, coeffs=coeffs, compute=compute,
                     chunk_budget_bytes=int(args.budget), workspace=ws, stream=stream)
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     with PowerSampler() as ps:
-        for _ in range(args.warmup):
-            step()
-        torch.cuda.synchronize()
-        log(f"warmup {args.warmup} steps done")
-        ps.restart()
-        t_start = time.perf_counter()
-        for i in range(args.steps):
-            ev[i][0].record(stream)
-            step()
-            ev[i][1].record(stream)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t_start
-    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
-    log(f"timed {args.steps} steps: wall {wall * 1e3:.2f} ms, event median {np.median(step_ms):.3f} ms/step")
+        wall, region_ms, step_ms = timed_steps(torch, np, step, stream, args.steps, args.warmup, ps)
+    log(f"timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {region_ms:.2f} ms; "
+        f"per-step median {np.median(step_ms):.3f} ms")
     power = ps.summary()
     if power:
         log(f"socket power {power['socket_w_median']} W, graphics clock {power['gfx_mhz_median']} MHz "
@@ -720,8 +712,8 @@ def main():
 
     ms_per_step = wall * 1e3 / args.steps
     value = flops_step / (wall / args.steps) / 1e12
-    # per launch: a step is one descriptor upload plus `launches` kernel launches
-    launch_ms = float(np.mean(step_ms)) / launches
+    # per launch: a step is one call of `launches` kernel launches
+    launch_ms = region_ms / args.steps / launches
     flops_launch = flops_step / launches
     achieved = flops_launch / (launch_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[op_name]
@@ -757,7 +749,8 @@ def main():
             "mfma_issued_frac": round(achieved * issued / peak, 4),
         },
         "step_ms": {"median": round(float(np.median(step_ms)), 4),
-                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4)},
+                    "iqr": round(float(np.percentile(step_ms, 75) - np.percentile(step_ms, 25)), 4),
+                    "steps": len(step_ms)},
         "power": power,
     }
     if args.cpu_seconds > 0:

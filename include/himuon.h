@@ -478,7 +478,8 @@ int himuon_version(void);
  * only (read once per lane). out: device memory of grid * 256 floats,
  * written (the lanes' sums, so that nothing is optimised away). Enqueue only,
  * on `stream` (NULL: the default stream). Errors: HIMUON_ERR_INVALID_ARG
- * (null pointer, grid or iters below 1, another compute value),
+ * (null pointer, grid or iters below 1, grid above 2^20, another compute
+ * value),
  * HIMUON_ERR_HIP.
  */
 int himuon_calib_mfma(int compute, const void* ops, float* out, int grid, int iters, void* stream);

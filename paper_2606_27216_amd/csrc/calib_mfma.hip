@@ -18,6 +18,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kCalibThreads = 256;
 constexpr int kCalibOperands = 4096;  // 16-byte operand words read from `ops`
+constexpr int kCalibMaxGrid = 1 << 20;  // keeps 4 * (global lane index) within int
 
 // Every wave keeps four independent accumulators (so no product waits on
 // the one before it) and issues 4 * iters products on operands loaded once;
@@ -58,7 +59,7 @@ __global__ void __launch_bounds__(kCalibThreads) calib_mfma_kernel(const u32x4* 
 extern "C" int himuon_calib_mfma(int compute, const void* ops, float* out, int grid, int iters, void* stream)
 {
     using namespace himuon;
-    if (!ops || !out || grid < 1 || iters < 1) return HIMUON_ERR_INVALID_ARG;
+    if (!ops || !out || grid < 1 || grid > kCalibMaxGrid || iters < 1) return HIMUON_ERR_INVALID_ARG;
     if (compute != HIMUON_COMPUTE_F16 && compute != HIMUON_COMPUTE_BF16) return HIMUON_ERR_INVALID_ARG;
     hipStream_t hs = static_cast<hipStream_t>(stream);
     if (compute == HIMUON_COMPUTE_BF16)

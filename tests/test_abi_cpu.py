@@ -368,6 +368,7 @@ def test_gemm_hw_workspace_and_validation():
     (hm.COMPUTE_F16, 0, FAKE, 1, 1),        # no operands
     (hm.COMPUTE_F16, FAKE, 0, 1, 1),        # no output
     (hm.COMPUTE_F16, FAKE, FAKE, 0, 1),     # empty grid
+    (hm.COMPUTE_F16, FAKE, FAKE, (1 << 20) + 1, 1),  # lane indices past int range
     (hm.COMPUTE_BF16, FAKE, FAKE, 1, 0),    # no products
     (hm.COMPUTE_F32, FAKE, FAKE, 1, 1),     # fp32 operands: no such calibration
     (hm.COMPUTE_DEFAULT, FAKE, FAKE, 1, 1),

@@ -184,6 +184,14 @@ int resolve_operand(int dtype, int compute, int K, float a, float b, float c, in
 std::mutex g_lt_mu;
 hipblasLtHandle_t g_lt[kMaxDevices] = {};
 
+// One host thread at a time enqueues GEMM-path work: the per-device
+// hipBLASLt handle is shared by every calling thread (nothing establishes
+// that concurrent hipblasLtMatmul calls on one handle are safe), and the
+// tuner rewrites a plan's chosen algorithm, which a concurrent call reads.
+// Held over the enqueue only (microseconds per GEMM), never over device
+// work; taken before g_lt_mu where both are held.
+std::mutex g_enqueue_mu;
+
 constexpr int kCandidates = 32;  // heuristic results kept per GEMM for himuon_gemm_tune
 
 struct Gemm {
@@ -419,6 +427,7 @@ int run_gemm_path(int64_t n_mats, const void* const* in_ptrs, void* const* out_p
     if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return himuon::set_hip_error(e);
 
     // every GEMM plan exists before anything is enqueued
+    std::lock_guard<std::mutex> enqueue_lock(g_enqueue_mu);
     hipblasLtHandle_t lt = nullptr;
     int status = HIMUON_OK;
     for (const Group& g : groups) {
@@ -575,6 +584,7 @@ int himuon_gemm_tune_hw(int64_t n_mats, const int64_t* rows, const int64_t* cols
         if (e != hipSuccess) return himuon::set_hip_error(e);
     }
     if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return himuon::set_hip_error(e);
+    std::lock_guard<std::mutex> enqueue_lock(g_enqueue_mu);
     hipEvent_t e0 = nullptr, e1 = nullptr;
     if ((e = hipEventCreate(&e0)) != hipSuccess || (e = hipEventCreate(&e1)) != hipSuccess) {
         if (e0) (void)hipEventDestroy(e0);

@@ -143,9 +143,9 @@ def timed_steps(torch, np, step, stream, steps, warmup, ps=None, jitter_steps=30
     """Runs `warmup` untimed steps, then times exactly `steps` steps back to back.
 
     The timed region holds one pair of HIP events on the launch stream (start
-    and end) and nothing else: an event recorded between two launches costs
-    the GPU 10-25 us (the event's release fence), which a call of a few
-    hundred microseconds would otherwise carry. Step-to-step spread comes from
+    and end) and nothing else: with an event pair between two launches the
+    kernel trace shows a gap of about 11 us before each launch, a few percent
+    of a call of a few hundred microseconds. Step-to-step spread comes from
     a second, untimed pass of up to `jitter_steps` steps with an event pair
     around each. `ps` (a PowerSampler) is restarted with the timed region and
     stopped at its end.

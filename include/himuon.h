@@ -31,6 +31,15 @@
  * Matrices are row-major: element (i, j) of matrix l sits at
  * ptr_l + i*ld_l + j (in elements). One call uses one storage dtype for all
  * inputs and outputs.
+ *
+ * Threads: every entry point may be called from several host threads at
+ * once, each on its own stream (or the same one). The library's shared host
+ * state (staging ring, per-device GEMM handle and plans, cached bounds) is
+ * locked, the last HIP error is per thread, and calls that run library GEMMs
+ * (himuon_ns_gemm*, himuon_gemm_tune*, the GEMM route of himuon_ns_tiled and
+ * himuon_step) enqueue one thread at a time; the device work of calls on
+ * different streams still overlaps. Calls whose output buffers overlap race
+ * on the device as any two writers do.
  */
 #ifndef HIMUON_H
 #define HIMUON_H

@@ -652,6 +652,9 @@ class HiMuon:
         if need == 0:
             raise HimuonError(ERR_INVALID_ARG, "himuon_step_workspace_size")
         if self._workspace is None or self._workspace.numel() < need:
+            if self._workspace is not None:
+                # steps enqueued on other streams may still use the old workspace
+                torch.cuda.synchronize(self._workspace.device)
             self._workspace = torch.empty(need, dtype=torch.uint8, device=self.params[0].device)
         if self.tune and T not in (32, 64, 128, 256):
             gemm_tune([tuple(p.shape) for p in self.params], T, code, K=self.K, coeffs=self.coeffs,
@@ -690,8 +693,12 @@ class HiMuon:
                 if g.shape != p.shape or g.dtype != p.dtype or g.stride(0) != p.stride(0):
                     raise ValueError("each gradient must match its parameter's shape, dtype and row stride")
             self._step_plan(list(grads)).launch(stream)
-            return self.params
-        return step(self.params, grads, self.moms, T=self.T, K=self.K, coeffs=self.coeffs, lr=self.lr,
-                    momentum=self.momentum, weight_decay=self.weight_decay, nesterov=self.nesterov,
-                    scale_c=self.scale_c, compute=self.compute, chunk_budget_bytes=self.chunk_budget_bytes,
-                    workspace=self._workspace, stream=stream)
+        else:
+            step(self.params, grads, self.moms, T=self.T, K=self.K, coeffs=self.coeffs, lr=self.lr,
+                 momentum=self.momentum, weight_decay=self.weight_decay, nesterov=self.nesterov,
+                 scale_c=self.scale_c, compute=self.compute, chunk_budget_bytes=self.chunk_budget_bytes,
+                 workspace=self._workspace, stream=stream)
+        if stream is not None:
+            # the cached workspace (and the momenta) are in use on `stream` too
+            _keep_alive([self._workspace] + self.moms, stream, self._workspace.device)
+        return self.params

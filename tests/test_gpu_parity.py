@@ -165,6 +165,30 @@ def test_config5_fp32_K8_every_tile(T):
     check_full(x, y, T, K=8)
 
 
+def test_fp32_K8_worst_tile_over_draws():
+    """The spread of the fp32 path's per-tile error over five more draws of
+    the heavy-tailed 2048x2048 matrix at T = 32, K = 8 (every tile). The
+    worst tile of such a draw sits at the floor of fp32 arithmetic for this
+    map: an emulation of the kernels' fp32 arithmetic puts it between 6e-6
+    and 1.1e-5 depending on a one-ulp change of a single input, and on two of
+    these draws one tile of 4,096 lies above 1e-5. What is asserted here is
+    the distribution (p99 and median, with margin) and a worst tile within
+    twice the bar; the bar itself is asserted on every tile of the fixed
+    draw above."""
+    for seed in range(900, 905):
+        announce(f"2048x2048 fp32 Student-t K=8 T=32, seed {seed}, all tiles")
+        x = workloads.student_t(2048, 2048, seed, "f32", DEV)
+        (y,) = run([x], 32, K=8)
+        e = tile_errors(to_f64(y), oracle.ns_tiled(to_f64(x), 32, 8, *COEF32), 32)
+        p99, p50 = np.percentile(e, 99), np.median(e)
+        print(f"[gpu-err] seed {seed}: max {e.max():.3e} p99 {p99:.3e} p50 {p50:.3e} "
+              f"tiles over 1e-5: {int((e > 1e-5).sum())}", flush=True)
+        assert np.all(np.isfinite(e))
+        assert p99 <= 4e-6 and p50 <= 1.5e-6, (seed, p99, p50)
+        assert e.max() <= 2e-5, (seed, e.max())
+        assert int((e > TOL[torch.float32]).sum()) <= 2, seed
+
+
 # ------------------------------------------------------------- edge cases
 
 RAGGED = [(100, 300), (257, 129), (33, 4096), (1, 1), (5, 700), (130, 2), (64, 64)]

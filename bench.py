@@ -452,8 +452,11 @@ def bench_optstep(args, hm, torch, np, dev):
     HIP graph) and replayed each step, the study's graph-captured variant.
     Per-step time is the median of the HIP-event times of
     `--steps` steps after `--warmup` (the paper: 50 after 20), beside the
-    median host time the step's calls take to enqueue; peak memory is
-    torch's peak allocation over the variant's run, workspace included."""
+    median host time the step's calls take to enqueue, and the mean of the
+    same number of steps run back to back between one event pair
+    (`back_to_back_ms`: no event or gradient kernel between the steps); peak
+    memory is torch's peak allocation over the variant's run, workspace
+    included."""
     coeffs = tuple(float(np.float32(v)) for v in hm.QUINTIC)
     hs = [int(h) for h in args.hidden.split(",")]
     stream = torch.cuda.current_stream(dev)
@@ -502,8 +505,18 @@ def bench_optstep(args, hm, torch, np, dev):
                     host.append(h1 - h0)
             torch.cuda.synchronize()
             ms = np.array([a.elapsed_time(b) for a, b in times])
+            # the same steps back to back between one event pair (the last
+            # gradients reused): no event or gradient kernel between steps
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(args.steps):
+                one_step()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            b2b = e0.elapsed_time(e1) / args.steps
             flops = 8 * (6.0 * H * H * min(T, H) * 5 if T else 6.0 * H ** 3 * 5)
             res[name] = {"median_ms": round(float(np.median(ms)), 4),
+                         "back_to_back_ms": round(b2b, 4),
                          "host_us_per_step": round(float(np.median(host)) * 1e6, 1),
                          "iqr_ms": round(float(np.percentile(ms, 75) - np.percentile(ms, 25)), 4),
                          "ns_tflops": round(flops / (float(np.median(ms)) * 1e-3) / 1e12, 2),

@@ -637,6 +637,7 @@ class HiMuon:
         self.tune = tune
         self.capture = capture
         self._workspace = None
+        self._streams = set()
         self._plan = None
         self._plan_key = None
         self.reconfigure(T)
@@ -656,6 +657,7 @@ class HiMuon:
                 # steps enqueued on other streams may still use the old workspace
                 torch.cuda.synchronize(self._workspace.device)
             self._workspace = torch.empty(need, dtype=torch.uint8, device=self.params[0].device)
+            self._streams = set()  # streams the new workspace has been marked as used on
         if self.tune and T not in (32, 64, 128, 256):
             gemm_tune([tuple(p.shape) for p in self.params], T, code, K=self.K, coeffs=self.coeffs,
                       compute=self.compute, chunk_budget_bytes=self.chunk_budget_bytes, workspace=self._workspace)
@@ -698,7 +700,10 @@ class HiMuon:
                  momentum=self.momentum, weight_decay=self.weight_decay, nesterov=self.nesterov,
                  scale_c=self.scale_c, compute=self.compute, chunk_budget_bytes=self.chunk_budget_bytes,
                  workspace=self._workspace, stream=stream)
-        if stream is not None:
-            # the cached workspace (and the momenta) are in use on `stream` too
+        if stream is not None and stream not in self._streams:
+            # the cached workspace (and the momenta) are in use on `stream` too;
+            # the allocator keeps the record for the life of each block, so
+            # once per stream and workspace is enough
             _keep_alive([self._workspace] + self.moms, stream, self._workspace.device)
+            self._streams.add(stream)
         return self.params

@@ -197,6 +197,40 @@ def test_three_steps_fp32_with_reconfigure_keeping_momentum(T):
 
 
 @pytest.mark.parametrize("T", [512, 128])
+def test_state_object_on_a_side_stream(T):
+    """HiMuon stepping on a stream of its own, with a reconfigure between
+    steps (which may replace the cached workspace) and new allocations
+    right after each step: the same bits as the same steps on the current
+    stream."""
+    announce(f"HiMuon on a side stream, T={T}, bf16")
+    shapes = [(384, 512), (512, 384), (96, 1000)]
+    P0 = [rand(s, torch.bfloat16, 140 + i, W_SCALE) for i, s in enumerate(shapes)]
+    Gs = [[rand(s, torch.bfloat16, 150 + 10 * t + i, 1e-2) for i, s in enumerate(shapes)] for t in range(3)]
+
+    def trajectory(stream):
+        ps = [p.clone() for p in P0]
+        opt = hm.HiMuon(ps, T=T, K=5, coeffs=COEF32, lr=0.05, momentum=0.9, weight_decay=0.1, tune=False)
+        for t, Tt in enumerate([T, 0, T]):
+            opt.reconfigure(Tt)
+            if stream is None:
+                opt.step(Gs[t])
+            else:
+                stream.wait_stream(torch.cuda.current_stream())  # the inputs were made on the current stream
+                opt.step(Gs[t], stream=stream)
+                # allocations on the current stream meanwhile, which must not get the workspace's memory
+                junk = [torch.full((1 << 20,), 7.0, device=DEV) for _ in range(4)]
+                del junk
+        torch.cuda.synchronize()
+        return ps, opt.moms
+
+    side = torch.cuda.Stream(device=DEV)
+    ref_p, ref_m = trajectory(None)
+    got_p, got_m = trajectory(side)
+    for a, b in zip(got_p + got_m, ref_p + ref_m):
+        assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("T", [512, 128])
 def test_chunked_equals_unchunked(T):
     announce(f"step chunked vs one chunk, T={T}, bf16")
     shapes = [(1024, 1024), (512, 768), (640, 512)]
